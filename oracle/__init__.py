@@ -1,0 +1,232 @@
+"""CPU oracle for the local-shard SBP linear layer.
+
+TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the
+benchmark's ``cpu_baseline`` leg may import this package; the product path
+(``paper_2301_06813_amd``) never does, and this package imports nothing from
+it. The arithmetic lives in ``oracle.c`` (plain C, fp64 accumulation); this
+module only builds it, loads it and marshals numpy arrays.
+
+What it computes follows AutoDDL Sec. 4.2 (the SBP matrix multiplication and
+its local matmul) and Sec. 4.3 (a broadcast weight receives partial-sum
+gradients); see the header of ``oracle.c``.
+
+Parity status: pinned by ``tests/test_oracle_pins.py`` (reassembly
+invariant against brute-force global products, exact integer inputs, closed
+forms, the p = 1 textbook case, Listing 1 shard shapes, bf16 rounding against
+a library conversion). ``orc_round_bf16`` does not model bf16 subnormals
+(never produced by the tests): parity unpinned below 2^-126.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+# signature ids (the oracle's own numbering)
+DP, COL, KS = 0, 1, 2
+SIGNATURES = {"DP": DP, "COL": COL, "KS": KS}
+# operation ids
+FWD, BWD_DATA, BWD_WEIGHT = 0, 1, 2
+OPS = {"fwd": FWD, "bwd_data": BWD_DATA, "bwd_weight": BWD_WEIGHT}
+# state kinds
+SPLIT, BCAST, PARTIAL = 0, 1, 2
+# input encodings
+IN_BF16, IN_F32 = 0, 1
+
+
+def build(force: bool = False, src: str = SRC, out: str = LIB) -> str:
+    """Compile oracle.c (or a given copy of it) into a shared library with gcc.
+
+    OpenMP parallelises over output elements only; -ffp-contract=off keeps
+    every product and sum a separately rounded fp64 operation.
+    """
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(src):
+        tmp = out + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+               "-std=c11", "-o", tmp, src, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, out)
+    return out
+
+
+class Oracle:
+    """Handle on one build of the oracle library (the default build, or a
+    mutated copy that a test compiles to check that the pins catch it)."""
+
+    def __init__(self, path: str):
+        lib = ctypes.CDLL(path)
+        i64, i32 = ctypes.c_int64, ctypes.c_int32
+        p64 = ctypes.POINTER(ctypes.c_int64)
+        p32 = ctypes.POINTER(ctypes.c_int32)
+        vp = ctypes.c_void_p
+        lib.orc_split.argtypes = [i64, i64, i64, p64, p64]
+        lib.orc_split.restype = None
+        lib.orc_tags.argtypes = [ctypes.c_int, p32, p32]
+        lib.orc_tags.restype = ctypes.c_int
+        lib.orc_out_shape.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64, i64, i64,
+                                      p64, p64, p32, p32]
+        lib.orc_out_shape.restype = ctypes.c_int
+        lib.orc_linear_block.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, i64, i64, i64,
+                                         i64, i64, vp, vp, vp, i64, i64, i64, i64, vp]
+        lib.orc_linear_block.restype = ctypes.c_int
+        lib.orc_linear_samples.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, i64, i64, i64,
+                                           i64, i64, vp, vp, vp, i64, vp, vp, vp]
+        lib.orc_linear_samples.restype = ctypes.c_int
+        lib.orc_round_bf16.argtypes = [vp, vp, i64]
+        lib.orc_round_bf16.restype = None
+        self.lib = lib
+
+    def split(self, D: int, p: int, r: int) -> tuple[int, int]:
+        """(offset, length) of rank r's contiguous block of an extent D over p ranks."""
+        off, ln = ctypes.c_int64(), ctypes.c_int64()
+        self.lib.orc_split(D, p, r, ctypes.byref(off), ctypes.byref(ln))
+        return off.value, ln.value
+
+    def tags(self, sig: int) -> list[tuple[int, int]]:
+        """(kind, axis) of X, W, Y, dY, dX, dW under signature sig."""
+        k = (ctypes.c_int32 * 6)()
+        a = (ctypes.c_int32 * 6)()
+        if self.lib.orc_tags(sig, k, a) != 0:
+            raise ValueError("unknown signature %r" % sig)
+        return [(k[t], a[t]) for t in range(6)]
+
+    def out_shape(self, sig: int, op: int, M: int, K: int, N: int, p: int, r: int):
+        """(rows, cols, kind, axis) of rank r's output of op under sig."""
+        rows, cols = ctypes.c_int64(), ctypes.c_int64()
+        kind, axis = ctypes.c_int32(), ctypes.c_int32()
+        rc = self.lib.orc_out_shape(sig, op, M, K, N, p, r, ctypes.byref(rows),
+                                    ctypes.byref(cols), ctypes.byref(kind), ctypes.byref(axis))
+        if rc != 0:
+            raise ValueError("bad oracle arguments")
+        return rows.value, cols.value, kind.value, axis.value
+
+    def linear(self, sig: int, op: int, X, W, dY, p: int, r: int, rows=None, cols=None,
+               M=None, K=None, N=None) -> np.ndarray:
+        """Rank r's output of op under sig, as fp64.
+
+        X (M x K), W (K x N) and dY (M x N) are the global tensors: uint16 bf16
+        bit patterns or float32, row-major. Pass None for a tensor the op does
+        not read, together with the global sizes M, K, N. rows/cols select a
+        block (Python ranges with step 1) of the local output.
+        """
+        (X, W, dY), enc = _prep(X, W, dY)
+        M, K, N = _dims(X, W, dY, M, K, N)
+        orow, ocol, _, _ = self.out_shape(sig, op, M, K, N, p, r)
+        rows = range(orow) if rows is None else rows
+        cols = range(ocol) if cols is None else cols
+        out = np.empty((len(rows), len(cols)), dtype=np.float64)
+        rc = self.lib.orc_linear_block(sig, op, enc, M, K, N, p, r, _ptr(X), _ptr(W), _ptr(dY),
+                                       rows.start, rows.start + len(rows),
+                                       cols.start, cols.start + len(cols), out.ctypes.data)
+        if rc != 0:
+            raise ValueError("bad oracle arguments")
+        return out
+
+    def linear_samples(self, sig: int, op: int, X, W, dY, p: int, r: int, ii, jj,
+                       M=None, K=None, N=None) -> np.ndarray:
+        """Single elements (ii[s], jj[s]) of rank r's output of op under sig, as fp64."""
+        (X, W, dY), enc = _prep(X, W, dY)
+        M, K, N = _dims(X, W, dY, M, K, N)
+        ii = np.ascontiguousarray(ii, dtype=np.int64)
+        jj = np.ascontiguousarray(jj, dtype=np.int64)
+        out = np.empty(ii.shape[0], dtype=np.float64)
+        rc = self.lib.orc_linear_samples(sig, op, enc, M, K, N, p, r, _ptr(X), _ptr(W),
+                                         _ptr(dY), ii.shape[0], ii.ctypes.data,
+                                         jj.ctypes.data, out.ctypes.data)
+        if rc != 0:
+            raise ValueError("bad oracle arguments")
+        return out
+
+    def round_bf16(self, x) -> np.ndarray:
+        """Round fp64 values to bf16 (nearest, ties to even); returns uint16 bit patterns."""
+        x = np.ascontiguousarray(x, dtype=np.float64)
+        out = np.empty(x.shape, dtype=np.uint16)
+        self.lib.orc_round_bf16(x.ctypes.data, out.ctypes.data, x.size)
+        return out
+
+
+def _encode(a):
+    """Return (contiguous array, encoding) for bf16 bit patterns (uint16) or fp32."""
+    if a is None:
+        return None, None
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return a, IN_BF16
+    if a.dtype == np.float32:
+        return a, IN_F32
+    raise TypeError("oracle inputs are uint16 bf16 bit patterns or float32, got %s" % a.dtype)
+
+
+def _prep(X, W, dY):
+    arrs, encs = [], set()
+    for a in (X, W, dY):
+        c, e = _encode(a)
+        arrs.append(c)
+        if e is not None:
+            encs.add(e)
+    if len(encs) != 1:
+        raise TypeError("oracle inputs must share one encoding")
+    return arrs, encs.pop()
+
+
+def _dims(X, W, dY, M, K, N):
+    if X is not None:
+        M, K = X.shape
+    if W is not None:
+        K, N = W.shape
+    if dY is not None:
+        M, N = dY.shape
+    return M, K, N
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+_default = None
+
+
+def default() -> Oracle:
+    """The oracle built from oracle.c (built on first use if missing)."""
+    global _default
+    if _default is None:
+        if not os.path.exists(LIB):
+            build()
+        _default = Oracle(LIB)
+    return _default
+
+
+def split(D, p, r):
+    return default().split(D, p, r)
+
+
+def tags(sig):
+    return default().tags(sig)
+
+
+def out_shape(sig, op, M, K, N, p, r):
+    return default().out_shape(sig, op, M, K, N, p, r)
+
+
+def linear(sig, op, X, W, dY, p, r, rows=None, cols=None, M=None, K=None, N=None):
+    return default().linear(sig, op, X, W, dY, p, r, rows, cols, M, K, N)
+
+
+def linear_samples(sig, op, X, W, dY, p, r, ii, jj, M=None, K=None, N=None):
+    return default().linear_samples(sig, op, X, W, dY, p, r, ii, jj, M, K, N)
+
+
+def round_bf16(x) -> np.ndarray:
+    return default().round_bf16(x)
+
+
+def bf16_to_f64(bits) -> np.ndarray:
+    """Decode uint16 bf16 bit patterns exactly."""
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
