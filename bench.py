@@ -1,0 +1,274 @@
+#!/usr/bin/env python3
+"""Benchmark: one per-rank training step of SBP linear layers on one MI355X.
+
+Workload (the step): the 96 linear layers of a 24-layer Transformer (hidden
+1024, ffn 4096, 16 heads, 8192 global tokens, p = 8 devices), each with its
+own seeded SBP signature from {DP (S(0),B)->S(0), COL (B,S(1))->S(1),
+KS (S(1),S(0))->P}; rank 0's share runs: every forward in layer order, then
+every backward-data and backward-weight product in reverse order, 288
+launches of the library's kernels on one HIP stream. Inputs are seeded
+synthetic tensors resident in HBM (the global X, W and dY of every linear;
+the library reads rank 0's shares in place).
+
+`value` is whole-step TFLOP/s (sum of 2 m n k over the 288 local products,
+divided by the measured step time); the step is replayed from a HIP graph
+captured once after warm-up. Per-kernel durations come from HIP events
+around every launch in a separate eager pass over the same steps.
+
+Prints one JSON line. Only one GPU: --gpus above 1 exits with a message.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 2516.6      # 256 CU x 2.4 GHz x 4096 flop/clk (dense)
+HBM_PEAK_GBS = 8000.0
+RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+OPS = ("fwd", "bwd_data", "bwd_weight")
+ORIENT = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2}
+KMAJ = {"fwd": ("true", "false"), "bwd_data": ("true", "true"), "bwd_weight": ("false", "false")}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Step:
+    """Rank r's launches of one workload, with all buffers preallocated."""
+
+    def __init__(self, wl, r, device="cuda"):
+        import torch
+        from paper_2301_06813_amd import linear, sbp, workloads
+        self.sbp = sbp
+        self.calls = []       # (fn, args...) in launch order
+        self.meta = []        # per launch: dict(linear, sig, op, m, n, k, flops, bytes, kernel)
+        self.keep = []
+        fwd, bwd = [], []
+        for lin in wl.linears:
+            X, W, dY = workloads.make_tensors(lin, wl.dtype, device)
+            L = linear.layouts(lin.sig, wl.p, r)
+            self.keep += [X, W, dY]
+            vX, vW, vdY = sbp.view(X), sbp.view(W), sbp.view(dY)
+            for op in OPS:
+                out = linear.alloc_out(op, lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype, device)
+                self.keep.append(out)
+                vo = sbp.view(out, sbp.SBP_LOCAL)
+                if op == "fwd":
+                    call = ("sbp_linear_fwd", vX, L["x"], vW, L["w"], vo)
+                    m, n = out.shape
+                    k = sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols
+                elif op == "bwd_data":
+                    call = ("sbp_linear_bwd_data", vdY, L["dy"], vW, L["w"], vo)
+                    m, n = out.shape
+                    k = sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols
+                else:
+                    call = ("sbp_linear_bwd_weight", vX, L["x"], vdY, L["dy"], vo)
+                    m, n = out.shape
+                    k = sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows
+                ob = 4 if out.dtype == torch.float32 else 2
+                tm, tn, sp = sbp.sbp_plan(ORIENT[op], m, n, k, sbp.SBP_BF16,
+                                          sbp.SBP_F32 if ob == 4 else sbp.SBP_BF16)
+                kern = "gemm_bf16_kernel<%d, %d, %s, %s, %s>" % (
+                    tm, tn, KMAJ[op][0], KMAJ[op][1], "true" if ob == 4 else "false")
+                meta = dict(linear=lin.name, sig=lin.sig, op=op, m=m, n=n, k=k,
+                            flops=2.0 * m * n * k, bytes=2.0 * (m * k + k * n) + ob * m * n,
+                            kernel=kern, splits=sp)
+                (fwd if op == "fwd" else bwd).append((call, meta))
+        order = fwd + [c for i in range(len(bwd) // 2 - 1, -1, -1) for c in bwd[2 * i:2 * i + 2]]
+        for call, meta in order:
+            self.calls.append(call)
+            self.meta.append(meta)
+        self.flops = sum(m["flops"] for m in self.meta)
+        import ctypes
+        L_ = sbp.lib()
+        self._fns = [getattr(L_, c[0]) for c in self.calls]
+        self._args = [tuple(ctypes.byref(a) for a in c[1:]) for c in self.calls]
+        self._lo = sbp.sbp_layout_t()
+        self._lo_ref = ctypes.byref(self._lo)
+
+    def launch_all(self, stream, events=None):
+        import ctypes
+        s = ctypes.c_void_p(stream)
+        for i, (fn, a) in enumerate(zip(self._fns, self._args)):
+            if events is not None:
+                events[i][0].record()
+            rc = fn(*a, self._lo_ref, s)
+            if rc != 0:
+                raise self.sbp.SbpError(rc, self.sbp.sbp_last_hip_error())
+            if events is not None:
+                events[i][1].record()
+
+
+def cpu_baseline(wl, seconds):
+    """The oracle on a bounded sample of the same step: leading output rows of
+    every product of layer 0's four linears, timed on the host cores."""
+    import numpy as np
+    import oracle
+    from paper_2301_06813_amd import inputs, workloads
+    sig_id = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS}
+    op_id = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
+    oracle.build()
+    lins = wl.linears[:4]
+    host = []
+    for lin in lins:
+        X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
+        host.append(tuple(inputs.host_bits(t) for t in (X, W, dY)))
+        del X, W, dY
+
+    def run(nrows):
+        fl, t0 = 0.0, time.perf_counter()
+        for lin, (Xh, Wh, dYh) in zip(lins, host):
+            for op in OPS:
+                rows, cols, _, _ = oracle.out_shape(sig_id[lin.sig], op_id[op], lin.M, lin.K,
+                                                    lin.N, wl.p, 0)
+                nr = min(nrows, rows)
+                oracle.linear(sig_id[lin.sig], op_id[op], Xh, Wh, dYh, wl.p, 0,
+                              rows=range(0, nr))
+                # every local product of a linear is 2 M K N / p flops
+                fl += lin.flops_per_op(wl.p) * nr / rows
+        return fl, time.perf_counter() - t0
+
+    fl1, t1 = run(1)
+    nrows = max(1, int(seconds / max(t1, 1e-6)))
+    fl, t = run(nrows)
+    cores = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    return {"value": fl / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": "first %d output rows of each of the 12 local products of layer 0 "
+                      "(qkv/out/fc1/fc2 x fwd/bwd_data/bwd_weight), rank 0; %.3g GFLOP in %.1f s"
+                      % (nrows, fl / 1e9, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="time eager launches, not a graph")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build measures rank r's local products on a "
+              "single MI355X and has no multi-GPU path (--gpus %d requested)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2301_06813_amd import sbp, workloads
+    sbp.lib()
+    torch.cuda.set_device(0)
+    wl = workloads.transformer_step()
+    log("building step: %d linears, p=%d, rank 0" % (len(wl.linears), wl.p))
+    step = Step(wl, 0)
+    stream = torch.cuda.Stream()
+    sid = stream.cuda_stream
+    torch.cuda.synchronize()
+    log("warmup %d" % args.warmup)
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            step.launch_all(sid)
+    torch.cuda.synchronize()
+
+    graph = None
+    if not args.eager:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            step.launch_all(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        for _ in range(2):
+            graph.replay()
+        torch.cuda.synchronize()
+
+    log("timing %d steps (%s)" % (args.steps, "eager" if args.eager else "graph"))
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        t0.record()
+        for _ in range(args.steps):
+            if graph is not None:
+                graph.replay()
+            else:
+                step.launch_all(sid)
+        t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    tflops = step.flops / (ms * 1e-3) / 1e12
+
+    # per-kernel durations: HIP events around every launch, on the launch stream
+    log("per-kernel event pass")
+    n = len(step.calls)
+    ksteps = max(1, min(args.steps, 5))
+    durs = [[] for _ in range(n)]
+    with torch.cuda.stream(stream):
+        for _ in range(ksteps):
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(n)]
+            step.launch_all(sid, ev)
+            torch.cuda.synchronize()
+            for i in range(n):
+                durs[i].append(ev[i][0].elapsed_time(ev[i][1]) * 1e-3)
+    avg = [sum(d) / len(d) for d in durs]
+    by_kernel = collections.defaultdict(lambda: [0.0, 0.0, 0.0, 0])
+    by_sig = collections.defaultdict(lambda: [0.0, 0.0])
+    for m, t in zip(step.meta, avg):
+        b = by_kernel[m["kernel"]]
+        b[0] += t
+        b[1] += m["flops"]
+        b[2] += m["bytes"]
+        b[3] += 1
+        by_sig[m["sig"]][0] += t
+        by_sig[m["sig"]][1] += m["flops"]
+    dom, (kt, kf, kb, kn) = max(by_kernel.items(), key=lambda kv: kv[1][0])
+    intensity = kf / kb
+    if intensity >= RIDGE:
+        roof = {"bound": "mfma", "achieved": kf / kt / 1e12, "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": kb / kt / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = dom
+    roof["launches_per_step"] = kn
+    roof["avg_launch_us"] = kt / kn * 1e6
+    roof["algorithmic_intensity_flop_per_byte"] = intensity
+
+    out = {
+        "metric": "local-shard GEMM TFLOP/s (fwd+bwd) per SBP signature; % of bf16 MFMA peak",
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations/gradients, N(0,1/K) weights)",
+        "config": {"workload": wl.name, "layers": 24, "hidden": 1024, "ffn": 4096,
+                   "heads": 16, "tokens": 8192, "p": wl.p, "rank": 0,
+                   "gemms_per_step": n, "gflop_per_step": step.flops / 1e9,
+                   "signatures": dict(collections.Counter(l.sig for l in wl.linears)),
+                   "mode": "eager" if args.eager else "hip_graph"},
+        "pct_of_bf16_peak": 100.0 * tflops / BF16_PEAK_TFLOPS,
+        "per_signature_tflops": {s: v[1] / v[0] / 1e12 for s, v in sorted(by_sig.items())},
+        "kernel_time_sum_ms": sum(avg) * 1e3,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle), ~%.0f s" % args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,188 @@
+/*
+ * sbp.h -- C ABI of the local-shard SBP linear layer for MI355X (gfx950).
+ *
+ * A linear layer Y = X W under an SBP (Split / Broadcast / Partial-sum)
+ * signature runs, on each device, a local matrix product of that device's
+ * shares of its operands (AutoDDL, Sec. 4.2, "Distributed Matrix
+ * Multiplication based on SBP": the local matmul of the 3-D SBP rule).
+ * This library runs rank r's local forward and backward products on one GPU
+ * and tags each output with its SBP state.
+ *
+ * Supported signatures (the 1-D factors of the Sec. 4.2 rule; a broadcast
+ * operand's gradient is a partial sum, Sec. 4.3 "Sources of Communication"):
+ *
+ *   name  X      W      -> Y     | dY     dX     dW
+ *   DP    S(0)   B      -> S(0)  | S(0)   S(0)   P
+ *   COL   B      S(1)   -> S(1)  | S(1)   P      S(1)
+ *   KS    S(1)   S(0)   -> P     | B      S(1)   S(0)
+ *
+ * Conventions (all functions):
+ *   - Matrices are row-major with a leading dimension ld (elements between
+ *     the starts of consecutive rows, ld >= cols). X is M x K, W is K x N,
+ *     dY and Y are M x N, as global tensors.
+ *   - Split(i) over p devices gives rank r the contiguous block
+ *     [off, off + len) of axis i with len = D/p + (r < D%p), off =
+ *     r*(D/p) + min(r, D%p) (the paper does not fix uneven splits; this is
+ *     the balanced reading). Broadcast and Partial-sum shares span the full
+ *     extent.
+ *   - Every pointer in an sbp_view_t is a DEVICE pointer on the current HIP
+ *     device. The caller owns every buffer; the library never copies inputs.
+ *   - Return value: SBP_OK (0) or a negative SBP_ERR_* code. Every check
+ *     except SBP_ERR_HIP happens on the host before any HIP call, so a
+ *     rejected call has no effect on the device.
+ *   - Compute calls are asynchronous on the given stream (0 = the null
+ *     stream) and never synchronise. Inputs must stay valid, and outputs
+ *     untouched, until the stream has run the call.
+ *   - Thread safety: calls on different host threads are safe. Calls that
+ *     pick the split-reduction path use a workspace that the library keeps
+ *     per (device, stream); two calls on the same stream are ordered by the
+ *     stream, so they never share it concurrently.
+ */
+#ifndef SBP_H
+#define SBP_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ codes --- */
+enum {
+    SBP_OK = 0,
+    SBP_ERR_NULL = -1,      /* a required pointer is NULL                       */
+    SBP_ERR_LAYOUT = -2,    /* p < 1, r outside [0,p), bad kind/axis, or layouts
+                               of one call disagree on p or r                    */
+    SBP_ERR_SIGNATURE = -3, /* the input states form no supported signature     */
+    SBP_ERR_SHAPE = -4,     /* inner dimensions disagree, ld < cols, a negative
+                               or > 2^31-1 extent, or the output view is not the
+                               local output shape                               */
+    SBP_ERR_DTYPE = -5,     /* unknown dtype, inputs of mixed dtype, a
+                               Partial-sum output that is not fp32, or a bf16
+                               output of fp32 inputs                            */
+    SBP_ERR_ALIAS = -6,     /* the output's memory overlaps an input's          */
+    SBP_ERR_ALIGN = -7,     /* a data pointer is not aligned to its element size */
+    SBP_ERR_HIP = -8        /* a HIP call failed; see sbp_last_hip_error()      */
+};
+
+/* ------------------------------------------------------------ types --- */
+typedef enum { SBP_SPLIT = 0, SBP_BROADCAST = 1, SBP_PARTIAL = 2 } sbp_kind_t;
+
+/* SBP state of a tensor on a 1-D mesh of p devices, seen from rank r.
+ * axis is 0 or 1 for SBP_SPLIT and -1 otherwise. */
+typedef struct {
+    int32_t kind;
+    int32_t axis;
+    int32_t p;
+    int32_t r;
+} sbp_layout_t;
+
+typedef enum { SBP_BF16 = 0, SBP_F32 = 1 } sbp_dtype_t;
+
+/* SBP_GLOBAL: the view spans the whole global tensor and the library selects
+ * rank r's share inside it (a strided sub-view, never a copy).
+ * SBP_LOCAL: the view is exactly rank r's share. */
+typedef enum { SBP_GLOBAL = 0, SBP_LOCAL = 1 } sbp_scope_t;
+
+/* A strided 2-D view: element (i, j) is at data + i*ld + j (elements). */
+typedef struct {
+    void *data;
+    int64_t rows;
+    int64_t cols;
+    int64_t ld;
+    int32_t dtype; /* sbp_dtype_t */
+    int32_t scope; /* sbp_scope_t; ignored for outputs, which are always local */
+} sbp_view_t;
+
+/* Rank r's share of a tensor: rows [row_off, row_off+rows) x cols
+ * [col_off, col_off+cols) of the global tensor. */
+typedef struct {
+    int64_t row_off;
+    int64_t col_off;
+    int64_t rows;
+    int64_t cols;
+} sbp_shard_t;
+
+/* ------------------------------------------------------- host logic --- */
+
+/* Rank l->r's share of a rows x cols tensor in state *l (Sec. 4.1: Split,
+ * Broadcast and Partial-sum states; Fig. 5). Pure host function.
+ * Errors: SBP_ERR_NULL, SBP_ERR_LAYOUT, SBP_ERR_SHAPE (negative extent). */
+int sbp_shard_index(const sbp_layout_t *l, int64_t rows, int64_t cols,
+                    sbp_shard_t *out);
+
+/* Resolves the signature of Y = X W from the states of X and W (Sec. 4.2)
+ * and writes the states of Y, dY, dX and dW (Sec. 4.3: a broadcast operand's
+ * gradient is a partial sum; a split operand's gradient is split the same
+ * way). Any of y, dy, dx, dw may be NULL. Pure host function.
+ * Errors: SBP_ERR_NULL (x or w), SBP_ERR_LAYOUT, SBP_ERR_SIGNATURE. */
+int sbp_signature(const sbp_layout_t *x, const sbp_layout_t *w,
+                  sbp_layout_t *y, sbp_layout_t *dy, sbp_layout_t *dx,
+                  sbp_layout_t *dw);
+
+/* ----------------------------------------------------- device compute --- */
+
+/* Forward local matmul Y_r = X_r W_r (Sec. 4.2, "local matmul").
+ * X: M x K (or rank r's share), state *lx; W: K x N (or share), state *lw.
+ * Y: rank r's local output, state written to *ly_out (may be NULL):
+ *    DP m_r x N, COL M x n_r, KS M x N (Partial-sum, must be fp32).
+ * Inputs bf16 or fp32 (same dtype); Y is fp32, or bf16 for bf16 inputs and
+ * a Split/Broadcast output (rounded to nearest even from the fp32
+ * accumulator). */
+int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx,
+                   const sbp_view_t *W, const sbp_layout_t *lw, sbp_view_t *Y,
+                   sbp_layout_t *ly_out, hipStream_t stream);
+
+/* Backward-data local matmul dX_r = dY_r W_r^T (Sec. 4.2: the redistributions
+ * of the forward path have backward counterparts; Sec. 4.3).
+ * dY: state *ldy (S(0) for DP, S(1) for COL, B for KS); W: state *lw.
+ * dX: rank r's local output, state to *ldx_out: DP m_r x K (S(0)),
+ *     COL M x K (Partial-sum, fp32), KS M x k_r (S(1)). */
+int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy,
+                        const sbp_view_t *W, const sbp_layout_t *lw,
+                        sbp_view_t *dX, sbp_layout_t *ldx_out,
+                        hipStream_t stream);
+
+/* Backward-weight local matmul dW_r = X_r^T dY_r (Sec. 4.3: a broadcast
+ * weight receives partial-sum gradients).
+ * X: state *lx; dY: state *ldy.
+ * dW: rank r's local output, state to *ldw_out: DP K x N (Partial-sum,
+ *     fp32), COL K x n_r (S(1)), KS k_r x N (S(0)). */
+int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx,
+                          const sbp_view_t *dY, const sbp_layout_t *ldy,
+                          sbp_view_t *dW, sbp_layout_t *ldw_out,
+                          hipStream_t stream);
+
+/* --------------------------------------------------------- utilities --- */
+
+/* Static description of an error code (never NULL). */
+const char *sbp_strerror(int code);
+
+/* hipError_t of the last SBP_ERR_HIP returned on the calling thread
+ * (0 if none). */
+int sbp_last_hip_error(void);
+
+/* Kernel plan the library would use for a local product of m x n outputs
+ * over a reduction of k, for input dtype in_dtype and output dtype out_dtype
+ * and operand orientation op (0 forward, 1 backward-data, 2
+ * backward-weight). Writes the tile rows, tile columns and number of
+ * reduction splits. For benchmarks and tests; pure host function.
+ * Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
+int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype,
+             int32_t out_dtype, int32_t *tile_m, int32_t *tile_n,
+             int32_t *splits);
+
+/* Thread-local override of the plan for subsequent calls on this thread
+ * (tests and tuning): tile_m x tile_n must be one of the compiled bf16 tile
+ * shapes (256x128, 128x256, 128x128, 128x64, 64x128, 64x64) and
+ * splits >= 1; tile_m = 0 clears the override. An override that a call
+ * cannot use (fp32 inputs, or more splits than reduction blocks) is
+ * clamped for that call. Errors: SBP_ERR_SHAPE for an unknown tile shape. */
+int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SBP_H */

@@ -1,0 +1,53 @@
+// gemm.h -- internal interface between the C-ABI host code and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sbpi {
+
+// Operand orientation of the three local products (see gemm_bf16_kernel.h):
+//   FWD         A k-major, B n-major     (Y  = X  W)
+//   BWD_DATA    A k-major, B k-major     (dX = dY W^T)
+//   BWD_WEIGHT  A m-major, B n-major     (dW = X^T dY)
+enum Orient { OR_FWD = 0, OR_BWD_DATA = 1, OR_BWD_WEIGHT = 2 };
+
+// dtype codes match sbp_dtype_t
+enum { DT_BF16 = 0, DT_F32 = 1 };
+
+struct Gemm {
+    int orient;
+    int in_dtype;
+    int out_dtype;
+    const void *A;
+    int64_t lda;
+    const void *B;
+    int64_t ldb;
+    void *C;
+    int64_t ldc;
+    int64_t m, n, k;
+};
+
+struct Plan {
+    int bm, bn;            // output tile
+    int splits;            // reduction splits actually launched
+    int kblk_per_split;    // 64-wide reduction blocks per split
+};
+
+// Workspace the split reduction needs, per (device, stream).
+constexpr size_t WS_FLOATS = size_t(16) << 20;   // 64 MiB of fp32 partials
+constexpr size_t WS_COUNTERS = size_t(1) << 16;  // tile counters
+
+// bf16 planning: heuristic choice of tile and splits (an override may be set
+// per thread through sbp_set_plan_override). Always fits the workspace.
+Plan plan_bf16(const Gemm &g);
+bool tile_supported(int bm, int bn);
+void set_override(int bm, int bn, int splits);   // bm = 0 clears
+
+hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, uint32_t *counters,
+                       hipStream_t s);
+hipError_t launch_f32(const Gemm &g, hipStream_t s);
+hipError_t zero_u32(uint32_t *p, size_t n, hipStream_t s);
+
+}  // namespace sbpi

@@ -1,0 +1,9 @@
+// bf16 GEMM instances for the bwd_data orientation (see gemm_bf16_kernel.h).
+#include "gemm_bf16_launch.h"
+
+namespace sbpi {
+hipError_t launch_bf16_bwd_data(const Gemm &g, const Plan &p, float *ws, uint32_t *counters,
+                               hipStream_t s) {
+    return launch_orient<true, true>(g, p, ws, counters, s);
+}
+}  // namespace sbpi

@@ -1,0 +1,363 @@
+// gemm_bf16_kernel.h -- bf16 MFMA GEMM for the local matmul of an SBP linear
+// layer on CDNA4 (gfx950).
+//
+// Computes C[i][j] = sum_k A(i,k) B(k,j) for an m x n output over a reduction
+// of length k, with fp32 accumulation, where each operand is a strided view
+// read in place:
+//   A_KMAJ:  A(i,k) = A[i*lda + k]   else  A(i,k) = A[k*lda + i]
+//   B_KMAJ:  B(k,j) = B[j*ldb + k]   else  B(k,j) = B[k*ldb + j]
+// The three local products of an SBP linear (AutoDDL Sec. 4.2 local matmul
+// and its backward) are the orientations
+//   forward       Y  = X  W     A k-major,  B n-major
+//   backward-data dX = dY W^T   A k-major,  B k-major
+//   backward-wt   dW = X^T dY   A m-major,  B n-major.
+//
+// Design (one workgroup = 4 waves of 64 lanes = 256 threads):
+//   * Output tile BM x BN, reduction step BK = 64; each wave owns a
+//     (BM/2) x (BN/2) quarter computed with v_mfma_f32_32x32x16_bf16.
+//   * Both operand tiles live in LDS "k-contiguous": one 128-byte row of 64
+//     bf16 reduction values per output row/column, cut into eight 16-byte
+//     chunks whose position is XOR-swizzled by the row index, so that the
+//     16-byte MFMA fragment reads and the tile writes are free of bank
+//     conflicts.
+//   * k-major operands are loaded as 16-byte vectors along k. m/n-major
+//     operands are loaded as 16-byte vectors along m/n, KB rows at a time,
+//     and transposed in registers (16-bit lane packing) before the LDS
+//     write, so both orientations share one LDS layout and one inner loop.
+//   * Register prefetch + two LDS buffers: the global loads of step t+1 are
+//     in flight while step t runs on the MFMA units; one barrier per step.
+//   * Split reduction (splits > 1): each workgroup reduces one k-range and
+//     writes its fp32 partial tile to a workspace; the last workgroup to
+//     finish a tile (an atomic counter per tile) adds the partials in split
+//     order -- deterministic -- and writes the output, then resets the
+//     counter for the next call.
+//   * Workgroup -> tile order is XCD-aware: consecutive workgroup ids go to
+//     different XCDs, so ids are remapped to give each XCD a contiguous run
+//     of tiles (shared A rows / B columns stay in that XCD's L2).
+//   * Edges: any m, n, k (including k = 0, which writes zeros) and any
+//     element alignment. Vector loads are used only where the whole 16-byte
+//     vector is inside the operand and the operand's base and leading
+//     dimension keep it 16-byte aligned (a uniform per-launch flag); other
+//     vectors are assembled from masked element loads.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sbpk {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int BK = 64;          // reduction step (elements)
+constexpr int NT = 256;         // threads per workgroup
+constexpr int ROWB = BK * 2;    // bytes per LDS row
+
+struct GemmArgs {
+    const uint16_t *A;
+    const uint16_t *B;
+    void *C;
+    int64_t lda, ldb, ldc;
+    int32_t m, n, k;
+    int32_t tiles_m, tiles_n;
+    int32_t splits;             // reduction splits (>= 1)
+    int32_t kblk_per_split;     // BK-blocks per split
+    float *ws;                  // split partials: tiles * splits * BM * BN floats
+    uint32_t *counters;         // one per tile, zero between calls
+    int32_t vec_a, vec_b;       // operand base and ld allow aligned 16-byte loads
+};
+
+// Byte offset of 16-byte chunk c (0..7) of LDS row `row`.
+__device__ __forceinline__ uint32_t lds_off(int row, int c) {
+    int sw = (row & 7) ^ ((row >> 3) & 7);
+    return (uint32_t)(row * ROWB + ((c ^ sw) << 4));
+}
+
+// Eight consecutive bf16 of a row starting at p; `valid` of them are inside
+// the operand (<= 0: none). Whole in-bounds vectors use one 16-byte load when
+// the operand's base and leading dimension make it 16-byte aligned (vec).
+__device__ __forceinline__ u32x4 load8(const uint16_t *p, int valid, bool vec) {
+    if (vec && valid >= 8) {
+        return *reinterpret_cast<const u32x4 *>(p);
+    }
+    uint32_t e[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) e[i] = (i < valid) ? (uint32_t)p[i] : 0u;
+    u32x4 v;
+    v[0] = e[0] | (e[1] << 16);
+    v[1] = e[2] | (e[3] << 16);
+    v[2] = e[4] | (e[5] << 16);
+    v[3] = e[6] | (e[7] << 16);
+    return v;
+}
+
+__device__ __forceinline__ uint32_t half16(const u32x4 &v, int c) {
+    uint32_t w = v[c >> 1];
+    return (c & 1) ? (w >> 16) : (w & 0xffffu);
+}
+
+// --------------------------------------------------------------------------
+// Operand tile loaders. A tile covers BMN rows of the output dimension
+// (m for A, n for B) and BK reduction values, starting at (mn0, k0).
+// mn_lim / k_lim are the exclusive bounds of the operand.
+// --------------------------------------------------------------------------
+
+// Storage contiguous along k: element (mn, k) at base[mn*ld + k].
+template <int BMN>
+struct KMajorTile {
+    static constexpr int NV = BMN * BK / 8 / NT;   // 16-byte vectors per thread
+    u32x4 v[NV];
+
+    __device__ __forceinline__ void load(const uint16_t *base, int64_t ld, int mn0,
+                                         int mn_lim, int k0, int k_lim, int tid, bool vec) {
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            int q = i * NT + tid;
+            int row = q >> 3;
+            int kc = q & 7;
+            int mn = mn0 + row;
+            int kk = k0 + kc * 8;
+            int valid = (mn < mn_lim) ? (k_lim - kk) : 0;
+            const uint16_t *p = base + (int64_t)(mn < mn_lim ? mn : 0) * ld + (valid > 0 ? kk : 0);
+            v[i] = load8(p, valid, vec);
+        }
+    }
+
+    __device__ __forceinline__ void store(char *lds, int tid) const {
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            int q = i * NT + tid;
+            int row = q >> 3;
+            int kc = q & 7;
+            *reinterpret_cast<u32x4 *>(lds + lds_off(row, kc)) = v[i];
+        }
+    }
+};
+
+// Storage contiguous along m/n: element (mn, k) at base[k*ld + mn].
+// Each thread owns a KB x 8 block (KB reduction rows x 8 output indices),
+// loaded as KB 16-byte row vectors and written to LDS transposed.
+template <int BMN>
+struct MNMajorTile {
+    static constexpr int KB = BMN * BK / 8 / NT;   // 8, 4 or 2
+    static constexpr int NMB = BMN / 8;            // 8-wide blocks per k-row
+    static_assert(KB == 8 || KB == 4 || KB == 2, "unsupported tile");
+    u32x4 v[KB];
+
+    __device__ __forceinline__ void load(const uint16_t *base, int64_t ld, int mn0,
+                                         int mn_lim, int k0, int k_lim, int tid, bool vec) {
+        int mnb = tid % NMB;
+        int kb = tid / NMB;
+        int mn = mn0 + mnb * 8;
+#pragma unroll
+        for (int r = 0; r < KB; ++r) {
+            int kk = k0 + kb * KB + r;
+            int valid = (kk < k_lim) ? (mn_lim - mn) : 0;
+            const uint16_t *p = base + (int64_t)(kk < k_lim ? kk : 0) * ld + (valid > 0 ? mn : 0);
+            v[r] = load8(p, valid, vec);
+        }
+    }
+
+    __device__ __forceinline__ void store(char *lds, int tid) const {
+        int mnb = tid % NMB;
+        int kb = tid / NMB;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            int row = mnb * 8 + c;
+            if constexpr (KB == 8) {
+                u32x4 w;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    w[q] = half16(v[2 * q], c) | (half16(v[2 * q + 1], c) << 16);
+                *reinterpret_cast<u32x4 *>(lds + lds_off(row, kb)) = w;
+            } else if constexpr (KB == 4) {
+                u32x2 w;
+                w[0] = half16(v[0], c) | (half16(v[1], c) << 16);
+                w[1] = half16(v[2], c) | (half16(v[3], c) << 16);
+                *reinterpret_cast<u32x2 *>(lds + lds_off(row, kb >> 1) + ((kb & 1) << 3)) = w;
+            } else {
+                uint32_t w = half16(v[0], c) | (half16(v[1], c) << 16);
+                *reinterpret_cast<uint32_t *>(lds + lds_off(row, kb >> 2) + ((kb & 3) << 2)) = w;
+            }
+        }
+    }
+};
+
+template <int BMN, bool KMAJ>
+using TileOf = typename std::conditional<KMAJ, KMajorTile<BMN>, MNMajorTile<BMN>>::type;
+
+// Logical tile index of this workgroup: XCD-contiguous runs, see header.
+__device__ __forceinline__ int remap_xcd(int wg, int total) {
+    constexpr int NX = 8;
+    int per = total / NX;
+    int rem = total % NX;
+    int x = wg % NX;
+    int idx = wg / NX;
+    return (x < rem) ? x * (per + 1) + idx : rem * (per + 1) + (x - rem) * per + idx;
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+    __bf16 h = (__bf16)f;   // round to nearest even (v_cvt_pk_bf16_f32)
+    return __builtin_bit_cast(uint16_t, h);
+}
+
+template <int BM, int BN, bool A_KMAJ, bool B_KMAJ, bool OUT_F32>
+__global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
+    constexpr int WM = BM / 2, WN = BN / 2;       // wave tile
+    constexpr int MI = WM / 32, NI = WN / 32;     // 32x32 MFMA blocks per wave
+    constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB;
+    constexpr int STAGE = A_BYTES + B_BYTES;
+    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+    __shared__ int last_flag;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    // ---- which tile and which reduction range
+    const int tiles = g.tiles_m * g.tiles_n;
+    const int L = remap_xcd(blockIdx.x, tiles * g.splits);
+    const int split = L / tiles;
+    const int t = L % tiles;
+    // grouped order: runs of GROUP tile-rows, column-major inside a run
+    constexpr int GROUP = 8;
+    const int grp = t / (GROUP * g.tiles_n);
+    const int first_m = grp * GROUP;
+    const int gsize = min(g.tiles_m - first_m, GROUP);
+    const int tm = first_m + (t % (GROUP * g.tiles_n)) % gsize;
+    const int tn = (t % (GROUP * g.tiles_n)) / gsize;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const int kb_total = (g.k + BK - 1) / BK;
+    const int kb_begin = split * g.kblk_per_split;
+    const int kb_end = min(kb_total, kb_begin + g.kblk_per_split);
+    const int nkb = max(0, kb_end - kb_begin);
+    const int k_lim = min(g.k, kb_end * BK);
+
+    TileOf<BM, A_KMAJ> ta;
+    TileOf<BN, B_KMAJ> tb;
+    const bool va = g.vec_a != 0, vb = g.vec_b != 0;
+
+    f32x16 acc[MI][NI];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    if (nkb > 0) {
+        int k0 = kb_begin * BK;
+        ta.load(g.A, g.lda, m0, g.m, k0, k_lim, tid, va);
+        tb.load(g.B, g.ldb, n0, g.n, k0, k_lim, tid, vb);
+        ta.store(smem, tid);
+        tb.store(smem + A_BYTES, tid);
+        __syncthreads();
+
+        for (int it = 0; it < nkb; ++it) {
+            char *cur = smem + (it & 1) * STAGE;
+            const bool more = (it + 1 < nkb);
+            if (more) {
+                int kn = (kb_begin + it + 1) * BK;
+                ta.load(g.A, g.lda, m0, g.m, kn, k_lim, tid, va);
+                tb.load(g.B, g.ldb, n0, g.n, kn, k_lim, tid, vb);
+            }
+#pragma unroll
+            for (int ks = 0; ks < BK / 16; ++ks) {
+                const int chunk = ks * 2 + (lane >> 5);
+                bf16x8 af[MI], bfr[NI];
+#pragma unroll
+                for (int i = 0; i < MI; ++i) {
+                    int row = wm * WM + i * 32 + (lane & 31);
+                    af[i] = *reinterpret_cast<const bf16x8 *>(cur + lds_off(row, chunk));
+                }
+#pragma unroll
+                for (int j = 0; j < NI; ++j) {
+                    int row = wn * WN + j * 32 + (lane & 31);
+                    bfr[j] = *reinterpret_cast<const bf16x8 *>(cur + A_BYTES + lds_off(row, chunk));
+                }
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            }
+            if (more) {
+                char *nxt = smem + ((it + 1) & 1) * STAGE;
+                ta.store(nxt, tid);
+                tb.store(nxt + A_BYTES, tid);
+            }
+            __syncthreads();
+        }
+    }
+
+    // ---- split reduction: partials to workspace, last workgroup adds them
+    if (g.splits > 1) {
+        constexpr int PER = MI * NI * 16;          // floats per thread
+        const size_t tile_base = (size_t)t * g.splits;
+        float *mine = g.ws + (tile_base + split) * (size_t)(PER * NT);
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+            for (int j = 0; j < NI; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    mine[((i * NI + j) * 16 + r) * NT + tid] = acc[i][j][r];
+        __threadfence();
+        __syncthreads();
+        if (tid == 0) {
+            uint32_t done = atomicAdd(&g.counters[t], 1u);
+            last_flag = (done == (uint32_t)(g.splits - 1));
+        }
+        __syncthreads();
+        if (!last_flag) return;
+        __threadfence();
+        // Sum the partials in split order 0, 1, ..., splits-1 (this
+        // workgroup's own partial is read back too), so the result does not
+        // depend on which workgroup finished last.
+        for (int s = 0; s < g.splits; ++s) {
+            const float *part = g.ws + (tile_base + s) * (size_t)(PER * NT);
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        float v = __builtin_nontemporal_load(&part[((i * NI + j) * 16 + r) * NT + tid]);
+                        acc[i][j][r] = (s == 0) ? v : acc[i][j][r] + v;
+                    }
+        }
+        if (tid == 0) atomicExch(&g.counters[t], 0u);
+    }
+
+    // ---- epilogue: MFMA 32x32 accumulator layout -> row-major C
+    // lane holds column (lane & 31); register r holds row 8*(r/4) + 4*(lane/32) + r%4.
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int col = n0 + wn * WN + j * 32 + (lane & 31);
+            const int rbase = m0 + wm * WM + i * 32 + 4 * (lane >> 5);
+            if (col < g.n) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = rbase + 8 * (r >> 2) + (r & 3);
+                    if (row < g.m) {
+                        if constexpr (OUT_F32) {
+                            float *C = reinterpret_cast<float *>(g.C);
+                            C[(int64_t)row * g.ldc + col] = acc[i][j][r];
+                        } else {
+                            uint16_t *C = reinterpret_cast<uint16_t *>(g.C);
+                            C[(int64_t)row * g.ldc + col] = f32_to_bf16_bits(acc[i][j][r]);
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+}  // namespace sbpk

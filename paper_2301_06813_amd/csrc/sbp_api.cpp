@@ -1,0 +1,403 @@
+// sbp_api.cpp -- the C ABI declared in include/sbp.h.
+//
+// Host-side SBP logic (AutoDDL Sec. 4.1 states, Sec. 4.2 SBP matmul rule,
+// Sec. 4.3 gradient states): layout checks, shard indexing, signature
+// resolution, argument validation, then one kernel launch on the caller's
+// stream. Every validation happens before the first HIP call.
+#include <stdint.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "../../include/sbp.h"
+#include "gemm.h"
+
+namespace {
+
+thread_local int g_last_hip = 0;
+
+enum Sig { SIG_DP = 0, SIG_COL = 1, SIG_KS = 2, SIG_NONE = -1 };
+
+bool is_split(const sbp_layout_t *l, int axis) {
+    return l->kind == SBP_SPLIT && l->axis == axis;
+}
+bool is_bcast(const sbp_layout_t *l) { return l->kind == SBP_BROADCAST; }
+
+int check_layout(const sbp_layout_t *l) {
+    if (!l) return SBP_ERR_NULL;
+    if (l->p < 1 || l->r < 0 || l->r >= l->p) return SBP_ERR_LAYOUT;
+    if (l->kind == SBP_SPLIT) {
+        if (l->axis != 0 && l->axis != 1) return SBP_ERR_LAYOUT;
+    } else if (l->kind == SBP_BROADCAST || l->kind == SBP_PARTIAL) {
+        if (l->axis != -1) return SBP_ERR_LAYOUT;
+    } else {
+        return SBP_ERR_LAYOUT;
+    }
+    return SBP_OK;
+}
+
+int check_pair(const sbp_layout_t *a, const sbp_layout_t *b) {
+    int rc = check_layout(a);
+    if (rc) return rc;
+    rc = check_layout(b);
+    if (rc) return rc;
+    if (a->p != b->p || a->r != b->r) return SBP_ERR_LAYOUT;
+    return SBP_OK;
+}
+
+// Forward rule (Sec. 4.2, 1-D factors): (S0,B)->S0, (B,S1)->S1, (S1,S0)->P.
+Sig sig_from_xw(const sbp_layout_t *x, const sbp_layout_t *w) {
+    if (is_split(x, 0) && is_bcast(w)) return SIG_DP;
+    if (is_bcast(x) && is_split(w, 1)) return SIG_COL;
+    if (is_split(x, 1) && is_split(w, 0)) return SIG_KS;
+    return SIG_NONE;
+}
+// Backward-data inputs: dY takes Y's dual state (S stays S, P becomes B).
+Sig sig_from_dyw(const sbp_layout_t *dy, const sbp_layout_t *w) {
+    if (is_split(dy, 0) && is_bcast(w)) return SIG_DP;
+    if (is_split(dy, 1) && is_split(w, 1)) return SIG_COL;
+    if (is_bcast(dy) && is_split(w, 0)) return SIG_KS;
+    return SIG_NONE;
+}
+Sig sig_from_xdy(const sbp_layout_t *x, const sbp_layout_t *dy) {
+    if (is_split(x, 0) && is_split(dy, 0)) return SIG_DP;
+    if (is_bcast(x) && is_split(dy, 1)) return SIG_COL;
+    if (is_split(x, 1) && is_bcast(dy)) return SIG_KS;
+    return SIG_NONE;
+}
+
+sbp_layout_t mk(int32_t kind, int32_t axis, const sbp_layout_t *like) {
+    sbp_layout_t l;
+    l.kind = kind;
+    l.axis = axis;
+    l.p = like->p;
+    l.r = like->r;
+    return l;
+}
+
+// States of Y, dY, dX, dW for a signature (gradient of S(i) is S(i), of B is
+// P, of P is B; Sec. 4.3 states the broadcast-weight case).
+void states_of(Sig s, const sbp_layout_t *like, sbp_layout_t out[4]) {
+    switch (s) {
+        case SIG_DP:
+            out[0] = mk(SBP_SPLIT, 0, like);
+            out[1] = mk(SBP_SPLIT, 0, like);
+            out[2] = mk(SBP_SPLIT, 0, like);
+            out[3] = mk(SBP_PARTIAL, -1, like);
+            break;
+        case SIG_COL:
+            out[0] = mk(SBP_SPLIT, 1, like);
+            out[1] = mk(SBP_SPLIT, 1, like);
+            out[2] = mk(SBP_PARTIAL, -1, like);
+            out[3] = mk(SBP_SPLIT, 1, like);
+            break;
+        default:
+            out[0] = mk(SBP_PARTIAL, -1, like);
+            out[1] = mk(SBP_BROADCAST, -1, like);
+            out[2] = mk(SBP_SPLIT, 1, like);
+            out[3] = mk(SBP_SPLIT, 0, like);
+            break;
+    }
+}
+
+size_t elsize(int32_t dtype) { return dtype == SBP_F32 ? 4 : 2; }
+
+// A validated local (rank-r) operand.
+struct Local {
+    const char *ptr;
+    int64_t rows, cols, ld;
+    int32_t dtype;
+    bool global;
+    int64_t grows, gcols;   // global extent when the view was global
+};
+
+int check_view_common(const sbp_view_t *v) {
+    if (!v) return SBP_ERR_NULL;
+    if (v->dtype != SBP_BF16 && v->dtype != SBP_F32) return SBP_ERR_DTYPE;
+    if (v->rows < 0 || v->cols < 0 || v->rows > INT32_MAX || v->cols > INT32_MAX)
+        return SBP_ERR_SHAPE;
+    if (v->ld < v->cols || v->ld < 1) return SBP_ERR_SHAPE;
+    if (v->rows > 0 && v->cols > 0) {
+        if (!v->data) return SBP_ERR_NULL;
+        if (reinterpret_cast<uintptr_t>(v->data) % elsize(v->dtype)) return SBP_ERR_ALIGN;
+    }
+    return SBP_OK;
+}
+
+int local_input(const sbp_view_t *v, const sbp_layout_t *l, Local *out) {
+    int rc = check_view_common(v);
+    if (rc) return rc;
+    if (v->scope != SBP_GLOBAL && v->scope != SBP_LOCAL) return SBP_ERR_SHAPE;
+    out->dtype = v->dtype;
+    out->ld = v->ld;
+    out->grows = v->rows;
+    out->gcols = v->cols;
+    out->global = (v->scope == SBP_GLOBAL);
+    if (out->global) {
+        sbp_shard_t s;
+        rc = sbp_shard_index(l, v->rows, v->cols, &s);
+        if (rc) return rc;
+        out->rows = s.rows;
+        out->cols = s.cols;
+        out->ptr = static_cast<const char *>(v->data);
+        if (s.rows > 0 && s.cols > 0)
+            out->ptr += (s.row_off * v->ld + s.col_off) * (int64_t)elsize(v->dtype);
+    } else {
+        out->rows = v->rows;
+        out->cols = v->cols;
+        out->ptr = static_cast<const char *>(v->data);
+    }
+    return SBP_OK;
+}
+
+// [begin, end) bytes a view touches (empty when it has no elements).
+std::pair<uintptr_t, uintptr_t> extent(const void *p, int64_t rows, int64_t cols, int64_t ld,
+                                       int32_t dtype) {
+    if (rows <= 0 || cols <= 0 || !p) return {0, 0};
+    uintptr_t b = reinterpret_cast<uintptr_t>(p);
+    uintptr_t e = b + (uintptr_t)(((rows - 1) * ld + cols) * (int64_t)elsize(dtype));
+    return {b, e};
+}
+
+bool overlaps(std::pair<uintptr_t, uintptr_t> a, std::pair<uintptr_t, uintptr_t> b) {
+    if (a.first == a.second || b.first == b.second) return false;
+    return a.first < b.second && b.first < a.second;
+}
+
+// Output checks shared by the three entry points.
+int check_output(const sbp_view_t *o, int64_t rows, int64_t cols, int32_t in_dtype,
+                 int32_t out_kind, const Local &a, const Local &b) {
+    int rc = check_view_common(o);
+    if (rc) return rc;
+    if (o->rows != rows || o->cols != cols) return SBP_ERR_SHAPE;
+    if (in_dtype == SBP_F32 && o->dtype != SBP_F32) return SBP_ERR_DTYPE;
+    if (out_kind == SBP_PARTIAL && o->dtype != SBP_F32) return SBP_ERR_DTYPE;
+    auto oe = extent(o->data, o->rows, o->cols, o->ld, o->dtype);
+    if (overlaps(oe, extent(a.ptr, a.rows, a.cols, a.ld, a.dtype)) ||
+        overlaps(oe, extent(b.ptr, b.rows, b.cols, b.ld, b.dtype)))
+        return SBP_ERR_ALIAS;
+    return SBP_OK;
+}
+
+// ---------------------------------------------------------------- workspace
+struct Workspace {
+    float *ws = nullptr;
+    uint32_t *counters = nullptr;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+int workspace_for(hipStream_t s, Workspace *out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        g_last_hip = (int)e;
+        return SBP_ERR_HIP;
+    }
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    Workspace &w = g_ws[{dev, s}];
+    if (!w.ws) {
+        e = hipMalloc(&w.ws, sbpi::WS_FLOATS * sizeof(float));
+        if (e == hipSuccess) e = hipMalloc(&w.counters, sbpi::WS_COUNTERS * sizeof(uint32_t));
+        if (e == hipSuccess) e = sbpi::zero_u32(w.counters, sbpi::WS_COUNTERS, s);
+        if (e != hipSuccess) {
+            if (w.ws) (void)hipFree(w.ws);
+            if (w.counters) (void)hipFree(w.counters);
+            w = Workspace{};
+            g_last_hip = (int)e;
+            return SBP_ERR_HIP;
+        }
+    }
+    *out = w;
+    return SBP_OK;
+}
+
+int run(const sbpi::Gemm &g, hipStream_t s) {
+    if (g.m == 0 || g.n == 0) return SBP_OK;
+    hipError_t e;
+    if (g.in_dtype == SBP_F32) {
+        e = sbpi::launch_f32(g, s);
+    } else {
+        sbpi::Plan p = sbpi::plan_bf16(g);
+        Workspace w;
+        if (p.splits > 1) {
+            int rc = workspace_for(s, &w);
+            if (rc) return rc;
+        }
+        e = sbpi::launch_bf16(g, p, w.ws, w.counters, s);
+    }
+    if (e != hipSuccess) {
+        g_last_hip = (int)e;
+        return SBP_ERR_HIP;
+    }
+    return SBP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sbp_shard_index(const sbp_layout_t *l, int64_t rows, int64_t cols, sbp_shard_t *out) {
+    if (!l || !out) return SBP_ERR_NULL;
+    int rc = check_layout(l);
+    if (rc) return rc;
+    if (rows < 0 || cols < 0) return SBP_ERR_SHAPE;
+    sbp_shard_t s{0, 0, rows, cols};
+    if (l->kind == SBP_SPLIT) {
+        const int64_t D = (l->axis == 0) ? rows : cols;
+        const int64_t base = D / l->p, rem = D % l->p;
+        const int64_t len = base + (l->r < rem ? 1 : 0);
+        const int64_t off = (int64_t)l->r * base + (l->r < rem ? l->r : rem);
+        if (l->axis == 0) {
+            s.row_off = off;
+            s.rows = len;
+        } else {
+            s.col_off = off;
+            s.cols = len;
+        }
+    }
+    *out = s;
+    return SBP_OK;
+}
+
+int sbp_signature(const sbp_layout_t *x, const sbp_layout_t *w, sbp_layout_t *y,
+                  sbp_layout_t *dy, sbp_layout_t *dx, sbp_layout_t *dw) {
+    if (!x || !w) return SBP_ERR_NULL;
+    int rc = check_pair(x, w);
+    if (rc) return rc;
+    Sig s = sig_from_xw(x, w);
+    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    sbp_layout_t st[4];
+    states_of(s, x, st);
+    if (y) *y = st[0];
+    if (dy) *dy = st[1];
+    if (dx) *dx = st[2];
+    if (dw) *dw = st[3];
+    return SBP_OK;
+}
+
+int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *W,
+                   const sbp_layout_t *lw, sbp_view_t *Y, sbp_layout_t *ly_out,
+                   hipStream_t stream) {
+    if (!X || !W || !Y || !lx || !lw) return SBP_ERR_NULL;
+    int rc = check_pair(lx, lw);
+    if (rc) return rc;
+    Sig s = sig_from_xw(lx, lw);
+    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    Local x, w;
+    if ((rc = local_input(X, lx, &x))) return rc;
+    if ((rc = local_input(W, lw, &w))) return rc;
+    if (x.dtype != w.dtype) return SBP_ERR_DTYPE;
+    if (x.global && w.global && x.gcols != w.grows) return SBP_ERR_SHAPE;
+    if (x.cols != w.rows) return SBP_ERR_SHAPE;
+    sbp_layout_t st[4];
+    states_of(s, lx, st);
+    if ((rc = check_output(Y, x.rows, w.cols, x.dtype, st[0].kind, x, w))) return rc;
+    sbpi::Gemm g{sbpi::OR_FWD, x.dtype, Y->dtype, x.ptr, x.ld, w.ptr, w.ld,
+                 Y->data, Y->ld, x.rows, w.cols, x.cols};
+    if ((rc = run(g, stream))) return rc;
+    if (ly_out) *ly_out = st[0];
+    return SBP_OK;
+}
+
+int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *W,
+                        const sbp_layout_t *lw, sbp_view_t *dX, sbp_layout_t *ldx_out,
+                        hipStream_t stream) {
+    if (!dY || !W || !dX || !ldy || !lw) return SBP_ERR_NULL;
+    int rc = check_pair(ldy, lw);
+    if (rc) return rc;
+    Sig s = sig_from_dyw(ldy, lw);
+    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    Local d, w;
+    if ((rc = local_input(dY, ldy, &d))) return rc;
+    if ((rc = local_input(W, lw, &w))) return rc;
+    if (d.dtype != w.dtype) return SBP_ERR_DTYPE;
+    if (d.global && w.global && d.gcols != w.gcols) return SBP_ERR_SHAPE;
+    if (d.cols != w.cols) return SBP_ERR_SHAPE;
+    sbp_layout_t st[4];
+    states_of(s, ldy, st);
+    if ((rc = check_output(dX, d.rows, w.rows, d.dtype, st[2].kind, d, w))) return rc;
+    sbpi::Gemm g{sbpi::OR_BWD_DATA, d.dtype, dX->dtype, d.ptr, d.ld, w.ptr, w.ld,
+                 dX->data, dX->ld, d.rows, w.rows, d.cols};
+    if ((rc = run(g, stream))) return rc;
+    if (ldx_out) *ldx_out = st[2];
+    return SBP_OK;
+}
+
+int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *dY,
+                          const sbp_layout_t *ldy, sbp_view_t *dW, sbp_layout_t *ldw_out,
+                          hipStream_t stream) {
+    if (!X || !dY || !dW || !lx || !ldy) return SBP_ERR_NULL;
+    int rc = check_pair(lx, ldy);
+    if (rc) return rc;
+    Sig s = sig_from_xdy(lx, ldy);
+    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    Local x, d;
+    if ((rc = local_input(X, lx, &x))) return rc;
+    if ((rc = local_input(dY, ldy, &d))) return rc;
+    if (x.dtype != d.dtype) return SBP_ERR_DTYPE;
+    if (x.global && d.global && x.grows != d.grows) return SBP_ERR_SHAPE;
+    if (x.rows != d.rows) return SBP_ERR_SHAPE;
+    sbp_layout_t st[4];
+    states_of(s, lx, st);
+    if ((rc = check_output(dW, x.cols, d.cols, x.dtype, st[3].kind, x, d))) return rc;
+    sbpi::Gemm g{sbpi::OR_BWD_WEIGHT, x.dtype, dW->dtype, x.ptr, x.ld, d.ptr, d.ld,
+                 dW->data, dW->ld, x.cols, d.cols, x.rows};
+    if ((rc = run(g, stream))) return rc;
+    if (ldw_out) *ldw_out = st[3];
+    return SBP_OK;
+}
+
+const char *sbp_strerror(int code) {
+    switch (code) {
+        case SBP_OK: return "success";
+        case SBP_ERR_NULL: return "a required pointer is NULL";
+        case SBP_ERR_LAYOUT: return "invalid SBP layout (p, r, kind or axis), or layouts disagree on p or r";
+        case SBP_ERR_SIGNATURE: return "the input SBP states form no supported signature";
+        case SBP_ERR_SHAPE: return "shape mismatch, ld < cols, or output view is not the local output shape";
+        case SBP_ERR_DTYPE: return "unsupported or inconsistent dtype (partial-sum outputs must be fp32)";
+        case SBP_ERR_ALIAS: return "the output overlaps an input";
+        case SBP_ERR_ALIGN: return "a data pointer is not aligned to its element size";
+        case SBP_ERR_HIP: return "a HIP runtime call failed";
+    }
+    return "unknown error code";
+}
+
+int sbp_last_hip_error(void) { return g_last_hip; }
+
+int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype, int32_t out_dtype,
+             int32_t *tile_m, int32_t *tile_n, int32_t *splits) {
+    if (!tile_m || !tile_n || !splits) return SBP_ERR_NULL;
+    if (m < 0 || n < 0 || k < 0 || m > INT32_MAX || n > INT32_MAX || k > INT32_MAX ||
+        op < 0 || op > 2)
+        return SBP_ERR_SHAPE;
+    if ((in_dtype != SBP_BF16 && in_dtype != SBP_F32) ||
+        (out_dtype != SBP_BF16 && out_dtype != SBP_F32))
+        return SBP_ERR_DTYPE;
+    if (in_dtype == SBP_F32) {
+        *tile_m = 64;
+        *tile_n = 64;
+        *splits = 1;
+        return SBP_OK;
+    }
+    sbpi::Gemm g{op, in_dtype, out_dtype, nullptr, 0, nullptr, 0, nullptr, 0, m, n, k};
+    sbpi::Plan p = sbpi::plan_bf16(g);
+    *tile_m = p.bm;
+    *tile_n = p.bn;
+    *splits = p.splits;
+    return SBP_OK;
+}
+
+int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits) {
+    if (tile_m == 0) {
+        sbpi::set_override(0, 0, 1);
+        return SBP_OK;
+    }
+    if (!sbpi::tile_supported(tile_m, tile_n) || splits < 1) return SBP_ERR_SHAPE;
+    sbpi::set_override(tile_m, tile_n, splits);
+    return SBP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,205 @@
+"""ctypes binding of libsbp.so, the C ABI declared in include/sbp.h.
+
+Argument marshalling only: every computation runs in the library's kernels.
+The functions carry the C names; a nonzero return code raises SbpError.
+Loading fails loudly when the library has not been built
+(``python -m paper_2301_06813_amd.build``); there is no fallback.
+
+``view(tensor, scope)`` turns a 2-D torch tensor with unit column stride into
+an ``sbp_view_t`` (pointer, rows, cols, ld, dtype, scope); torch is used only
+for device memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsbp.so")
+
+# ---------------------------------------------------------------- constants
+SBP_OK = 0
+SBP_ERR_NULL = -1
+SBP_ERR_LAYOUT = -2
+SBP_ERR_SIGNATURE = -3
+SBP_ERR_SHAPE = -4
+SBP_ERR_DTYPE = -5
+SBP_ERR_ALIAS = -6
+SBP_ERR_ALIGN = -7
+SBP_ERR_HIP = -8
+
+SBP_SPLIT, SBP_BROADCAST, SBP_PARTIAL = 0, 1, 2
+SBP_BF16, SBP_F32 = 0, 1
+SBP_GLOBAL, SBP_LOCAL = 0, 1
+
+EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd_data",
+           "sbp_linear_bwd_weight", "sbp_strerror", "sbp_last_hip_error", "sbp_plan",
+           "sbp_set_plan_override")
+
+
+class sbp_layout_t(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("axis", ctypes.c_int32),
+                ("p", ctypes.c_int32), ("r", ctypes.c_int32)]
+
+    def __repr__(self):
+        name = {SBP_SPLIT: "S(%d)" % self.axis, SBP_BROADCAST: "B", SBP_PARTIAL: "P"}.get(
+            self.kind, "?%d" % self.kind)
+        return "%s[p=%d,r=%d]" % (name, self.p, self.r)
+
+    def key(self):
+        return (self.kind, self.axis, self.p, self.r)
+
+
+class sbp_view_t(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("ld", ctypes.c_int64), ("dtype", ctypes.c_int32), ("scope", ctypes.c_int32)]
+
+
+class sbp_shard_t(ctypes.Structure):
+    _fields_ = [("row_off", ctypes.c_int64), ("col_off", ctypes.c_int64),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64)]
+
+
+class SbpError(RuntimeError):
+    def __init__(self, code, hip_error=0):
+        self.code = code
+        self.hip_error = hip_error
+        msg = "%s (%d)" % (sbp_strerror(code), code)
+        if code == SBP_ERR_HIP:
+            msg += ", hipError %d" % hip_error
+        super().__init__(msg)
+
+
+def split(axis: int, p: int, r: int) -> sbp_layout_t:
+    return sbp_layout_t(SBP_SPLIT, axis, p, r)
+
+
+def broadcast(p: int, r: int) -> sbp_layout_t:
+    return sbp_layout_t(SBP_BROADCAST, -1, p, r)
+
+
+def partial(p: int, r: int) -> sbp_layout_t:
+    return sbp_layout_t(SBP_PARTIAL, -1, p, r)
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libsbp.so is not built (%s); run `python -m "
+                              "paper_2301_06813_amd.build`" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.sbp_shard_index.argtypes = [P(sbp_layout_t), ctypes.c_int64, ctypes.c_int64,
+                                      P(sbp_shard_t)]
+        L.sbp_signature.argtypes = [P(sbp_layout_t)] * 6
+        for fn in ("sbp_linear_fwd", "sbp_linear_bwd_data", "sbp_linear_bwd_weight"):
+            getattr(L, fn).argtypes = [P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
+                                       P(sbp_layout_t), P(sbp_view_t), P(sbp_layout_t),
+                                       ctypes.c_void_p]
+        L.sbp_strerror.argtypes = [ctypes.c_int]
+        L.sbp_strerror.restype = ctypes.c_char_p
+        L.sbp_last_hip_error.argtypes = []
+        L.sbp_plan.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                               ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32),
+                               P(ctypes.c_int32), P(ctypes.c_int32)]
+        L.sbp_set_plan_override.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
+        for fn in EXPORTS:
+            if fn != "sbp_strerror":
+                getattr(L, fn).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(code):
+    if code != SBP_OK:
+        raise SbpError(code, lib().sbp_last_hip_error() if code == SBP_ERR_HIP else 0)
+
+
+# ------------------------------------------------------------------- views
+def view(t, scope=SBP_GLOBAL) -> sbp_view_t:
+    """sbp_view_t of a 2-D torch tensor whose columns are contiguous."""
+    import torch
+    if t.dim() != 2:
+        raise ValueError("views are 2-D")
+    if t.stride(1) != 1 and t.shape[1] > 1:
+        raise ValueError("views need unit column stride")
+    dt = {torch.bfloat16: SBP_BF16, torch.float32: SBP_F32}.get(t.dtype)
+    if dt is None:
+        raise TypeError("unsupported dtype %s" % t.dtype)
+    ld = max(t.stride(0), t.shape[1], 1)
+    return sbp_view_t(t.data_ptr(), t.shape[0], t.shape[1], ld, dt, scope)
+
+
+def raw_view(ptr, rows, cols, ld, dtype, scope=SBP_GLOBAL) -> sbp_view_t:
+    return sbp_view_t(ptr, rows, cols, ld, dtype, scope)
+
+
+def current_stream():
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+# ------------------------------------------------------------- functions
+def sbp_strerror(code: int) -> str:
+    return lib().sbp_strerror(code).decode()
+
+
+def sbp_shard_index(layout: sbp_layout_t, rows: int, cols: int) -> sbp_shard_t:
+    out = sbp_shard_t()
+    _check(lib().sbp_shard_index(ctypes.byref(layout), rows, cols, ctypes.byref(out)))
+    return out
+
+
+def sbp_signature(x: sbp_layout_t, w: sbp_layout_t):
+    """(Y, dY, dX, dW) states for X in state x and W in state w."""
+    y, dy, dx, dw = sbp_layout_t(), sbp_layout_t(), sbp_layout_t(), sbp_layout_t()
+    _check(lib().sbp_signature(ctypes.byref(x), ctypes.byref(w), ctypes.byref(y),
+                               ctypes.byref(dy), ctypes.byref(dx), ctypes.byref(dw)))
+    return y, dy, dx, dw
+
+
+def _compute(fn, a, la, b, lb, out, stream):
+    lo = sbp_layout_t()
+    s = current_stream() if stream is None else stream
+    _check(getattr(lib(), fn)(ctypes.byref(a), ctypes.byref(la), ctypes.byref(b),
+                              ctypes.byref(lb), ctypes.byref(out), ctypes.byref(lo),
+                              ctypes.c_void_p(s)))
+    return lo
+
+
+def sbp_linear_fwd(X: sbp_view_t, lx: sbp_layout_t, W: sbp_view_t, lw: sbp_layout_t,
+                   Y: sbp_view_t, stream=None) -> sbp_layout_t:
+    """Y_r = X_r W_r on `stream` (default: torch's current stream); returns Y's state."""
+    return _compute("sbp_linear_fwd", X, lx, W, lw, Y, stream)
+
+
+def sbp_linear_bwd_data(dY: sbp_view_t, ldy: sbp_layout_t, W: sbp_view_t, lw: sbp_layout_t,
+                        dX: sbp_view_t, stream=None) -> sbp_layout_t:
+    """dX_r = dY_r W_r^T; returns dX's state."""
+    return _compute("sbp_linear_bwd_data", dY, ldy, W, lw, dX, stream)
+
+
+def sbp_linear_bwd_weight(X: sbp_view_t, lx: sbp_layout_t, dY: sbp_view_t, ldy: sbp_layout_t,
+                          dW: sbp_view_t, stream=None) -> sbp_layout_t:
+    """dW_r = X_r^T dY_r; returns dW's state."""
+    return _compute("sbp_linear_bwd_weight", X, lx, dY, ldy, dW, stream)
+
+
+def sbp_last_hip_error() -> int:
+    return lib().sbp_last_hip_error()
+
+
+def sbp_plan(op: int, m: int, n: int, k: int, in_dtype: int, out_dtype: int):
+    """(tile_m, tile_n, splits) the library would launch for this product."""
+    tm, tn, sp = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().sbp_plan(op, m, n, k, in_dtype, out_dtype, ctypes.byref(tm), ctypes.byref(tn),
+                          ctypes.byref(sp)))
+    return tm.value, tn.value, sp.value
+
+
+def sbp_set_plan_override(tile_m: int, tile_n: int, splits: int) -> None:
+    _check(lib().sbp_set_plan_override(tile_m, tile_n, splits))

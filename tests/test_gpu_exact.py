@@ -1,0 +1,186 @@
+"""Bit-exact GPU checks through the C ABI.
+
+Integer inputs in [-3, 3] make every product and every partial sum an exact
+fp32 integer (|sum| <= 9 K < 2^24), so the library's fp32 result must equal
+the oracle's exactly in any summation order, and a bf16 output must equal
+the oracle's round-to-nearest-even of that exact integer. This covers every
+signature, operation, tile shape and split count, ragged sizes, uneven
+shards and misaligned shard views.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2301_06813_amd import inputs, linear, sbp
+
+from helpers import TILES, decode, expect_state, oracle_full, out_bits, run_gpu, say
+
+pytestmark = pytest.mark.gpu
+SIGS = ("DP", "COL", "KS")
+OPS = ("fwd", "bwd_data", "bwd_weight")
+
+
+def _int_inputs(M, K, N, seed, device="cuda"):
+    X = inputs.randint((M, K), -3, 3, seed + 1, torch.bfloat16, device)
+    W = inputs.randint((K, N), -3, 3, seed + 2, torch.bfloat16, device)
+    dY = inputs.randint((M, N), -3, 3, seed + 3, torch.bfloat16, device)
+    return X, W, dY
+
+
+def _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh):
+    out, st = run_gpu(op, sig, p, r, X, W, dY)
+    expect_state(op, sig, p, r, st)
+    want = oracle_full(op, sig, p, r, Xh, Wh, dYh)
+    assert out.shape == want.shape, (op, sig, p, r, out.shape, want.shape)
+    if out.dtype == torch.bfloat16:
+        assert np.array_equal(out_bits(out), oracle.round_bf16(want)), (op, sig, p, r)
+    else:
+        assert np.array_equal(decode(out), want), (op, sig, p, r)
+
+
+@pytest.mark.parametrize("shape", [(300, 1000, 270), (64, 64, 64), (1, 70, 9), (517, 129, 33)])
+def test_exact_all_signatures_default_plan(shape):
+    M, K, N = shape
+    X, W, dY = _int_inputs(M, K, N, 100)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    for p in (1, 3, 8):
+        for r in sorted({0, p // 2, p - 1}):
+            for sig in SIGS:
+                for op in OPS:
+                    say("exact", shape, p, r, sig, op)
+                    _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
+
+
+@pytest.mark.parametrize("tile", TILES, ids=["%dx%d" % t for t in TILES])
+def test_exact_every_tile_and_split(tile):
+    M, K, N = 300, 1100, 270
+    X, W, dY = _int_inputs(M, K, N, 200)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    p, r = 2, 1
+    try:
+        for splits in (1, 3, 7):
+            sbp.sbp_set_plan_override(tile[0], tile[1], splits)
+            for sig in SIGS:
+                for op in OPS:
+                    say("tile", tile, "splits", splits, sig, op)
+                    _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
+
+
+def test_exact_long_reduction_split():
+    # reduction of 8192 (the longest in the workloads), |sum| <= 9 * 8192 < 2^24
+    M, K, N = 8192, 256, 200
+    X, W, dY = _int_inputs(M, K, N, 300)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    for sig in ("COL", "KS"):
+        say("long reduction", sig)
+        _check_exact("bwd_weight", sig, 8, 3, X, W, dY, Xh, Wh, dYh)
+
+
+def test_exact_misaligned_column_shards():
+    # COL with N = 1000 over 8 ranks: W and dY column shards start at 125 r,
+    # i.e. byte offsets 250 r, not 16-byte aligned for odd r.
+    M, K, N = 96, 256, 1000
+    X, W, dY = _int_inputs(M, K, N, 400)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    for r in range(8):
+        for op in OPS:
+            say("misaligned", r, op)
+            _check_exact(op, "COL", 8, r, X, W, dY, Xh, Wh, dYh)
+
+
+def test_exact_local_scope_padded_ld():
+    # LOCAL views with ld > cols and an odd element offset; the result must
+    # equal the GLOBAL-scope call on the same share.
+    M, K, N, p, r = 130, 96, 72, 4, 2
+    X, W, dY = _int_inputs(M, K, N, 500)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    want = oracle_full("fwd", "DP", p, r, Xh, Wh, dYh)
+    sh = sbp.sbp_shard_index(sbp.split(0, p, r), M, K)
+    buf = torch.zeros((sh.rows + 1, K + 9), dtype=torch.bfloat16, device="cuda")
+    Xr = buf[1:, 3:3 + K]
+    Xr.copy_(X[sh.row_off:sh.row_off + sh.rows])
+    out = torch.empty((sh.rows, N), dtype=torch.float32, device="cuda")
+    L = linear.layouts("DP", p, r)
+    sbp.sbp_linear_fwd(sbp.view(Xr, sbp.SBP_LOCAL), L["x"], sbp.view(W), L["w"],
+                       sbp.view(out, sbp.SBP_LOCAL))
+    torch.cuda.synchronize()
+    assert np.array_equal(decode(out), want)
+
+
+def test_k_zero_share_writes_zeros():
+    # K = 3 over p = 4: rank 3 holds an empty reduction share, so its
+    # Partial-sum forward output is all zeros (and must be written).
+    M, K, N, p, r = 40, 3, 50, 4, 3
+    X, W, dY = _int_inputs(M, K, N, 600)
+    out = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    linear.run("fwd", "KS", p, r, X, W, dY, out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 0)
+
+
+def test_shard_readback_identity():
+    # With an identity weight the forward output is the selected share of X,
+    # bit for bit (x 1.0 and + 0.0 are exact): checks the shard views through
+    # the kernel for every signature and rank.
+    M, K, p = 200, 136, 8
+    g = torch.Generator(device="cuda").manual_seed(7)
+    X = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+    I = torch.eye(K, dtype=torch.bfloat16, device="cuda")
+    for r in range(p):
+        for sig in SIGS:
+            say("readback", sig, r)
+            out, _ = run_gpu("fwd", sig, p, r, X, I, None)
+            xs = sbp.sbp_shard_index(linear.layouts(sig, p, r)["x"], M, K)
+            ws = sbp.sbp_shard_index(linear.layouts(sig, p, r)["w"], K, K)
+            want = torch.zeros((xs.rows, ws.cols), dtype=torch.float32, device="cuda")
+            # X_r I_r: the columns of X_r that meet the ones of the identity share
+            Xr = X[xs.row_off:xs.row_off + xs.rows, xs.col_off:xs.col_off + xs.cols].float()
+            for j in range(ws.cols):
+                kk = ws.col_off + j - ws.row_off
+                if 0 <= kk < xs.cols:
+                    want[:, j] = Xr[:, kk]
+            assert torch.equal(out.float(), want), (sig, r)
+
+
+def test_guard_bands_untouched():
+    # Outputs inside a NaN-filled buffer (ld > cols, rows above and below):
+    # the guard stays NaN and every element of the share is written.
+    M, K, N, p = 150, 200, 140, 3
+    X, W, dY = _int_inputs(M, K, N, 700)
+    for tile in TILES:
+        sbp.sbp_set_plan_override(tile[0], tile[1], 2)
+        try:
+            for sig in SIGS:
+                for op in OPS:
+                    r = 1
+                    L = linear.layouts(sig, p, r)
+                    rows, cols = linear.out_shape(op, L, M, K, N)
+                    dt = linear.out_dtype(op, L, torch.bfloat16)
+                    buf = torch.full((rows + 2, cols + 7), float("nan"), dtype=dt, device="cuda")
+                    out = buf[1:rows + 1, 2:2 + cols]
+                    linear.run(op, sig, p, r, X, W, dY, out)
+                    torch.cuda.synchronize()
+                    guard = torch.ones_like(buf, dtype=torch.bool)
+                    guard[1:rows + 1, 2:2 + cols] = False
+                    assert torch.all(torch.isnan(buf[guard])), (tile, sig, op)
+                    assert not torch.any(torch.isnan(out)), (tile, sig, op)
+        finally:
+            sbp.sbp_set_plan_override(0, 0, 1)
+
+
+def test_split_reduction_is_deterministic():
+    M, K, N = 384, 4096, 320
+    g = torch.Generator(device="cuda").manual_seed(3)
+    X = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+    dY = torch.randn((M, N), generator=g, device="cuda").to(torch.bfloat16)
+    sbp.sbp_set_plan_override(128, 128, 5)
+    try:
+        for sig in ("DP", "COL"):
+            a, _ = run_gpu("bwd_weight", sig, 1, 0, X, None, dY)
+            b, _ = run_gpu("bwd_weight", sig, 1, 0, X, None, dY)
+            assert torch.equal(a, b)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
