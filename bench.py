@@ -75,10 +75,15 @@ class Step:
                     m, n = out.shape
                     k = sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows
                 ob = 4 if out.dtype == torch.float32 else 2
-                tm, tn, sp = sbp.sbp_plan(ORIENT[op], m, n, k, sbp.SBP_BF16,
-                                          sbp.SBP_F32 if ob == 4 else sbp.SBP_BF16)
-                kern = "gemm_bf16_kernel<%d, %d, %s, %s, %s>" % (
-                    tm, tn, KMAJ[op][0], KMAJ[op][1], "true" if ob == 4 else "false")
+                tm, tn, sp, kn = sbp.sbp_plan(ORIENT[op], m, n, k, sbp.SBP_BF16,
+                                              sbp.SBP_F32 if ob == 4 else sbp.SBP_BF16)
+                if kn == sbp.KERNEL_PIPELINED:
+                    ns = {(256, 256): 2, (256, 128): 3, (128, 256): 3}.get((tm, tn), 4)
+                    kern = "gemm_bf16_dma_kernel<%d, %d, %d, %s, %s, %s>" % (
+                        tm, tn, ns, KMAJ[op][0], KMAJ[op][1], "true" if ob == 4 else "false")
+                else:
+                    kern = "gemm_bf16_kernel<%d, %d, %s, %s, %s>" % (
+                        tm, tn, KMAJ[op][0], KMAJ[op][1], "true" if ob == 4 else "false")
                 meta = dict(linear=lin.name, sig=lin.sig, op=op, m=m, n=n, k=k,
                             flops=2.0 * m * n * k, bytes=2.0 * (m * k + k * n) + ob * m * n,
                             kernel=kern, splits=sp)
@@ -155,6 +160,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager launches, not a graph")
+    ap.add_argument("--dump", default=None, help="write per-launch shapes and durations (JSON)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build measures rank r's local products on a "
@@ -217,6 +223,9 @@ def main():
             for i in range(n):
                 durs[i].append(ev[i][0].elapsed_time(ev[i][1]) * 1e-3)
     avg = [sum(d) / len(d) for d in durs]
+    if args.dump:
+        with open(args.dump, "w") as f:
+            json.dump([dict(m, us=t * 1e6) for m, t in zip(step.meta, avg)], f)
     by_kernel = collections.defaultdict(lambda: [0.0, 0.0, 0.0, 0])
     by_sig = collections.defaultdict(lambda: [0.0, 0.0])
     for m, t in zip(step.meta, avg):

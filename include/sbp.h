@@ -164,22 +164,28 @@ const char *sbp_strerror(int code);
 int sbp_last_hip_error(void);
 
 /* Kernel plan the library would use for a local product of m x n outputs
- * over a reduction of k, for input dtype in_dtype and output dtype out_dtype
- * and operand orientation op (0 forward, 1 backward-data, 2
- * backward-weight). Writes the tile rows, tile columns and number of
- * reduction splits. For benchmarks and tests; pure host function.
+ * over a reduction of k with 16-byte aligned operands and tight leading
+ * dimensions, for input dtype in_dtype, output dtype out_dtype and operand
+ * orientation op (0 forward, 1 backward-data, 2 backward-weight). Writes
+ * the tile rows and columns, the number of reduction splits and the kernel
+ * (1 pipelined direct-to-LDS bf16, 2 generic bf16, 3 fp32). For benchmarks
+ * and tests; pure host function.
  * Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
 int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype,
              int32_t out_dtype, int32_t *tile_m, int32_t *tile_n,
-             int32_t *splits);
+             int32_t *splits, int32_t *kernel);
 
-/* Thread-local override of the plan for subsequent calls on this thread
- * (tests and tuning): tile_m x tile_n must be one of the compiled bf16 tile
- * shapes (256x128, 128x256, 128x128, 128x64, 64x128, 64x64) and
- * splits >= 1; tile_m = 0 clears the override. An override that a call
- * cannot use (fp32 inputs, or more splits than reduction blocks) is
- * clamped for that call. Errors: SBP_ERR_SHAPE for an unknown tile shape. */
-int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits);
+/* Thread-local override of the bf16 plan for subsequent calls on this
+ * thread (tests and tuning). tile_m x tile_n is one of 256x128, 128x256,
+ * 128x128, 128x64, 64x128, 64x64; splits >= 1; kernel 0 = the
+ * library's choice, 1 = pipelined direct-to-LDS, 2 = generic. A call whose
+ * operands the pipelined kernel cannot read runs the generic kernel; splits
+ * are clamped to the reduction blocks and
+ * to the workspace. tile_m = 0 clears the override.
+ * Errors: SBP_ERR_SHAPE for an unknown tile shape, splits < 1 or kernel
+ * outside 0..2. */
+int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits,
+                          int32_t kernel);
 
 #ifdef __cplusplus
 }

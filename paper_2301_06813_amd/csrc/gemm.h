@@ -33,21 +33,28 @@ struct Plan {
     int bm, bn;            // output tile
     int splits;            // reduction splits actually launched
     int kblk_per_split;    // 64-wide reduction blocks per split
+    bool dma;              // pipelined direct-to-LDS kernel (else the generic kernel)
 };
 
-// Workspace the split reduction needs, per (device, stream).
-constexpr size_t WS_FLOATS = size_t(16) << 20;   // 64 MiB of fp32 partials
-constexpr size_t WS_COUNTERS = size_t(1) << 16;  // tile counters
+// Whether the pipelined direct-to-LDS kernel can run this product: every
+// operand 16-byte aligned, leading dimensions and contiguous extents
+// multiples of 8 elements, and tile offsets that fit 31-bit buffer offsets.
+bool dma_eligible(const Gemm &g);
+
+// Workspace the split reduction needs, per (device, stream): splits slices
+// of m x n fp32 partials.
+constexpr size_t WS_FLOATS = size_t(32) << 20;   // 128 MiB
 
 // bf16 planning: heuristic choice of tile and splits (an override may be set
 // per thread through sbp_set_plan_override). Always fits the workspace.
 Plan plan_bf16(const Gemm &g);
-bool tile_supported(int bm, int bn);
-void set_override(int bm, int bn, int splits);   // bm = 0 clears
+bool tile_supported(int bm, int bn, bool dma);
+void set_override(int bm, int bn, int splits, int kernel);   // bm = 0 clears
 
-hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, uint32_t *counters,
-                       hipStream_t s);
+// GEMM of plan p; with p.splits > 1 it writes partials to ws and then runs
+// the split reduction into g.C.
+hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, hipStream_t s);
+hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipStream_t s);
 hipError_t launch_f32(const Gemm &g, hipStream_t s);
-hipError_t zero_u32(uint32_t *p, size_t n, hipStream_t s);
 
 }  // namespace sbpi

@@ -2,8 +2,7 @@
 #include "gemm_bf16_launch.h"
 
 namespace sbpi {
-hipError_t launch_bf16_bwd_data(const Gemm &g, const Plan &p, float *ws, uint32_t *counters,
-                               hipStream_t s) {
-    return launch_orient<true, true>(g, p, ws, counters, s);
+hipError_t launch_bf16_bwd_data(const Gemm &g, const Plan &p, float *ws, hipStream_t s) {
+    return launch_orient<true, true>(g, p, ws, s);
 }
 }  // namespace sbpi

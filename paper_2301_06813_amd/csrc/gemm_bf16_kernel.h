@@ -27,10 +27,11 @@
 //   * Register prefetch + two LDS buffers: the global loads of step t+1 are
 //     in flight while step t runs on the MFMA units; one barrier per step.
 //   * Split reduction (splits > 1): each workgroup reduces one k-range and
-//     writes its fp32 partial tile to a workspace; the last workgroup to
-//     finish a tile (an atomic counter per tile) adds the partials in split
-//     order -- deterministic -- and writes the output, then resets the
-//     counter for the next call.
+//     writes its fp32 partial tile to slice `split` of a workspace laid out
+//     like the output; a second kernel (split_reduce_kernel) adds the slices
+//     in split order -- deterministic -- and writes the output. Kernel
+//     boundaries order the two, so no device-scope fences or atomics are
+//     needed (on gfx950 such fences write back and invalidate the XCD's L2).
 //   * Workgroup -> tile order is XCD-aware: consecutive workgroup ids go to
 //     different XCDs, so ids are remapped to give each XCD a contiguous run
 //     of tiles (shared A rows / B columns stay in that XCD's L2).
@@ -64,8 +65,7 @@ struct GemmArgs {
     int32_t tiles_m, tiles_n;
     int32_t splits;             // reduction splits (>= 1)
     int32_t kblk_per_split;     // BK-blocks per split
-    float *ws;                  // split partials: tiles * splits * BM * BN floats
-    uint32_t *counters;         // one per tile, zero between calls
+    float *ws;                  // split partials: splits slices of m x n floats
     int32_t vec_a, vec_b;       // operand base and ld allow aligned 16-byte loads
 };
 
@@ -110,8 +110,20 @@ struct KMajorTile {
     static constexpr int NV = BMN * BK / 8 / NT;   // 16-byte vectors per thread
     u32x4 v[NV];
 
-    __device__ __forceinline__ void load(const uint16_t *base, int64_t ld, int mn0,
-                                         int mn_lim, int k0, int k_lim, int tid, bool vec) {
+    // Whole tile inside the operand and 16-byte aligned: plain vector loads.
+    __device__ __forceinline__ void load_full(const uint16_t *base, int64_t ld, int mn0, int k0,
+                                              int tid) {
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            int q = i * NT + tid;
+            const uint16_t *p = base + (int64_t)(mn0 + (q >> 3)) * ld + (k0 + (q & 7) * 8);
+            v[i] = *reinterpret_cast<const u32x4 *>(p);
+        }
+    }
+
+    // Edge or unaligned tile: masked loads, zero outside the operand.
+    __device__ __forceinline__ void load_edge(const uint16_t *base, int64_t ld, int mn0, int mn_lim,
+                                           int k0, int k_lim, int tid, bool vec) {
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             int q = i * NT + tid;
@@ -146,8 +158,17 @@ struct MNMajorTile {
     static_assert(KB == 8 || KB == 4 || KB == 2, "unsupported tile");
     u32x4 v[KB];
 
-    __device__ __forceinline__ void load(const uint16_t *base, int64_t ld, int mn0,
-                                         int mn_lim, int k0, int k_lim, int tid, bool vec) {
+    __device__ __forceinline__ void load_full(const uint16_t *base, int64_t ld, int mn0, int k0,
+                                              int tid) {
+        const int mnb = tid % NMB;
+        const int kb = tid / NMB;
+        const uint16_t *p = base + (int64_t)(k0 + kb * KB) * ld + (mn0 + mnb * 8);
+#pragma unroll
+        for (int r = 0; r < KB; ++r) v[r] = *reinterpret_cast<const u32x4 *>(p + (int64_t)r * ld);
+    }
+
+    __device__ __forceinline__ void load_edge(const uint16_t *base, int64_t ld, int mn0, int mn_lim,
+                                           int k0, int k_lim, int tid, bool vec) {
         int mnb = tid % NMB;
         int kb = tid / NMB;
         int mn = mn0 + mnb * 8;
@@ -203,6 +224,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
     return __builtin_bit_cast(uint16_t, h);
 }
 
+
 template <int BM, int BN, bool A_KMAJ, bool B_KMAJ, bool OUT_F32>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     constexpr int WM = BM / 2, WN = BN / 2;       // wave tile
@@ -210,7 +232,6 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB;
     constexpr int STAGE = A_BYTES + B_BYTES;
     __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
-    __shared__ int last_flag;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -240,6 +261,16 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     TileOf<BM, A_KMAJ> ta;
     TileOf<BN, B_KMAJ> tb;
     const bool va = g.vec_a != 0, vb = g.vec_b != 0;
+    // uniform per workgroup: the tile's m (n) range is inside the operand and aligned
+    const bool a_in = va && (m0 + BM <= g.m);
+    const bool b_in = vb && (n0 + BN <= g.n);
+    auto load_tiles = [&](int k0) {
+        const bool k_in = (k0 + BK <= k_lim);
+        if (a_in && k_in) ta.load_full(g.A, g.lda, m0, k0, tid);
+        else ta.load_edge(g.A, g.lda, m0, g.m, k0, k_lim, tid, va);
+        if (b_in && k_in) tb.load_full(g.B, g.ldb, n0, k0, tid);
+        else tb.load_edge(g.B, g.ldb, n0, g.n, k0, k_lim, tid, vb);
+    };
 
     f32x16 acc[MI][NI];
 #pragma unroll
@@ -250,9 +281,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     if (nkb > 0) {
-        int k0 = kb_begin * BK;
-        ta.load(g.A, g.lda, m0, g.m, k0, k_lim, tid, va);
-        tb.load(g.B, g.ldb, n0, g.n, k0, k_lim, tid, vb);
+        load_tiles(kb_begin * BK);
         ta.store(smem, tid);
         tb.store(smem + A_BYTES, tid);
         __syncthreads();
@@ -261,9 +290,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
             char *cur = smem + (it & 1) * STAGE;
             const bool more = (it + 1 < nkb);
             if (more) {
-                int kn = (kb_begin + it + 1) * BK;
-                ta.load(g.A, g.lda, m0, g.m, kn, k_lim, tid, va);
-                tb.load(g.B, g.ldb, n0, g.n, kn, k_lim, tid, vb);
+                load_tiles((kb_begin + it + 1) * BK);
             }
 #pragma unroll
             for (int ks = 0; ks < BK / 16; ++ks) {
@@ -296,41 +323,25 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
 
     // ---- split reduction: partials to workspace, last workgroup adds them
     if (g.splits > 1) {
-        constexpr int PER = MI * NI * 16;          // floats per thread
-        const size_t tile_base = (size_t)t * g.splits;
-        float *mine = g.ws + (tile_base + split) * (size_t)(PER * NT);
+        // Split reduction: this workgroup's fp32 partial goes to slice
+        // `split` of the workspace, laid out like the output (m x n, ld n);
+        // a separate kernel adds the slices in split order.
+        float *P = g.ws + (size_t)split * (size_t)g.m * (size_t)g.n;
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
-            for (int j = 0; j < NI; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    mine[((i * NI + j) * 16 + r) * NT + tid] = acc[i][j][r];
-        __threadfence();
-        __syncthreads();
-        if (tid == 0) {
-            uint32_t done = atomicAdd(&g.counters[t], 1u);
-            last_flag = (done == (uint32_t)(g.splits - 1));
-        }
-        __syncthreads();
-        if (!last_flag) return;
-        __threadfence();
-        // Sum the partials in split order 0, 1, ..., splits-1 (this
-        // workgroup's own partial is read back too), so the result does not
-        // depend on which workgroup finished last.
-        for (int s = 0; s < g.splits; ++s) {
-            const float *part = g.ws + (tile_base + s) * (size_t)(PER * NT);
-#pragma unroll
-            for (int i = 0; i < MI; ++i)
-#pragma unroll
-                for (int j = 0; j < NI; ++j)
+            for (int j = 0; j < NI; ++j) {
+                const int col = n0 + wn * WN + j * 32 + (lane & 31);
+                const int rbase = m0 + wm * WM + i * 32 + 4 * (lane >> 5);
+                if (col < g.n) {
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
-                        float v = __builtin_nontemporal_load(&part[((i * NI + j) * 16 + r) * NT + tid]);
-                        acc[i][j][r] = (s == 0) ? v : acc[i][j][r] + v;
+                        const int row = rbase + 8 * (r >> 2) + (r & 3);
+                        if (row < g.m) P[(int64_t)row * g.n + col] = acc[i][j][r];
                     }
-        }
-        if (tid == 0) atomicExch(&g.counters[t], 0u);
+                }
+            }
+        return;
     }
 
     // ---- epilogue: MFMA 32x32 accumulator layout -> row-major C

@@ -4,16 +4,23 @@
 #pragma once
 
 #include "gemm.h"
-#include "gemm_bf16_kernel.h"
+#include "gemm_bf16_dma.h"
 
 namespace sbpi {
 
 template <bool AK, bool BK_, bool OUTF>
-static hipError_t launch_tile(int bm, int bn, const sbpk::GemmArgs &a, int grid, hipStream_t s) {
+static hipError_t launch_tile(int bm, int bn, bool dma, const sbpk::GemmArgs &a, int grid,
+                              hipStream_t s) {
 #define SBP_TILE(BM_, BN_)                                                                  \
-    if (bm == BM_ && bn == BN_) {                                                           \
+    if (!dma && bm == BM_ && bn == BN_) {                                                   \
         hipLaunchKernelGGL((sbpk::gemm_bf16_kernel<BM_, BN_, AK, BK_, OUTF>), dim3(grid),   \
                            dim3(sbpk::NT), 0, s, a);                                        \
+        return hipGetLastError();                                                           \
+    }
+#define SBP_DMA_TILE(BM_, BN_, NS_)                                                         \
+    if (dma && bm == BM_ && bn == BN_) {                                                    \
+        hipLaunchKernelGGL((sbpk::gemm_bf16_dma_kernel<BM_, BN_, NS_, AK, BK_, OUTF>),      \
+                           dim3(grid), dim3(sbpk::NT), 0, s, a);                            \
         return hipGetLastError();                                                           \
     }
     SBP_TILE(256, 128)
@@ -22,13 +29,19 @@ static hipError_t launch_tile(int bm, int bn, const sbpk::GemmArgs &a, int grid,
     SBP_TILE(128, 64)
     SBP_TILE(64, 128)
     SBP_TILE(64, 64)
+    SBP_DMA_TILE(256, 128, 3)
+    SBP_DMA_TILE(128, 256, 3)
+    SBP_DMA_TILE(128, 128, 4)
+    SBP_DMA_TILE(128, 64, 4)
+    SBP_DMA_TILE(64, 128, 4)
+    SBP_DMA_TILE(64, 64, 4)
 #undef SBP_TILE
+#undef SBP_DMA_TILE
     return hipErrorInvalidValue;
 }
 
 template <bool AK, bool BK_>
-static hipError_t launch_orient(const Gemm &g, const Plan &p, float *ws, uint32_t *counters,
-                                hipStream_t s) {
+static hipError_t launch_orient(const Gemm &g, const Plan &p, float *ws, hipStream_t s) {
     sbpk::GemmArgs a;
     a.A = static_cast<const uint16_t *>(g.A);
     a.B = static_cast<const uint16_t *>(g.B);
@@ -44,12 +57,15 @@ static hipError_t launch_orient(const Gemm &g, const Plan &p, float *ws, uint32_
     a.splits = p.splits;
     a.kblk_per_split = p.kblk_per_split;
     a.ws = ws;
-    a.counters = counters;
     a.vec_a = ((reinterpret_cast<uintptr_t>(g.A) & 15) == 0) && (g.lda % 8 == 0);
     a.vec_b = ((reinterpret_cast<uintptr_t>(g.B) & 15) == 0) && (g.ldb % 8 == 0);
     const int grid = a.tiles_m * a.tiles_n * a.splits;
-    if (g.out_dtype == DT_F32) return launch_tile<AK, BK_, true>(p.bm, p.bn, a, grid, s);
-    return launch_tile<AK, BK_, false>(p.bm, p.bn, a, grid, s);
+    // with splits the GEMM writes fp32 partials, whatever the output dtype
+    hipError_t e = (g.out_dtype == DT_F32 || p.splits > 1)
+                       ? launch_tile<AK, BK_, true>(p.bm, p.bn, p.dma, a, grid, s)
+                       : launch_tile<AK, BK_, false>(p.bm, p.bn, p.dma, a, grid, s);
+    if (e != hipSuccess || p.splits == 1) return e;
+    return launch_split_reduce(g, p.splits, ws, s);
 }
 
 }  // namespace sbpi

@@ -1,5 +1,5 @@
-// gemm_f32.hip -- fp32-input path of the local matmul, the bf16 dispatch by
-// orientation, and a small fill kernel.
+// gemm_f32.hip -- fp32-input path of the local matmul and the bf16 dispatch
+// by orientation.
 //
 // The fp32 path serves fp32 workloads (small layers trained in single
 // precision). It is a plain LDS-tiled fp32 FMA kernel: 64 x 64 output tile,
@@ -86,25 +86,19 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(F32Args g) {
     }
 }
 
-__global__ void fill_zero_u32(uint32_t *p, size_t n) {
-    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = 0u;
-}
-
 }  // namespace sbpk
 
 namespace sbpi {
 
-hipError_t launch_bf16_fwd(const Gemm &, const Plan &, float *, uint32_t *, hipStream_t);
-hipError_t launch_bf16_bwd_data(const Gemm &, const Plan &, float *, uint32_t *, hipStream_t);
-hipError_t launch_bf16_bwd_weight(const Gemm &, const Plan &, float *, uint32_t *, hipStream_t);
+hipError_t launch_bf16_fwd(const Gemm &, const Plan &, float *, hipStream_t);
+hipError_t launch_bf16_bwd_data(const Gemm &, const Plan &, float *, hipStream_t);
+hipError_t launch_bf16_bwd_weight(const Gemm &, const Plan &, float *, hipStream_t);
 
-hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, uint32_t *counters,
-                       hipStream_t s) {
+hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, hipStream_t s) {
     switch (g.orient) {
-        case OR_FWD: return launch_bf16_fwd(g, p, ws, counters, s);
-        case OR_BWD_DATA: return launch_bf16_bwd_data(g, p, ws, counters, s);
-        case OR_BWD_WEIGHT: return launch_bf16_bwd_weight(g, p, ws, counters, s);
+        case OR_FWD: return launch_bf16_fwd(g, p, ws, s);
+        case OR_BWD_DATA: return launch_bf16_bwd_data(g, p, ws, s);
+        case OR_BWD_WEIGHT: return launch_bf16_bwd_weight(g, p, ws, s);
     }
     return hipErrorInvalidValue;
 }
@@ -136,12 +130,6 @@ hipError_t launch_f32(const Gemm &g, hipStream_t s) {
         default:
             return hipErrorInvalidValue;
     }
-    return hipGetLastError();
-}
-
-hipError_t zero_u32(uint32_t *p, size_t n, hipStream_t s) {
-    const unsigned blocks = (unsigned)((n + 255) / 256);
-    hipLaunchKernelGGL(sbpk::fill_zero_u32, dim3(blocks), dim3(256), 0, s, p, n);
     return hipGetLastError();
 }
 

@@ -184,7 +184,6 @@ int check_output(const sbp_view_t *o, int64_t rows, int64_t cols, int32_t in_dty
 // ---------------------------------------------------------------- workspace
 struct Workspace {
     float *ws = nullptr;
-    uint32_t *counters = nullptr;
 };
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
@@ -200,11 +199,7 @@ int workspace_for(hipStream_t s, Workspace *out) {
     Workspace &w = g_ws[{dev, s}];
     if (!w.ws) {
         e = hipMalloc(&w.ws, sbpi::WS_FLOATS * sizeof(float));
-        if (e == hipSuccess) e = hipMalloc(&w.counters, sbpi::WS_COUNTERS * sizeof(uint32_t));
-        if (e == hipSuccess) e = sbpi::zero_u32(w.counters, sbpi::WS_COUNTERS, s);
         if (e != hipSuccess) {
-            if (w.ws) (void)hipFree(w.ws);
-            if (w.counters) (void)hipFree(w.counters);
             w = Workspace{};
             g_last_hip = (int)e;
             return SBP_ERR_HIP;
@@ -226,7 +221,7 @@ int run(const sbpi::Gemm &g, hipStream_t s) {
             int rc = workspace_for(s, &w);
             if (rc) return rc;
         }
-        e = sbpi::launch_bf16(g, p, w.ws, w.counters, s);
+        e = sbpi::launch_bf16(g, p, w.ws, s);
     }
     if (e != hipSuccess) {
         g_last_hip = (int)e;
@@ -368,8 +363,8 @@ const char *sbp_strerror(int code) {
 int sbp_last_hip_error(void) { return g_last_hip; }
 
 int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype, int32_t out_dtype,
-             int32_t *tile_m, int32_t *tile_n, int32_t *splits) {
-    if (!tile_m || !tile_n || !splits) return SBP_ERR_NULL;
+             int32_t *tile_m, int32_t *tile_n, int32_t *splits, int32_t *kernel) {
+    if (!tile_m || !tile_n || !splits || !kernel) return SBP_ERR_NULL;
     if (m < 0 || n < 0 || k < 0 || m > INT32_MAX || n > INT32_MAX || k > INT32_MAX ||
         op < 0 || op > 2)
         return SBP_ERR_SHAPE;
@@ -380,23 +375,29 @@ int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype, int32_t 
         *tile_m = 64;
         *tile_n = 64;
         *splits = 1;
+        *kernel = 3;
         return SBP_OK;
     }
-    sbpi::Gemm g{op, in_dtype, out_dtype, nullptr, 0, nullptr, 0, nullptr, 0, m, n, k};
+    // Plan for 16-byte aligned operands with tight leading dimensions.
+    static const char aligned[16] __attribute__((aligned(16))) = {0};
+    const int64_t lda = (op == 2) ? m : k, ldb = (op == 1) ? k : n;
+    sbpi::Gemm g{op, in_dtype, out_dtype, aligned, lda, aligned, ldb, nullptr, 0, m, n, k};
     sbpi::Plan p = sbpi::plan_bf16(g);
     *tile_m = p.bm;
     *tile_n = p.bn;
     *splits = p.splits;
+    *kernel = p.dma ? 1 : 2;
     return SBP_OK;
 }
 
-int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits) {
+int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits, int32_t kernel) {
     if (tile_m == 0) {
-        sbpi::set_override(0, 0, 1);
+        sbpi::set_override(0, 0, 1, 0);
         return SBP_OK;
     }
-    if (!sbpi::tile_supported(tile_m, tile_n) || splits < 1) return SBP_ERR_SHAPE;
-    sbpi::set_override(tile_m, tile_n, splits);
+    if (kernel < 0 || kernel > 2) return SBP_ERR_SHAPE;
+    if (!sbpi::tile_supported(tile_m, tile_n, true) || splits < 1) return SBP_ERR_SHAPE;
+    sbpi::set_override(tile_m, tile_n, splits, kernel);
     return SBP_OK;
 }
 

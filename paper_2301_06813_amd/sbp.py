@@ -105,8 +105,8 @@ def lib():
         L.sbp_last_hip_error.argtypes = []
         L.sbp_plan.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32),
-                               P(ctypes.c_int32), P(ctypes.c_int32)]
-        L.sbp_set_plan_override.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
+                               P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_int32)]
+        L.sbp_set_plan_override.argtypes = [ctypes.c_int32] * 4
         for fn in EXPORTS:
             if fn != "sbp_strerror":
                 getattr(L, fn).restype = ctypes.c_int
@@ -193,13 +193,17 @@ def sbp_last_hip_error() -> int:
     return lib().sbp_last_hip_error()
 
 
+KERNEL_AUTO, KERNEL_PIPELINED, KERNEL_GENERIC, KERNEL_F32 = 0, 1, 2, 3
+
+
 def sbp_plan(op: int, m: int, n: int, k: int, in_dtype: int, out_dtype: int):
-    """(tile_m, tile_n, splits) the library would launch for this product."""
-    tm, tn, sp = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    """(tile_m, tile_n, splits, kernel) the library would launch for this product
+    with aligned operands; kernel is KERNEL_PIPELINED, KERNEL_GENERIC or KERNEL_F32."""
+    tm, tn, sp, kn = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     _check(lib().sbp_plan(op, m, n, k, in_dtype, out_dtype, ctypes.byref(tm), ctypes.byref(tn),
-                          ctypes.byref(sp)))
-    return tm.value, tn.value, sp.value
+                          ctypes.byref(sp), ctypes.byref(kn)))
+    return tm.value, tn.value, sp.value, kn.value
 
 
-def sbp_set_plan_override(tile_m: int, tile_n: int, splits: int) -> None:
-    _check(lib().sbp_set_plan_override(tile_m, tile_n, splits))
+def sbp_set_plan_override(tile_m: int, tile_n: int, splits: int, kernel: int = 0) -> None:
+    _check(lib().sbp_set_plan_override(tile_m, tile_n, splits, kernel))

@@ -223,11 +223,20 @@ def test_strerror_and_plan(L):
     for code in range(-8, 1):
         assert sbp.sbp_strerror(code) and "unknown" not in sbp.sbp_strerror(code)
     assert "unknown" in sbp.sbp_strerror(-99)
-    tm, tn, s = sbp.sbp_plan(2, 1024, 384, 8192, sbp.SBP_BF16, sbp.SBP_BF16)
+    tm, tn, s, kn = sbp.sbp_plan(2, 1024, 384, 8192, sbp.SBP_BF16, sbp.SBP_BF16)
     assert (tm, tn) in {(256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)}
-    assert s >= 1
+    assert s >= 1 and kn == sbp.KERNEL_PIPELINED
+    # a reduction that is not a multiple of 8 cannot use the pipelined kernel
+    assert sbp.sbp_plan(0, 256, 256, 125, BF, BF)[3] == sbp.KERNEL_GENERIC
+    assert sbp.sbp_plan(0, 64, 64, 64, F32, F32)[3] == sbp.KERNEL_F32
     with pytest.raises(sbp.SbpError):
         sbp.sbp_set_plan_override(96, 96, 1)
+    with pytest.raises(sbp.SbpError):
+        sbp.sbp_set_plan_override(64, 64, 1, 5)
     sbp.sbp_set_plan_override(64, 64, 3)
-    assert sbp.sbp_plan(0, 100, 100, 1000, BF, BF) == (64, 64, 3)
+    assert sbp.sbp_plan(0, 128, 128, 1024, BF, BF) == (64, 64, 3, sbp.KERNEL_PIPELINED)
+    sbp.sbp_set_plan_override(256, 128, 2, sbp.KERNEL_GENERIC)
+    assert sbp.sbp_plan(0, 128, 128, 1024, BF, BF) == (256, 128, 2, sbp.KERNEL_GENERIC)
+    with pytest.raises(sbp.SbpError):
+        sbp.sbp_set_plan_override(256, 256, 1)
     sbp.sbp_set_plan_override(0, 0, 1)

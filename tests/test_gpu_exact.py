@@ -14,7 +14,7 @@ import torch
 import oracle
 from paper_2301_06813_amd import inputs, linear, sbp
 
-from helpers import TILES, decode, expect_state, oracle_full, out_bits, run_gpu, say
+from helpers import KERNELS, TILES, decode, expect_state, oracle_full, out_bits, run_gpu, say
 
 pytestmark = pytest.mark.gpu
 SIGS = ("DP", "COL", "KS")
@@ -52,18 +52,21 @@ def test_exact_all_signatures_default_plan(shape):
                     _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
 
 
+@pytest.mark.parametrize("kernel", KERNELS, ids=["pipelined", "generic"])
 @pytest.mark.parametrize("tile", TILES, ids=["%dx%d" % t for t in TILES])
-def test_exact_every_tile_and_split(tile):
-    M, K, N = 300, 1100, 270
+def test_exact_every_tile_and_split(tile, kernel):
+    # sizes are multiples of 8 (so the pipelined kernel is eligible) but not
+    # of any tile: every dimension has a ragged last tile
+    M, K, N = 304, 1104, 272
     X, W, dY = _int_inputs(M, K, N, 200)
     Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
     p, r = 2, 1
     try:
         for splits in (1, 3, 7):
-            sbp.sbp_set_plan_override(tile[0], tile[1], splits)
+            sbp.sbp_set_plan_override(tile[0], tile[1], splits, kernel)
             for sig in SIGS:
                 for op in OPS:
-                    say("tile", tile, "splits", splits, sig, op)
+                    say("tile", tile, "kernel", kernel, "splits", splits, sig, op)
                     _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
     finally:
         sbp.sbp_set_plan_override(0, 0, 1)
@@ -150,8 +153,8 @@ def test_guard_bands_untouched():
     # the guard stays NaN and every element of the share is written.
     M, K, N, p = 150, 200, 140, 3
     X, W, dY = _int_inputs(M, K, N, 700)
-    for tile in TILES:
-        sbp.sbp_set_plan_override(tile[0], tile[1], 2)
+    for tile, kernel in [(t, k) for t in TILES for k in KERNELS]:
+        sbp.sbp_set_plan_override(tile[0], tile[1], 2, kernel)
         try:
             for sig in SIGS:
                 for op in OPS:
@@ -165,8 +168,8 @@ def test_guard_bands_untouched():
                     torch.cuda.synchronize()
                     guard = torch.ones_like(buf, dtype=torch.bool)
                     guard[1:rows + 1, 2:2 + cols] = False
-                    assert torch.all(torch.isnan(buf[guard])), (tile, sig, op)
-                    assert not torch.any(torch.isnan(out)), (tile, sig, op)
+                    assert torch.all(torch.isnan(buf[guard])), (tile, kernel, sig, op)
+                    assert not torch.any(torch.isnan(out)), (tile, kernel, sig, op)
         finally:
             sbp.sbp_set_plan_override(0, 0, 1)
 
@@ -176,9 +179,9 @@ def test_split_reduction_is_deterministic():
     g = torch.Generator(device="cuda").manual_seed(3)
     X = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
     dY = torch.randn((M, N), generator=g, device="cuda").to(torch.bfloat16)
-    sbp.sbp_set_plan_override(128, 128, 5)
     try:
-        for sig in ("DP", "COL"):
+        for sig, kernel in (("DP", 1), ("COL", 1), ("DP", 2), ("COL", 2)):
+            sbp.sbp_set_plan_override(128, 128, 5, kernel)
             a, _ = run_gpu("bwd_weight", sig, 1, 0, X, None, dY)
             b, _ = run_gpu("bwd_weight", sig, 1, 0, X, None, dY)
             assert torch.equal(a, b)
