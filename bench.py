@@ -36,10 +36,43 @@ RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
 OPS = ("fwd", "bwd_data", "bwd_weight")
 ORIENT = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2}
 KMAJ = {"fwd": ("true", "false"), "bwd_data": ("true", "true"), "bwd_weight": ("false", "false")}
+# pipelined kernel instances: (tile_m, tile_n) -> (reduction step, stages, wave rows, wave cols)
+DMA_SHAPE = {(256, 256): (64, 2, 2, 4), (256, 128): (64, 3, 2, 2), (128, 256): (64, 3, 2, 2)}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the library's kernel and host sources (sorted by name)."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2301_06813_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".h", ".hip", ".cpp")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+def counted_traffic(kernel: str):
+    """HBM bytes per dispatch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy), or None if
+    the summary is missing, lacks this kernel, or was taken from other
+    kernel sources."""
+    path = os.path.join(ROOT, "profiles", "gemm_bf16_transformer_step_hbm_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    if "Kernel sources sha256: " + kernel_source_hash() not in text:
+        return None
+    for line in text.splitlines():
+        cells = [c.strip().strip("`") for c in line.split("|")]
+        if len(cells) > 5 and cells[1].replace("sbpk::", "") == kernel:
+            return float(cells[5]) * 1e6
+    return None
 
 
 class Step:
@@ -78,12 +111,13 @@ class Step:
                 tm, tn, sp, kn = sbp.sbp_plan(ORIENT[op], m, n, k, sbp.SBP_BF16,
                                               sbp.SBP_F32 if ob == 4 else sbp.SBP_BF16)
                 if kn == sbp.KERNEL_PIPELINED:
-                    ns = {(256, 256): 2, (256, 128): 3, (128, 256): 3}.get((tm, tn), 4)
-                    kern = "gemm_bf16_dma_kernel<%d, %d, %d, %s, %s, %s>" % (
-                        tm, tn, ns, KMAJ[op][0], KMAJ[op][1], "true" if ob == 4 else "false")
+                    bkd, ns, wgm, wgn = DMA_SHAPE.get((tm, tn), (64, 4, 2, 2))
+                    kern = "gemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %s, %s, %s>" % (
+                        tm, tn, bkd, ns, wgm, wgn, KMAJ[op][0], KMAJ[op][1],
+                        "true" if (ob == 4 or sp > 1) else "false")
                 else:
                     kern = "gemm_bf16_kernel<%d, %d, %s, %s, %s>" % (
-                        tm, tn, KMAJ[op][0], KMAJ[op][1], "true" if ob == 4 else "false")
+                        tm, tn, KMAJ[op][0], KMAJ[op][1], "true" if (ob == 4 or sp > 1) else "false")
                 meta = dict(linear=lin.name, sig=lin.sig, op=op, m=m, n=n, k=k,
                             flops=2.0 * m * n * k, bytes=2.0 * (m * k + k * n) + ob * m * n,
                             kernel=kern, splits=sp)
@@ -115,14 +149,14 @@ class Step:
 
 def cpu_baseline(wl, seconds):
     """The oracle on a bounded sample of the same step: leading output rows of
-    every product of layer 0's four linears, timed on the host cores."""
+    every product of the first four layers' 16 linears, timed on the host cores."""
     import numpy as np
     import oracle
     from paper_2301_06813_amd import inputs, workloads
     sig_id = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS}
     op_id = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
     oracle.build()
-    lins = wl.linears[:4]
+    lins = wl.linears[:16]
     host = []
     for lin in lins:
         X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
@@ -142,12 +176,19 @@ def cpu_baseline(wl, seconds):
                 fl += lin.flops_per_op(wl.p) * nr / rows
         return fl, time.perf_counter() - t0
 
-    fl1, t1 = run(1)
-    nrows = max(1, int(seconds / max(t1, 1e-6)))
+    # calibrate: double the row sample until it takes a measurable time, then
+    # scale it to the requested duration
+    nrows, t1 = 1, 0.0
+    while True:
+        _, t1 = run(nrows)
+        if t1 >= min(1.0, seconds / 4) or nrows >= 8192:
+            break
+        nrows *= 2
+    nrows = max(1, min(8192, int(nrows * seconds / max(t1, 1e-6))))
     fl, t = run(nrows)
     cores = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
     return {"value": fl / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-            "sample": "first %d output rows of each of the 12 local products of layer 0 "
+            "sample": "first %d output rows of each of the 48 local products of layers 0-3 "
                       "(qkv/out/fc1/fc2 x fwd/bwd_data/bwd_weight), rank 0; %.3g GFLOP in %.1f s"
                       % (nrows, fl / 1e9, t)}
 
@@ -161,6 +202,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager launches, not a graph")
     ap.add_argument("--dump", default=None, help="write per-launch shapes and durations (JSON)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 5 times (scale for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build measures rank r's local products on a "
@@ -170,8 +213,17 @@ def main():
 
     import torch
     from paper_2301_06813_amd import sbp, workloads
-    sbp.lib()
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": src.numel() * 2, "copy_bytes_written": dst.numel() * 2,
+                          "copies": 5}))
+        return
+    sbp.lib()
     wl = workloads.transformer_step()
     log("building step: %d linears, p=%d, rank 0" % (len(wl.linears), wl.p))
     step = Step(wl, 0)
@@ -244,7 +296,10 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": kb / kt / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    hbm = counted_traffic(dom)
+    roof["traffic"] = None if hbm is None else {
+        "hbm_bytes_per_launch": hbm, "algorithmic_bytes_per_launch": kb / kn,
+        "ratio": hbm / (kb / kn), "source": "profiles/gemm_bf16_transformer_step_hbm_counters.md"}
     roof["kernel"] = dom
     roof["launches_per_step"] = kn
     roof["avg_launch_us"] = kt / kn * 1e6

@@ -176,11 +176,11 @@ int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype,
              int32_t *splits, int32_t *kernel);
 
 /* Thread-local override of the bf16 plan for subsequent calls on this
- * thread (tests and tuning). tile_m x tile_n is one of 256x128, 128x256,
- * 128x128, 128x64, 64x128, 64x64; splits >= 1; kernel 0 = the
+ * thread (tests and tuning). tile_m x tile_n is one of 256x256, 256x128,
+ * 128x256, 128x128, 128x64, 64x128, 64x64; splits >= 1; kernel 0 = the
  * library's choice, 1 = pipelined direct-to-LDS, 2 = generic. A call whose
- * operands the pipelined kernel cannot read runs the generic kernel; splits
- * are clamped to the reduction blocks and
+ * operands the pipelined kernel cannot read runs the generic kernel, where
+ * 256x256 becomes 256x128; splits are clamped to the reduction blocks and
  * to the workspace. tile_m = 0 clears the override.
  * Errors: SBP_ERR_SHAPE for an unknown tile shape, splits < 1 or kernel
  * outside 0..2. */

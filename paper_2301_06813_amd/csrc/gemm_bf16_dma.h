@@ -5,16 +5,22 @@
 // elements, so each 16-byte chunk of an operand is either wholly inside or
 // wholly outside it.
 //
-// Design (one workgroup = 4 waves = 256 threads, 2 x 2 wave grid):
+// Design:
+//   * Workgroups of 4 waves (2 x 2) or 8 waves (2 x 4, two per SIMD, for
+//     the 256 x 256 tile, whose 128 fp32 accumulator registers per wave
+//     leave room for two waves per SIMD).
 //   * Operand tiles move HBM -> LDS with buffer loads that write LDS
 //     directly (16 bytes per lane, lane l's bytes at base + 16 l); no
 //     registers are spent on staging, so NS pipeline stages (2-4, as LDS
 //     allows) are in flight: the loads of step t + NS - 1 are issued while
 //     step t computes, hiding HBM latency behind NS - 1 steps of MFMA work.
 //     Chunks outside the operand get an out-of-range offset and read as 0.
-//   * k-major operand tiles keep their storage order in LDS: one 128-byte
-//     row of 64 reduction values per output row, 16-byte chunks XOR-swizzled
-//     by row; fragments are read with ds_read_b128.
+//   * The reduction step BKD is a template parameter (64 for every instance;
+//     32 is supported for deeper pipelines but its row swizzle is not yet free
+//     of bank conflicts on gfx950).
+//   * k-major operand tiles keep their storage order in LDS: one row of BKD
+//     reduction values per output row, 16-byte chunks XOR-swizzled by row;
+//     fragments are read with ds_read_b128.
 //   * m/n-major operand tiles also keep their storage order: one row of BMN
 //     values per reduction index, chunks XOR-swizzled by 4 (row % 4); MFMA
 //     fragments (8 consecutive reduction values of one output index per
@@ -64,22 +70,36 @@ __device__ __forceinline__ void dma16(i32x4 r, char *lds, int voff) {
 }
 
 // ---------------------------------------------------------------- k-major
-// LDS: BMN rows x 128 B; chunk c of row r at r*128 + 16*(c ^ sw8(r)).
-template <int BMN>
+// LDS: BMN rows x RB bytes (RB = 2 BK: 64 reduction values in 8 chunks of
+// 16 B, or 32 in 4). Chunk c of row r sits at r*RB + 16*(c ^ f(r)); f makes
+// the 16-byte fragment reads of 8 consecutive rows (32 banks) and of 16
+// (64 banks) hit distinct banks.
+template <int BMN, int NW, int BK_>
 struct KTileDma {
-    static constexpr int SEGS = BMN / 8;          // 1 KB segments (8 rows each)
-    static constexpr int PER_WAVE = SEGS / 4;     // segments each wave loads
+    static constexpr int RB = BK_ * 2;            // bytes per row
+    static constexpr int CPR = BK_ / 8;           // chunks per row
+    static constexpr int RPS = 1024 / RB;         // rows per 1 KB segment
+    static constexpr int SEGS = BMN * RB / 1024;
+    static constexpr int PER_WAVE = SEGS / NW;    // segments each wave loads
+    static_assert(SEGS % NW == 0, "tile too small for the wave count");
 
-    // Issue the loads of one stage: rows [mn0, mn0+BMN) x reduction [k0, k0+64).
+    __device__ __forceinline__ static int swz(int row) {
+        return CPR == 8 ? ((row & 7) ^ ((row >> 3) & 7)) : (((row >> 1) ^ (row >> 3)) & 3);
+    }
+    __device__ __forceinline__ static int off(int row, int c) {
+        return row * RB + ((c ^ swz(row)) << 4);
+    }
+
+    // Issue the loads of one stage: rows [mn0, mn0+BMN) x reduction [k0, k0+BK_).
     __device__ __forceinline__ static void issue(const uint16_t *base, int64_t ld, int mn0,
                                                  int mn_lim, int k0, int k_lim, char *lds,
                                                  int wave, int lane) {
         const i32x4 r = make_rsrc(base + (int64_t)mn0 * ld + k0);
 #pragma unroll
         for (int i = 0; i < PER_WAVE; ++i) {
-            const int s = i * 4 + wave;
-            const int row = s * 8 + (lane >> 3);
-            const int c = (lane & 7) ^ ((row & 7) ^ ((row >> 3) & 7));
+            const int s = i * NW + wave;
+            const int row = s * RPS + lane / CPR;
+            const int c = (lane % CPR) ^ swz(row);
             const bool ok = (mn0 + row < mn_lim) && (k0 + c * 8 + 8 <= k_lim);
             const int voff = ok ? (int)((row * ld + c * 8) * 2) : OOB;
             dma16(r, lds + s * 1024, voff);
@@ -90,19 +110,20 @@ struct KTileDma {
     __device__ __forceinline__ static bf16x8 frag(const char *lds, int r0, int ks, int lane) {
         const int row = r0 + (lane & 31);
         const int chunk = ks * 2 + (lane >> 5);
-        return *reinterpret_cast<const bf16x8 *>(lds + lds_off(row, chunk));
+        return *reinterpret_cast<const bf16x8 *>(lds + off(row, chunk));
     }
 };
 
 // ---------------------------------------------------------------- m/n-major
-// LDS: 64 rows (reduction index) x BMN values; chunk c of row r at
+// LDS: BK rows (reduction index) x BMN values; chunk c of row r at
 // r*RB + 16*(c ^ (4*(r%4) % CPR)) with RB = 2*BMN bytes, CPR chunks per row.
-template <int BMN>
+template <int BMN, int NW, int BK_>
 struct MNTileDma {
     static constexpr int RB = BMN * 2;            // bytes per row
     static constexpr int CPR = BMN / 8;           // chunks per row
-    static constexpr int SEGS = BMN / 8;          // 1 KB segments in the 64-row tile
-    static constexpr int PER_WAVE = SEGS / 4;
+    static constexpr int SEGS = BMN * BK_ * 2 / 1024;   // 1 KB segments in the BK_-row tile
+    static constexpr int PER_WAVE = SEGS / NW;
+    static_assert(SEGS % NW == 0, "tile too small for the wave count");
 
     __device__ __forceinline__ static int swz(int row) {
         return CPR >= 16 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
@@ -114,7 +135,7 @@ struct MNTileDma {
         const i32x4 r = make_rsrc(base + (int64_t)k0 * ld + mn0);
 #pragma unroll
         for (int i = 0; i < PER_WAVE; ++i) {
-            const int s = i * 4 + wave;
+            const int s = i * NW + wave;
             const int byte = s * 1024 + lane * 16;
             const int row = byte / RB;
             const int phys = (byte % RB) >> 4;
@@ -144,27 +165,32 @@ struct MNTileDma {
     }
 };
 
-template <int BMN, bool KMAJ>
-using DmaTileOf = typename std::conditional<KMAJ, KTileDma<BMN>, MNTileDma<BMN>>::type;
+template <int BMN, int NW, int BK_, bool KMAJ>
+using DmaTileOf =
+    typename std::conditional<KMAJ, KTileDma<BMN, NW, BK_>, MNTileDma<BMN, NW, BK_>>::type;
 
 template <int N>
 __device__ __forceinline__ void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int BM, int BN, int NS, bool A_KMAJ, bool B_KMAJ, bool OUT_F32>
-__global__ __launch_bounds__(NT) void gemm_bf16_dma_kernel(GemmArgs g) {
-    constexpr int WM = BM / 2, WN = BN / 2;
+// WGM x WGN waves per workgroup (2 x 2, or 2 x 4 for the 256 x 256 tile:
+// 8 waves, two per SIMD, each owning 128 x 64 outputs).
+template <int BM, int BN, int BKD, int NS, int WGM, int WGN, bool A_KMAJ, bool B_KMAJ,
+          bool OUT_F32>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_kernel(GemmArgs g) {
+    constexpr int NW = WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int MI = WM / 32, NI = WN / 32;
-    constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;   // 64 reduction values per stage
+    constexpr int A_BYTES = BM * BKD * 2, B_BYTES = BN * BKD * 2;   // one stage
     constexpr int STAGE = A_BYTES + B_BYTES;
-    constexpr int LOADS = (BM / 32) + (BN / 32);            // dma instructions per thread per stage
+    constexpr int LOADS = STAGE / 1024 / NW;                         // dma per thread per stage
     __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
 
     const int tiles = g.tiles_m * g.tiles_n;
     const int L = remap_xcd(blockIdx.x, tiles * g.splits);
@@ -178,18 +204,17 @@ __global__ __launch_bounds__(NT) void gemm_bf16_dma_kernel(GemmArgs g) {
     const int tn = (t % (GROUP * g.tiles_n)) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    const int kb_total = (g.k + BK - 1) / BK;
-    const int kb_begin = split * g.kblk_per_split;
-    const int kb_end = min(kb_total, kb_begin + g.kblk_per_split);
-    const int nkb = max(0, kb_end - kb_begin);
-    const int k_lim = min(g.k, kb_end * BK);
+    // this split's reduction range [k_begin, k_lim)
+    const int k_begin = split * g.kchunk;
+    const int k_lim = min(g.k, k_begin + g.kchunk);
+    const int nkb = max(0, (k_lim - k_begin + BKD - 1) / BKD);
 
-    using TA = DmaTileOf<BM, A_KMAJ>;
-    using TB = DmaTileOf<BN, B_KMAJ>;
+    using TA = DmaTileOf<BM, NW, BKD, A_KMAJ>;
+    using TB = DmaTileOf<BN, NW, BKD, B_KMAJ>;
 
     auto issue = [&](int kb, int stage) {
         char *base = smem + stage * STAGE;
-        const int k0 = (kb_begin + kb) * BK;
+        const int k0 = k_begin + kb * BKD;
         TA::issue(g.A, g.lda, m0, g.m, k0, k_lim, base, wave, lane);
         TB::issue(g.B, g.ldb, n0, g.n, k0, k_lim, base + A_BYTES, wave, lane);
     };
@@ -218,7 +243,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_dma_kernel(GemmArgs g) {
 
         const char *cur = smem + (it % NS) * STAGE;
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
+        for (int ks = 0; ks < BKD / 16; ++ks) {
             bf16x8 af[MI], bfr[NI];
 #pragma unroll
             for (int i = 0; i < MI; ++i)

@@ -64,7 +64,7 @@ struct GemmArgs {
     int32_t m, n, k;
     int32_t tiles_m, tiles_n;
     int32_t splits;             // reduction splits (>= 1)
-    int32_t kblk_per_split;     // BK-blocks per split
+    int32_t kchunk;             // reduction elements per split (a multiple of 64)
     float *ws;                  // split partials: splits slices of m x n floats
     int32_t vec_a, vec_b;       // operand base and ld allow aligned 16-byte loads
 };
@@ -252,11 +252,10 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     const int tn = (t % (GROUP * g.tiles_n)) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    const int kb_total = (g.k + BK - 1) / BK;
-    const int kb_begin = split * g.kblk_per_split;
-    const int kb_end = min(kb_total, kb_begin + g.kblk_per_split);
-    const int nkb = max(0, kb_end - kb_begin);
-    const int k_lim = min(g.k, kb_end * BK);
+    const int k_begin = split * g.kchunk;
+    const int k_lim = min(g.k, k_begin + g.kchunk);
+    const int nkb = max(0, (k_lim - k_begin + BK - 1) / BK);
+    const int kb_begin = k_begin / BK;
 
     TileOf<BM, A_KMAJ> ta;
     TileOf<BN, B_KMAJ> tb;

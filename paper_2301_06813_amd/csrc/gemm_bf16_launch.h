@@ -17,10 +17,11 @@ static hipError_t launch_tile(int bm, int bn, bool dma, const sbpk::GemmArgs &a,
                            dim3(sbpk::NT), 0, s, a);                                        \
         return hipGetLastError();                                                           \
     }
-#define SBP_DMA_TILE(BM_, BN_, NS_)                                                         \
+#define SBP_DMA_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_)                                       \
     if (dma && bm == BM_ && bn == BN_) {                                                    \
-        hipLaunchKernelGGL((sbpk::gemm_bf16_dma_kernel<BM_, BN_, NS_, AK, BK_, OUTF>),      \
-                           dim3(grid), dim3(sbpk::NT), 0, s, a);                            \
+        hipLaunchKernelGGL(                                                                 \
+            (sbpk::gemm_bf16_dma_kernel<BM_, BN_, BKD_, NS_, WGM_, WGN_, AK, BK_, OUTF>),   \
+            dim3(grid), dim3(64 * WGM_ * WGN_), 0, s, a);                                   \
         return hipGetLastError();                                                           \
     }
     SBP_TILE(256, 128)
@@ -29,12 +30,13 @@ static hipError_t launch_tile(int bm, int bn, bool dma, const sbpk::GemmArgs &a,
     SBP_TILE(128, 64)
     SBP_TILE(64, 128)
     SBP_TILE(64, 64)
-    SBP_DMA_TILE(256, 128, 3)
-    SBP_DMA_TILE(128, 256, 3)
-    SBP_DMA_TILE(128, 128, 4)
-    SBP_DMA_TILE(128, 64, 4)
-    SBP_DMA_TILE(64, 128, 4)
-    SBP_DMA_TILE(64, 64, 4)
+    SBP_DMA_TILE(256, 256, 64, 2, 2, 4)
+    SBP_DMA_TILE(256, 128, 64, 3, 2, 2)
+    SBP_DMA_TILE(128, 256, 64, 3, 2, 2)
+    SBP_DMA_TILE(128, 128, 64, 4, 2, 2)
+    SBP_DMA_TILE(128, 64, 64, 4, 2, 2)
+    SBP_DMA_TILE(64, 128, 64, 4, 2, 2)
+    SBP_DMA_TILE(64, 64, 64, 4, 2, 2)
 #undef SBP_TILE
 #undef SBP_DMA_TILE
     return hipErrorInvalidValue;
@@ -55,7 +57,7 @@ static hipError_t launch_orient(const Gemm &g, const Plan &p, float *ws, hipStre
     a.tiles_m = (int32_t)((g.m + p.bm - 1) / p.bm);
     a.tiles_n = (int32_t)((g.n + p.bn - 1) / p.bn);
     a.splits = p.splits;
-    a.kblk_per_split = p.kblk_per_split;
+    a.kchunk = p.kblk_per_split * 64;
     a.ws = ws;
     a.vec_a = ((reinterpret_cast<uintptr_t>(g.A) & 15) == 0) && (g.lda % 8 == 0);
     a.vec_b = ((reinterpret_cast<uintptr_t>(g.B) & 15) == 0) && (g.ldb % 8 == 0);

@@ -30,7 +30,7 @@ const TileClass kGeneric[] = {
 };
 // Pipelined direct-to-LDS kernel.
 const TileClass kDma[] = {
-    {256, 128, 1, 1.0}, {128, 256, 1, 1.0}, {128, 128, 1, 1.0},
+    {256, 256, 1, 1.0}, {256, 128, 1, 1.0}, {128, 256, 1, 1.0}, {128, 128, 1, 1.0},
     {128, 64, 1, 1.0},  {64, 128, 1, 1.0},  {64, 64, 2, 1.0},
 };
 
@@ -131,7 +131,7 @@ Plan plan_bf16(const Gemm &g) {
         // kernel: 0 either, 1 pipelined (if eligible), 2 generic
         const bool use_dma = dma && ov_kernel != 2;
         Plan p{ov_bm, ov_bn, 1, 1, use_dma};
-        if (!tile_supported(p.bm, p.bn, use_dma)) p.bn = 128;   // no 256x256 instance
+        if (!tile_supported(p.bm, p.bn, use_dma)) p.bn = 128;   // 256x256 only pipelined
         split_of(kb_total, ov_splits, &p.splits, &p.kblk_per_split);
         while (p.splits > 1 && !fits_ws(g, p.splits))
             split_of(kb_total, p.splits - 1, &p.splits, &p.kblk_per_split);

@@ -224,7 +224,8 @@ def test_strerror_and_plan(L):
         assert sbp.sbp_strerror(code) and "unknown" not in sbp.sbp_strerror(code)
     assert "unknown" in sbp.sbp_strerror(-99)
     tm, tn, s, kn = sbp.sbp_plan(2, 1024, 384, 8192, sbp.SBP_BF16, sbp.SBP_BF16)
-    assert (tm, tn) in {(256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)}
+    assert (tm, tn) in {(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128),
+                        (64, 64)}
     assert s >= 1 and kn == sbp.KERNEL_PIPELINED
     # a reduction that is not a multiple of 8 cannot use the pipelined kernel
     assert sbp.sbp_plan(0, 256, 256, 125, BF, BF)[3] == sbp.KERNEL_GENERIC
@@ -235,8 +236,10 @@ def test_strerror_and_plan(L):
         sbp.sbp_set_plan_override(64, 64, 1, 5)
     sbp.sbp_set_plan_override(64, 64, 3)
     assert sbp.sbp_plan(0, 128, 128, 1024, BF, BF) == (64, 64, 3, sbp.KERNEL_PIPELINED)
-    sbp.sbp_set_plan_override(256, 128, 2, sbp.KERNEL_GENERIC)
+    sbp.sbp_set_plan_override(256, 256, 2, sbp.KERNEL_GENERIC)
     assert sbp.sbp_plan(0, 128, 128, 1024, BF, BF) == (256, 128, 2, sbp.KERNEL_GENERIC)
+    sbp.sbp_set_plan_override(256, 256, 2, sbp.KERNEL_PIPELINED)
+    assert sbp.sbp_plan(0, 128, 128, 1024, BF, BF) == (256, 256, 2, sbp.KERNEL_PIPELINED)
     with pytest.raises(sbp.SbpError):
-        sbp.sbp_set_plan_override(256, 256, 1)
+        sbp.sbp_set_plan_override(512, 256, 1)
     sbp.sbp_set_plan_override(0, 0, 1)
