@@ -5,15 +5,17 @@ Workload (the step): the 96 linear layers of a 24-layer Transformer (hidden
 1024, ffn 4096, 16 heads, 8192 global tokens, p = 8 devices), each with its
 own seeded SBP signature from {DP (S(0),B)->S(0), COL (B,S(1))->S(1),
 KS (S(1),S(0))->P}; rank 0's share runs: every forward in layer order, then
-every backward-data and backward-weight product in reverse order, 288
-launches of the library's kernels on one HIP stream. Inputs are seeded
+the backward-data and backward-weight products of each linear in reverse
+order, 288 local products on one HIP stream. Inputs are seeded
 synthetic tensors resident in HBM (the global X, W and dY of every linear;
 the library reads rank 0's shares in place).
 
 `value` is whole-step TFLOP/s (sum of 2 m n k over the 288 local products,
 divided by the measured step time); the step is replayed from a HIP graph
-captured once after warm-up. Per-kernel durations come from HIP events
-around every launch in a separate eager pass over the same steps.
+captured once after warm-up. The backward products of each linear go
+through one sbp_linear_bwd call (they are independent and share one
+launch). Per-kernel durations come from HIP events that the library records
+with each kernel dispatch, in a separate eager pass over the same steps.
 
 Prints one JSON line. Only one GPU: --gpus above 1 exits with a message.
 """
@@ -34,10 +36,6 @@ HBM_PEAK_GBS = 8000.0
 RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
 
 OPS = ("fwd", "bwd_data", "bwd_weight")
-ORIENT = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2}
-KMAJ = {"fwd": ("true", "false"), "bwd_data": ("true", "true"), "bwd_weight": ("false", "false")}
-# pipelined kernel instances: (tile_m, tile_n) -> (reduction step, stages, wave rows, wave cols)
-DMA_SHAPE = {(256, 256): (64, 2, 2, 4), (256, 128): (64, 3, 2, 2), (128, 256): (64, 3, 2, 2)}
 
 
 def log(*a):
@@ -76,14 +74,15 @@ def counted_traffic(kernel: str):
 
 
 class Step:
-    """Rank r's launches of one workload, with all buffers preallocated."""
+    """Rank r's calls of one workload, with all buffers preallocated: every
+    forward product in layer order, then both backward products of each
+    linear (one sbp_linear_bwd call) in reverse order."""
 
     def __init__(self, wl, r, device="cuda"):
+        import ctypes
         import torch
         from paper_2301_06813_amd import linear, sbp, workloads
         self.sbp = sbp
-        self.calls = []       # (fn, args...) in launch order
-        self.meta = []        # per launch: dict(linear, sig, op, m, n, k, flops, bytes, kernel)
         self.keep = []
         fwd, bwd = [], []
         for lin in wl.linears:
@@ -91,60 +90,70 @@ class Step:
             L = linear.layouts(lin.sig, wl.p, r)
             self.keep += [X, W, dY]
             vX, vW, vdY = sbp.view(X), sbp.view(W), sbp.view(dY)
+            outs = {}
             for op in OPS:
                 out = linear.alloc_out(op, lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype, device)
                 self.keep.append(out)
-                vo = sbp.view(out, sbp.SBP_LOCAL)
-                if op == "fwd":
-                    call = ("sbp_linear_fwd", vX, L["x"], vW, L["w"], vo)
-                    m, n = out.shape
-                    k = sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols
-                elif op == "bwd_data":
-                    call = ("sbp_linear_bwd_data", vdY, L["dy"], vW, L["w"], vo)
-                    m, n = out.shape
-                    k = sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols
-                else:
-                    call = ("sbp_linear_bwd_weight", vX, L["x"], vdY, L["dy"], vo)
-                    m, n = out.shape
-                    k = sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows
+                outs[op] = out
+            prods = {}
+            for op, out in outs.items():
+                m, n = out.shape
+                k = {"fwd": sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols,
+                     "bwd_data": sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols,
+                     "bwd_weight": sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows}[op]
                 ob = 4 if out.dtype == torch.float32 else 2
-                tm, tn, sp, kn = sbp.sbp_plan(ORIENT[op], m, n, k, sbp.SBP_BF16,
-                                              sbp.SBP_F32 if ob == 4 else sbp.SBP_BF16)
-                if kn == sbp.KERNEL_PIPELINED:
-                    bkd, ns, wgm, wgn = DMA_SHAPE.get((tm, tn), (64, 4, 2, 2))
-                    kern = "gemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %s, %s, %s>" % (
-                        tm, tn, bkd, ns, wgm, wgn, KMAJ[op][0], KMAJ[op][1],
-                        "true" if (ob == 4 or sp > 1) else "false")
-                else:
-                    kern = "gemm_bf16_kernel<%d, %d, %s, %s, %s>" % (
-                        tm, tn, KMAJ[op][0], KMAJ[op][1], "true" if (ob == 4 or sp > 1) else "false")
-                meta = dict(linear=lin.name, sig=lin.sig, op=op, m=m, n=n, k=k,
-                            flops=2.0 * m * n * k, bytes=2.0 * (m * k + k * n) + ob * m * n,
-                            kernel=kern, splits=sp)
-                (fwd if op == "fwd" else bwd).append((call, meta))
-        order = fwd + [c for i in range(len(bwd) // 2 - 1, -1, -1) for c in bwd[2 * i:2 * i + 2]]
-        for call, meta in order:
+                prods[op] = dict(m=m, n=n, k=k, flops=2.0 * m * n * k,
+                                 bytes=2.0 * (m * k + k * n) + ob * m * n)
+            vo = {op: sbp.view(out, sbp.SBP_LOCAL) for op, out in outs.items()}
+            f = ("sbp_linear_fwd", (vX, L["x"], vW, L["w"], vo["fwd"]), 1)
+            fwd.append((f, dict(linear=lin.name, sig=lin.sig, ops=("fwd",), **prods["fwd"])))
+            bcall = ("sbp_linear_bwd", (vdY, L["dy"], vX, L["x"], vW, L["w"], vo["bwd_data"]),
+                     (vo["bwd_weight"],))
+            pb = dict(flops=prods["bwd_data"]["flops"] + prods["bwd_weight"]["flops"],
+                      bytes=prods["bwd_data"]["bytes"] + prods["bwd_weight"]["bytes"])
+            bwd.append((bcall, dict(linear=lin.name, sig=lin.sig, ops=("bwd_data", "bwd_weight"),
+                                    data=prods["bwd_data"], weight=prods["bwd_weight"], **pb)))
+        self.calls, self.meta = [], []
+        for call, meta in fwd + bwd[::-1]:
             self.calls.append(call)
             self.meta.append(meta)
         self.flops = sum(m["flops"] for m in self.meta)
-        import ctypes
         L_ = sbp.lib()
-        self._fns = [getattr(L_, c[0]) for c in self.calls]
-        self._args = [tuple(ctypes.byref(a) for a in c[1:]) for c in self.calls]
         self._lo = sbp.sbp_layout_t()
-        self._lo_ref = ctypes.byref(self._lo)
+        self._lo2 = sbp.sbp_layout_t()
+        lo, lo2 = ctypes.byref(self._lo), ctypes.byref(self._lo2)
+        self._bound = []
+        for name, args, extra in self.calls:
+            fn = getattr(L_, name)
+            refs = tuple(ctypes.byref(a) for a in args)
+            if name == "sbp_linear_bwd":
+                refs = refs + (lo, ctypes.byref(extra[0]), lo2)
+            else:
+                refs = refs + (lo,)
+            self._bound.append((fn, refs))
 
-    def launch_all(self, stream, events=None):
+    def launch_all(self, stream):
         import ctypes
         s = ctypes.c_void_p(stream)
-        for i, (fn, a) in enumerate(zip(self._fns, self._args)):
-            if events is not None:
-                events[i][0].record()
-            rc = fn(*a, self._lo_ref, s)
+        for fn, refs in self._bound:
+            rc = fn(*refs, s)
             if rc != 0:
                 raise self.sbp.SbpError(rc, self.sbp.sbp_last_hip_error())
-            if events is not None:
-                events[i][1].record()
+
+    def profile(self, stream):
+        """Per call: [(kernel name, us)] of every kernel it launched, each
+        timed by events recorded with its own dispatch."""
+        import ctypes
+        s = ctypes.c_void_p(stream)
+        out = []
+        for fn, refs in self._bound:
+            self.sbp.sbp_profile_begin(16)
+            rc = fn(*refs, s)
+            ks = self.sbp.sbp_profile_end(16)
+            if rc != 0:
+                raise self.sbp.SbpError(rc, self.sbp.sbp_last_hip_error())
+            out.append(ks)
+        return out
 
 
 def cpu_baseline(wl, seconds):
@@ -261,34 +270,39 @@ def main():
     ms = t0.elapsed_time(t1) / args.steps
     tflops = step.flops / (ms * 1e-3) / 1e12
 
-    # per-kernel durations: HIP events around every launch, on the launch stream
-    log("per-kernel event pass")
+    # per-kernel durations: the library records a HIP event pair with every
+    # kernel dispatch (sbp_profile_begin/end), so host time between launches
+    # is not counted
+    log("per-kernel profile pass")
     n = len(step.calls)
     ksteps = max(1, min(args.steps, 5))
-    durs = [[] for _ in range(n)]
+    per_call = [collections.defaultdict(float) for _ in range(n)]
     with torch.cuda.stream(stream):
         for _ in range(ksteps):
-            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(n)]
-            step.launch_all(sid, ev)
-            torch.cuda.synchronize()
-            for i in range(n):
-                durs[i].append(ev[i][0].elapsed_time(ev[i][1]) * 1e-3)
-    avg = [sum(d) / len(d) for d in durs]
-    if args.dump:
-        with open(args.dump, "w") as f:
-            json.dump([dict(m, us=t * 1e6) for m, t in zip(step.meta, avg)], f)
+            for i, ks in enumerate(step.profile(sid)):
+                for name, us in ks:
+                    per_call[i][name] += us / ksteps
     by_kernel = collections.defaultdict(lambda: [0.0, 0.0, 0.0, 0])
     by_sig = collections.defaultdict(lambda: [0.0, 0.0])
-    for m, t in zip(step.meta, avg):
-        b = by_kernel[m["kernel"]]
-        b[0] += t
-        b[1] += m["flops"]
-        b[2] += m["bytes"]
-        b[3] += 1
-        by_sig[m["sig"]][0] += t
+    launches = []
+    for m, ks in zip(step.meta, per_call):
+        t_call = sum(ks.values()) * 1e-6
+        by_sig[m["sig"]][0] += t_call
         by_sig[m["sig"]][1] += m["flops"]
-    dom, (kt, kf, kb, kn) = max(by_kernel.items(), key=lambda kv: kv[1][0])
+        for name, us in ks.items():
+            b = by_kernel[name]
+            b[0] += us * 1e-6
+            b[3] += 1
+            if name.startswith("gemm"):
+                # the product(s) of the call belong to its GEMM kernel
+                b[1] += m["flops"]
+                b[2] += m["bytes"]
+        launches.append(dict(m, kernels=dict(ks), us=sum(ks.values())))
+    if args.dump:
+        with open(args.dump, "w") as f:
+            json.dump(launches, f)
+    gemms = {k: v for k, v in by_kernel.items() if k.startswith("gemm")}
+    dom, (kt, kf, kb, kn) = max(gemms.items(), key=lambda kv: kv[1][0])
     intensity = kf / kb
     if intensity >= RIDGE:
         roof = {"bound": "mfma", "achieved": kf / kt / 1e12, "peak": BF16_PEAK_TFLOPS,
@@ -320,12 +334,13 @@ def main():
         "data": "synthetic (seeded N(0,1) activations/gradients, N(0,1/K) weights)",
         "config": {"workload": wl.name, "layers": 24, "hidden": 1024, "ffn": 4096,
                    "heads": 16, "tokens": 8192, "p": wl.p, "rank": 0,
-                   "gemms_per_step": n, "gflop_per_step": step.flops / 1e9,
+                   "local_products_per_step": 3 * len(wl.linears),
+                   "calls_per_step": n, "gflop_per_step": step.flops / 1e9,
                    "signatures": dict(collections.Counter(l.sig for l in wl.linears)),
                    "mode": "eager" if args.eager else "hip_graph"},
         "pct_of_bf16_peak": 100.0 * tflops / BF16_PEAK_TFLOPS,
         "per_signature_tflops": {s: v[1] / v[0] / 1e12 for s, v in sorted(by_sig.items())},
-        "kernel_time_sum_ms": sum(avg) * 1e3,
+        "kernel_time_sum_ms": sum(v[0] for v in by_kernel.values()) * 1e3,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -154,6 +154,22 @@ int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx,
                           sbp_view_t *dW, sbp_layout_t *ldw_out,
                           hipStream_t stream);
 
+/* Both backward products of the linear, dX_r = dY_r W_r^T and
+ * dW_r = X_r^T dY_r, in one call (usually one launch). The two products are
+ * independent -- each reads dY and one of X, W (Sec. 4.2 backward path,
+ * Sec. 4.3 gradient states) -- so they share the device: the longer work
+ * items of one run while the shorter ones of the other fill the remaining
+ * compute units. States, shapes, dtype rules and errors are those of
+ * sbp_linear_bwd_data and sbp_linear_bwd_weight; the three input states
+ * must form one signature (else SBP_ERR_SIGNATURE), and dX and dW must not
+ * overlap (SBP_ERR_ALIAS). Results equal the two separate calls up to fp32
+ * summation order. */
+int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy,
+                   const sbp_view_t *X, const sbp_layout_t *lx,
+                   const sbp_view_t *W, const sbp_layout_t *lw, sbp_view_t *dX,
+                   sbp_layout_t *ldx_out, sbp_view_t *dW, sbp_layout_t *ldw_out,
+                   hipStream_t stream);
+
 /* --------------------------------------------------------- utilities --- */
 
 /* Static description of an error code (never NULL). */
@@ -168,22 +184,47 @@ int sbp_last_hip_error(void);
  * dimensions, for input dtype in_dtype, output dtype out_dtype and operand
  * orientation op (0 forward, 1 backward-data, 2 backward-weight). Writes
  * the tile rows and columns, the number of reduction splits and the kernel
- * (1 pipelined direct-to-LDS bf16, 2 generic bf16, 3 fp32). For benchmarks
- * and tests; pure host function.
+ * (1 pipelined direct-to-LDS bf16, 2 generic bf16, 3 fp32, 4 pipelined
+ * bf16 with two stages, two workgroups per compute unit). For benchmarks and
+ * tests; pure host function.
  * Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
 int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype,
              int32_t out_dtype, int32_t *tile_m, int32_t *tile_n,
              int32_t *splits, int32_t *kernel);
 
+/* Plan of sbp_linear_bwd for bf16 inputs with 16-byte aligned operands and
+ * tight leading dimensions: the backward-data product is md x nd over a
+ * reduction of kd with output dtype out_d, the backward-weight product
+ * mw x nw over kw with out_w. Writes whether both run as one grouped launch,
+ * the tile of the backward-data product (shared when grouped), and the
+ * splits and kernel of each product (kernel as in sbp_plan). Pure host
+ * function. Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
+int sbp_plan_bwd(int64_t md, int64_t nd, int64_t kd, int32_t out_d, int64_t mw,
+                 int64_t nw, int64_t kw, int32_t out_w, int32_t *grouped,
+                 int32_t *tile_m, int32_t *tile_n, int32_t *splits_d,
+                 int32_t *splits_w);
+
+/* Per-kernel timing for benchmarks. After sbp_profile_begin(capacity), the
+ * first `capacity` kernels that the library launches from the calling
+ * thread are each bracketed by a HIP event pair recorded with the dispatch
+ * itself (hipExtLaunchKernelGGL). sbp_profile_end stops recording, waits for
+ * those events, writes each kernel's duration in microseconds to us[i] and
+ * its name (NUL-terminated, at most name_len bytes) to names + i*name_len
+ * (either may be NULL), and returns the number of kernels recorded, or
+ * SBP_ERR_HIP. Not for use while a stream is being captured into a graph. */
+int sbp_profile_begin(int capacity);
+int sbp_profile_end(float *us, char *names, int name_len);
+
 /* Thread-local override of the bf16 plan for subsequent calls on this
  * thread (tests and tuning). tile_m x tile_n is one of 256x256, 256x128,
  * 128x256, 128x128, 128x64, 64x128, 64x64; splits >= 1; kernel 0 = the
- * library's choice, 1 = pipelined direct-to-LDS, 2 = generic. A call whose
- * operands the pipelined kernel cannot read runs the generic kernel, where
- * 256x256 becomes 256x128; splits are clamped to the reduction blocks and
- * to the workspace. tile_m = 0 clears the override.
- * Errors: SBP_ERR_SHAPE for an unknown tile shape, splits < 1 or kernel
- * outside 0..2. */
+ * library's choice, 1 = pipelined direct-to-LDS, 2 = generic, 4 = pipelined
+ * with two stages (128x128 only). A call whose operands the pipelined kernel
+ * cannot read runs the generic kernel, where 256x256 becomes 256x128;
+ * splits are clamped to the reduction blocks and to the workspace.
+ * tile_m = 0 clears the override.
+ * Errors: SBP_ERR_SHAPE for an unknown tile shape, splits < 1, kernel
+ * outside {0, 1, 2, 4}, or kernel 4 with a tile other than 128x128. */
 int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits,
                           int32_t kernel);
 

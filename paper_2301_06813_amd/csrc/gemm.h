@@ -34,6 +34,7 @@ struct Plan {
     int splits;            // reduction splits actually launched
     int kblk_per_split;    // 64-wide reduction blocks per split
     bool dma;              // pipelined direct-to-LDS kernel (else the generic kernel)
+    int ns = 0;            // pipelined kernel: stages (0 = the tile's default)
 };
 
 // Whether the pipelined direct-to-LDS kernel can run this product: every
@@ -55,6 +56,14 @@ void set_override(int bm, int bn, int splits, int kernel);   // bm = 0 clears
 // the split reduction into g.C.
 hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, hipStream_t s);
 hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipStream_t s);
+
+// Backward-data (gd) and backward-weight (gw) products of one linear. If
+// plan_bf16_bwd returns true, *pd and *pw share a pipelined tile and
+// launch_bf16_bwd_group runs both in one grid (then the split reductions);
+// otherwise the two products run as separate launches of their own plans.
+bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw);
+hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
+                                 const Plan &pw, float *ws, hipStream_t s);
 hipError_t launch_f32(const Gemm &g, hipStream_t s);
 
 }  // namespace sbpi

@@ -174,18 +174,25 @@ __device__ __forceinline__ void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// WGM x WGN waves per workgroup (2 x 2, or 2 x 4 for the 256 x 256 tile:
-// 8 waves, two per SIMD, each owning 128 x 64 outputs).
+template <int BM, int BN, int BKD, int NS>
+struct DmaStage {
+    static constexpr int A_BYTES = BM * BKD * 2, B_BYTES = BN * BKD * 2;   // one stage
+    static constexpr int BYTES = A_BYTES + B_BYTES;
+};
+
+// One work item (an output tile and a reduction split) of a product, by the
+// whole workgroup: WGM x WGN waves (2 x 2, or 2 x 4 for the 256 x 256 tile:
+// 8 waves, two per SIMD, each owning 128 x 64 outputs). L is the item's
+// logical index in [0, tiles * splits).
 template <int BM, int BN, int BKD, int NS, int WGM, int WGN, bool A_KMAJ, bool B_KMAJ,
           bool OUT_F32>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_kernel(GemmArgs g) {
+__device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, char *smem) {
     constexpr int NW = WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int MI = WM / 32, NI = WN / 32;
-    constexpr int A_BYTES = BM * BKD * 2, B_BYTES = BN * BKD * 2;   // one stage
-    constexpr int STAGE = A_BYTES + B_BYTES;
+    constexpr int A_BYTES = DmaStage<BM, BN, BKD, NS>::A_BYTES;
+    constexpr int STAGE = DmaStage<BM, BN, BKD, NS>::BYTES;
     constexpr int LOADS = STAGE / 1024 / NW;                         // dma per thread per stage
-    __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -193,10 +200,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_kernel(GemmAr
     const int wm = wave / WGN, wn = wave % WGN;
 
     const int tiles = g.tiles_m * g.tiles_n;
-    const int L = remap_xcd(blockIdx.x, tiles * g.splits);
     const int split = L / tiles;
     const int t = L % tiles;
-    constexpr int GROUP = 8;
+    constexpr int GROUP = SBP_TILE_GROUP;
     const int grp = t / (GROUP * g.tiles_n);
     const int first_m = grp * GROUP;
     const int gsize = min(g.tiles_m - first_m, GROUP);
@@ -303,6 +309,42 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_kernel(GemmAr
                 }
             }
         }
+    }
+}
+
+
+template <int BM, int BN, int BKD, int NS, int WGM, int WGN, bool A_KMAJ, bool B_KMAJ,
+          bool OUT_F32>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_kernel(GemmArgs g) {
+    __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
+    const int total = g.tiles_m * g.tiles_n * g.splits;
+    dma_tile_body<BM, BN, BKD, NS, WGM, WGN, A_KMAJ, B_KMAJ, OUT_F32>(
+        g, remap_xcd(blockIdx.x, total), smem);
+}
+
+// The two backward products of one linear in one launch: gd is the
+// backward-data product (both operands k-major), gw the backward-weight
+// product (both m/n-major). They are independent (each reads only dY and one
+// of X, W), so their work items share the grid; the product whose work
+// items are longer is dispatched first (data_first) so that the short items
+// of the other fill the machine behind them.
+template <int BM, int BN, int BKD, int NS, int WGM, int WGN, bool OUTD_F32, bool OUTW_F32>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_bwd_kernel(GemmArgs gd,
+                                                                             GemmArgs gw,
+                                                                             int data_first) {
+    __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
+    const int wd = gd.tiles_m * gd.tiles_n * gd.splits;
+    const int ww = gw.tiles_m * gw.tiles_n * gw.splits;
+    const int b = blockIdx.x;
+    const bool is_data = data_first ? (b < wd) : (b >= ww);
+    if (is_data) {
+        const int local = data_first ? b : b - ww;
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, true, true, OUTD_F32>(gd, remap_xcd(local, wd),
+                                                                      smem);
+    } else {
+        const int local = data_first ? b - wd : b;
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, false, false, OUTW_F32>(gw, remap_xcd(local, ww),
+                                                                        smem);
     }
 }
 

@@ -210,7 +210,13 @@ template <int BMN, bool KMAJ>
 using TileOf = typename std::conditional<KMAJ, KMajorTile<BMN>, MNMajorTile<BMN>>::type;
 
 // Logical tile index of this workgroup: XCD-contiguous runs, see header.
+#ifndef SBP_TILE_GROUP
+#define SBP_TILE_GROUP 8
+#endif
 __device__ __forceinline__ int remap_xcd(int wg, int total) {
+#ifdef SBP_NO_XCD_REMAP
+    return wg;
+#endif
     constexpr int NX = 8;
     int per = total / NX;
     int rem = total % NX;
@@ -244,7 +250,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     const int split = L / tiles;
     const int t = L % tiles;
     // grouped order: runs of GROUP tile-rows, column-major inside a run
-    constexpr int GROUP = 8;
+    constexpr int GROUP = SBP_TILE_GROUP;
     const int grp = t / (GROUP * g.tiles_n);
     const int first_m = grp * GROUP;
     const int gsize = min(g.tiles_m - first_m, GROUP);

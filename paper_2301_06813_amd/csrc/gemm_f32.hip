@@ -8,6 +8,7 @@
 // Products and sums are single fp32 FMAs; the reduction order is
 // increasing k.
 #include "gemm.h"
+#include "profile.h"
 
 namespace sbpk {
 
@@ -119,18 +120,16 @@ hipError_t launch_f32(const Gemm &g, hipStream_t s) {
     const int grid = tiles_m * a.tiles_n;
     switch (g.orient) {
         case OR_FWD:
-            hipLaunchKernelGGL((sbpk::gemm_f32_kernel<true, false>), dim3(grid), dim3(256), 0, s, a);
-            break;
+            return launch_kernel(sbpk::gemm_f32_kernel<true, false>,
+                                 "gemm_f32_kernel<true, false>", dim3(grid), dim3(256), s, a);
         case OR_BWD_DATA:
-            hipLaunchKernelGGL((sbpk::gemm_f32_kernel<true, true>), dim3(grid), dim3(256), 0, s, a);
-            break;
+            return launch_kernel(sbpk::gemm_f32_kernel<true, true>,
+                                 "gemm_f32_kernel<true, true>", dim3(grid), dim3(256), s, a);
         case OR_BWD_WEIGHT:
-            hipLaunchKernelGGL((sbpk::gemm_f32_kernel<false, false>), dim3(grid), dim3(256), 0, s, a);
-            break;
-        default:
-            return hipErrorInvalidValue;
+            return launch_kernel(sbpk::gemm_f32_kernel<false, false>,
+                                 "gemm_f32_kernel<false, false>", dim3(grid), dim3(256), s, a);
     }
-    return hipGetLastError();
+    return hipErrorInvalidValue;
 }
 
 }  // namespace sbpi

@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <unordered_map>
 
 #include "gemm.h"
 
@@ -20,18 +21,22 @@ namespace {
 struct TileClass {
     int bm, bn;
     int occ;      // workgroups that fit one compute unit (LDS-limited)
-    double eff;   // fraction of the CU's MFMA peak the tile sustains when resident
+    double eff;   // rate factor of the tile's operand stream (see model below)
+    int ns;       // pipelined kernel stages (0 = default instance)
 };
 
 // Generic kernel (register-staged, one step ahead): slower per byte.
 const TileClass kGeneric[] = {
-    {256, 128, 1, 0.5}, {128, 256, 1, 0.5}, {128, 128, 2, 0.5},
-    {128, 64, 2, 0.5},  {64, 128, 2, 0.5},  {64, 64, 4, 0.5},
+    {256, 128, 1, 0.5, 0}, {128, 256, 1, 0.5, 0}, {128, 128, 2, 0.5, 0},
+    {128, 64, 2, 0.5, 0},  {64, 128, 2, 0.5, 0},  {64, 64, 4, 0.5, 0},
 };
 // Pipelined direct-to-LDS kernel.
+// The two-stage 128 x 128 instance (64 KB of LDS) runs two workgroups per
+// CU: one's output stores overlap the other's loads, which pays off when the
+// reduction is short and the output large.
 const TileClass kDma[] = {
-    {256, 256, 1, 1.0}, {256, 128, 1, 1.0}, {128, 256, 1, 1.0}, {128, 128, 1, 1.0},
-    {128, 64, 1, 1.0},  {64, 128, 1, 1.0},  {64, 64, 2, 1.0},
+    {256, 256, 1, 1.0, 0}, {256, 128, 1, 1.0, 0}, {128, 256, 1, 1.0, 0}, {128, 128, 1, 1.0, 0},
+    {128, 128, 2, 0.8, 2}, {128, 64, 1, 1.0, 0},  {64, 128, 1, 1.0, 0},  {64, 64, 2, 1.0, 0},
 };
 
 // Time model (measured on MI355X): a workgroup's 64-wide reduction step
@@ -68,25 +73,49 @@ bool fits_ws(const Gemm &g, int splits) {
     return (double)splits * (double)g.m * (double)g.n <= (double)WS_FLOATS;
 }
 
-double model_time(const Gemm &g, const TileClass &t, int splits, int per) {
+// Work items of one product under (tile, splits): count, time per item, and
+// the cost of its split reduction (0 without splits).
+struct Est {
+    double wgs, wg_time, extra;
+};
+
+Est estimate(const Gemm &g, const TileClass &t, int splits, int per) {
     const int64_t tiles = ((g.m + t.bm - 1) / t.bm) * ((g.n + t.bn - 1) / t.bn);
-    const double wgs = (double)tiles * splits;
-    const double rounds = std::ceil(wgs / (kCUs * t.occ));
     const double step_bytes = (t.bm + t.bn) * 128.0;
     const double step = std::max(2.0 * t.bm * t.bn * 64.0 / (kCuPeak * 0.9),
                                  step_bytes * t.occ / (kCuL2 * t.eff));
     const double out_bytes = (splits > 1 || g.out_dtype == DT_F32) ? 4.0 : 2.0;
-    const double epi = t.bm * t.bn * out_bytes * t.occ / kCuL2;
-    double time = rounds * (per * step + epi + kRoundLatency);
-    // the whole product cannot beat HBM for its operands and output
-    const double algo_bytes = 2.0 * (g.m * g.k + g.k * g.n) +
-                              ((g.out_dtype == DT_F32) ? 4.0 : 2.0) * g.m * g.n;
-    time = std::max(time, algo_bytes / kHbm);
+    // output stores overlap other workgroups' loads when two share a CU
+    const double epi = t.bm * t.bn * out_bytes / kCuL2 / t.occ;
+    Est e{(double)tiles * splits, per * step + epi + kRoundLatency / t.occ, 0.0};
     if (splits > 1) {
         const double red = (splits * 4.0 + ((g.out_dtype == DT_F32) ? 4.0 : 2.0)) * g.m * g.n;
-        time += red / kHbm + kLaunch;
+        e.extra = red / kHbm + kLaunch;
     }
-    return time;
+    return e;
+}
+
+double algo_bytes(const Gemm &g) {
+    return 2.0 * (g.m * g.k + g.k * g.n) + ((g.out_dtype == DT_F32) ? 4.0 : 2.0) * g.m * g.n;
+}
+
+double model_time(const Gemm &g, const TileClass &t, int splits, int per) {
+    const Est e = estimate(g, t, splits, per);
+    const double rounds = std::ceil(e.wgs / (kCUs * t.occ));
+    return std::max(rounds * e.wg_time, algo_bytes(g) / kHbm) + e.extra;
+}
+
+// Two products sharing one grid: the longer items are dispatched first and
+// the shorter fill in behind them.
+double model_pair(const Gemm &gd, const Gemm &gw, const TileClass &t, int sd, int pd, int sw,
+                  int pw) {
+    const Est a = estimate(gd, t, sd, pd), b = estimate(gw, t, sw, pw);
+    const Est &lo = (a.wg_time >= b.wg_time) ? a : b;
+    const Est &sh = (a.wg_time >= b.wg_time) ? b : a;
+    const double slots = kCUs * t.occ;
+    const double total = lo.wgs * lo.wg_time + sh.wgs * sh.wg_time;
+    const double mk = std::max(std::ceil(lo.wgs / slots) * lo.wg_time, total / slots + sh.wg_time);
+    return std::max(mk, (algo_bytes(gd) + algo_bytes(gw)) / kHbm) + a.extra + b.extra;
 }
 
 }  // namespace
@@ -123,14 +152,105 @@ bool dma_eligible(const Gemm &g) {
     return g.lda <= (int64_t(1) << 21) && g.ldb <= (int64_t(1) << 21);
 }
 
+static Plan plan_uncached(const Gemm &g);
+
+namespace {
+struct Key {
+    int64_t v[9];
+    bool operator==(const Key &o) const {
+        for (int i = 0; i < 9; ++i)
+            if (v[i] != o.v[i]) return false;
+        return true;
+    }
+};
+struct KeyHash {
+    size_t operator()(const Key &k) const {
+        size_t h = 1469598103934665603ull;
+        for (int i = 0; i < 9; ++i) h = (h ^ (size_t)k.v[i]) * 1099511628211ull;
+        return h;
+    }
+};
+Key key_of(const Gemm &g, bool dma) {
+    return Key{{g.orient, g.in_dtype, g.out_dtype, g.m, g.n, g.k, dma ? 1 : 0,
+                ov_bm * 1000 + ov_bn, ov_splits * 10 + ov_kernel}};
+}
+thread_local std::unordered_map<Key, Plan, KeyHash> plan_cache;
+}  // namespace
+
 Plan plan_bf16(const Gemm &g) {
+    const Key k = key_of(g, dma_eligible(g));
+    auto it = plan_cache.find(k);
+    if (it != plan_cache.end()) return it->second;
+    const Plan p = plan_uncached(g);
+    if (plan_cache.size() > 4096) plan_cache.clear();
+    plan_cache.emplace(k, p);
+    return p;
+}
+
+bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
+    *pd = plan_bf16(gd);
+    *pw = plan_bf16(gw);
+    if (ov_bm != 0 && ov_kernel == 2) return false;
+    if (!dma_eligible(gd) || !dma_eligible(gw)) return false;
+    if (ov_bm != 0) {
+        // an override fixes the tile (and the splits of both products)
+        pw->bm = pd->bm;
+        pw->bn = pd->bn;
+        pw->ns = pd->ns;
+        return pd->dma && pw->dma &&
+               (double)pd->splits * gd.m * gd.n + (double)pw->splits * gw.m * gw.n <=
+                   (double)WS_FLOATS;
+    }
+    const TileClass *sep_d = nullptr, *sep_w = nullptr;
+    for (const TileClass &t : kDma) {
+        if (t.bm == pd->bm && t.bn == pd->bn && t.ns == pd->ns) sep_d = &t;
+        if (t.bm == pw->bm && t.bn == pw->bn && t.ns == pw->ns) sep_w = &t;
+    }
+    if (!sep_d || !sep_w) return false;
+    double best = model_time(gd, *sep_d, pd->splits, pd->kblk_per_split) +
+                  model_time(gw, *sep_w, pw->splits, pw->kblk_per_split);
+    bool grouped = false;
+    const int kd = kblocks(gd.k), kw = kblocks(gw.k);
+    for (const TileClass &t : kDma) {
+        int last_d = 0;
+        for (int a = 1; a <= 16; ++a) {
+            int sd, perd;
+            split_of(kd, a, &sd, &perd);
+            if (sd == last_d) continue;
+            last_d = sd;
+            if (sd > 1 && perd < 2) continue;
+            int last_w = 0;
+            for (int b = 1; b <= 16; ++b) {
+                int sw, perw;
+                split_of(kw, b, &sw, &perw);
+                if (sw == last_w) continue;
+                last_w = sw;
+                if (sw > 1 && perw < 2) continue;
+                const double wsz = (sd > 1 ? (double)sd * gd.m * gd.n : 0.0) +
+                                   (sw > 1 ? (double)sw * gw.m * gw.n : 0.0);
+                if (wsz > (double)WS_FLOATS) continue;
+                const double tm = model_pair(gd, gw, t, sd, perd, sw, perw);
+                if (tm < best * 0.97) {
+                    best = tm;
+                    grouped = true;
+                    *pd = Plan{t.bm, t.bn, sd, perd, true, t.ns};
+                    *pw = Plan{t.bm, t.bn, sw, perw, true, t.ns};
+                }
+            }
+        }
+    }
+    return grouped;
+}
+
+static Plan plan_uncached(const Gemm &g) {
     const int kb_total = kblocks(g.k);
     const bool dma = dma_eligible(g);
     Plan best{128, 128, 1, std::max(1, kb_total), dma};
     if (ov_bm != 0) {
-        // kernel: 0 either, 1 pipelined (if eligible), 2 generic
+        // kernel: 0 either, 1 pipelined (if eligible), 2 generic, 4 pipelined
+        // two-stage 128 x 128 (if eligible)
         const bool use_dma = dma && ov_kernel != 2;
-        Plan p{ov_bm, ov_bn, 1, 1, use_dma};
+        Plan p{ov_bm, ov_bn, 1, 1, use_dma, (use_dma && ov_kernel == 4) ? 2 : 0};
         if (!tile_supported(p.bm, p.bn, use_dma)) p.bn = 128;   // 256x256 only pipelined
         split_of(kb_total, ov_splits, &p.splits, &p.kblk_per_split);
         while (p.splits > 1 && !fits_ws(g, p.splits))
@@ -154,7 +274,7 @@ Plan plan_bf16(const Gemm &g) {
             const double tm = model_time(g, t, splits, per);
             if (tm < best_t * 0.999) {
                 best_t = tm;
-                best = Plan{t.bm, t.bn, splits, per, dma};
+                best = Plan{t.bm, t.bn, splits, per, dma, t.ns};
             }
         }
     }

@@ -230,6 +230,101 @@ int run(const sbpi::Gemm &g, hipStream_t s) {
     return SBP_OK;
 }
 
+
+// Validation and operand mapping of the three products (no HIP calls).
+int prep_fwd(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *W,
+             const sbp_layout_t *lw, const sbp_view_t *Y, sbpi::Gemm *g, sbp_layout_t *st_out) {
+    if (!X || !W || !Y || !lx || !lw) return SBP_ERR_NULL;
+    int rc = check_pair(lx, lw);
+    if (rc) return rc;
+    Sig s = sig_from_xw(lx, lw);
+    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    Local x, w;
+    if ((rc = local_input(X, lx, &x))) return rc;
+    if ((rc = local_input(W, lw, &w))) return rc;
+    if (x.dtype != w.dtype) return SBP_ERR_DTYPE;
+    if (x.global && w.global && x.gcols != w.grows) return SBP_ERR_SHAPE;
+    if (x.cols != w.rows) return SBP_ERR_SHAPE;
+    sbp_layout_t st[4];
+    states_of(s, lx, st);
+    if ((rc = check_output(Y, x.rows, w.cols, x.dtype, st[0].kind, x, w))) return rc;
+    *g = sbpi::Gemm{sbpi::OR_FWD, x.dtype, Y->dtype, x.ptr, x.ld, w.ptr, w.ld,
+                    Y->data, Y->ld, x.rows, w.cols, x.cols};
+    *st_out = st[0];
+    return SBP_OK;
+}
+
+int prep_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *W,
+                  const sbp_layout_t *lw, const sbp_view_t *dX, sbpi::Gemm *g,
+                  sbp_layout_t *st_out) {
+    if (!dY || !W || !dX || !ldy || !lw) return SBP_ERR_NULL;
+    int rc = check_pair(ldy, lw);
+    if (rc) return rc;
+    Sig s = sig_from_dyw(ldy, lw);
+    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    Local d, w;
+    if ((rc = local_input(dY, ldy, &d))) return rc;
+    if ((rc = local_input(W, lw, &w))) return rc;
+    if (d.dtype != w.dtype) return SBP_ERR_DTYPE;
+    if (d.global && w.global && d.gcols != w.gcols) return SBP_ERR_SHAPE;
+    if (d.cols != w.cols) return SBP_ERR_SHAPE;
+    sbp_layout_t st[4];
+    states_of(s, ldy, st);
+    if ((rc = check_output(dX, d.rows, w.rows, d.dtype, st[2].kind, d, w))) return rc;
+    *g = sbpi::Gemm{sbpi::OR_BWD_DATA, d.dtype, dX->dtype, d.ptr, d.ld, w.ptr, w.ld,
+                    dX->data, dX->ld, d.rows, w.rows, d.cols};
+    *st_out = st[2];
+    return SBP_OK;
+}
+
+int prep_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *dY,
+                    const sbp_layout_t *ldy, const sbp_view_t *dW, sbpi::Gemm *g,
+                    sbp_layout_t *st_out) {
+    if (!X || !dY || !dW || !lx || !ldy) return SBP_ERR_NULL;
+    int rc = check_pair(lx, ldy);
+    if (rc) return rc;
+    Sig s = sig_from_xdy(lx, ldy);
+    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    Local x, d;
+    if ((rc = local_input(X, lx, &x))) return rc;
+    if ((rc = local_input(dY, ldy, &d))) return rc;
+    if (x.dtype != d.dtype) return SBP_ERR_DTYPE;
+    if (x.global && d.global && x.grows != d.grows) return SBP_ERR_SHAPE;
+    if (x.rows != d.rows) return SBP_ERR_SHAPE;
+    sbp_layout_t st[4];
+    states_of(s, lx, st);
+    if ((rc = check_output(dW, x.cols, d.cols, x.dtype, st[3].kind, x, d))) return rc;
+    *g = sbpi::Gemm{sbpi::OR_BWD_WEIGHT, x.dtype, dW->dtype, x.ptr, x.ld, d.ptr, d.ld,
+                    dW->data, dW->ld, x.cols, d.cols, x.rows};
+    *st_out = st[3];
+    return SBP_OK;
+}
+
+// Both backward products: one grouped launch when the planner finds it
+// faster, else two launches. An empty product is skipped.
+int run_pair(const sbpi::Gemm &gd, const sbpi::Gemm &gw, hipStream_t s) {
+    const bool ed = gd.m == 0 || gd.n == 0, ew = gw.m == 0 || gw.n == 0;
+    if (gd.in_dtype == SBP_BF16 && !ed && !ew) {
+        sbpi::Plan pd, pw;
+        if (sbpi::plan_bf16_bwd(gd, gw, &pd, &pw)) {
+            Workspace w;
+            if (pd.splits > 1 || pw.splits > 1) {
+                int rc = workspace_for(s, &w);
+                if (rc) return rc;
+            }
+            hipError_t e = sbpi::launch_bf16_bwd_group(gd, pd, gw, pw, w.ws, s);
+            if (e != hipSuccess) {
+                g_last_hip = (int)e;
+                return SBP_ERR_HIP;
+            }
+            return SBP_OK;
+        }
+    }
+    int rc = run(gd, s);
+    if (rc) return rc;
+    return run(gw, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -276,72 +371,65 @@ int sbp_signature(const sbp_layout_t *x, const sbp_layout_t *w, sbp_layout_t *y,
 int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *W,
                    const sbp_layout_t *lw, sbp_view_t *Y, sbp_layout_t *ly_out,
                    hipStream_t stream) {
-    if (!X || !W || !Y || !lx || !lw) return SBP_ERR_NULL;
-    int rc = check_pair(lx, lw);
+    sbpi::Gemm g;
+    sbp_layout_t st;
+    int rc = prep_fwd(X, lx, W, lw, Y, &g, &st);
     if (rc) return rc;
-    Sig s = sig_from_xw(lx, lw);
-    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
-    Local x, w;
-    if ((rc = local_input(X, lx, &x))) return rc;
-    if ((rc = local_input(W, lw, &w))) return rc;
-    if (x.dtype != w.dtype) return SBP_ERR_DTYPE;
-    if (x.global && w.global && x.gcols != w.grows) return SBP_ERR_SHAPE;
-    if (x.cols != w.rows) return SBP_ERR_SHAPE;
-    sbp_layout_t st[4];
-    states_of(s, lx, st);
-    if ((rc = check_output(Y, x.rows, w.cols, x.dtype, st[0].kind, x, w))) return rc;
-    sbpi::Gemm g{sbpi::OR_FWD, x.dtype, Y->dtype, x.ptr, x.ld, w.ptr, w.ld,
-                 Y->data, Y->ld, x.rows, w.cols, x.cols};
     if ((rc = run(g, stream))) return rc;
-    if (ly_out) *ly_out = st[0];
+    if (ly_out) *ly_out = st;
     return SBP_OK;
 }
 
 int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *W,
                         const sbp_layout_t *lw, sbp_view_t *dX, sbp_layout_t *ldx_out,
                         hipStream_t stream) {
-    if (!dY || !W || !dX || !ldy || !lw) return SBP_ERR_NULL;
-    int rc = check_pair(ldy, lw);
+    sbpi::Gemm g;
+    sbp_layout_t st;
+    int rc = prep_bwd_data(dY, ldy, W, lw, dX, &g, &st);
     if (rc) return rc;
-    Sig s = sig_from_dyw(ldy, lw);
-    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
-    Local d, w;
-    if ((rc = local_input(dY, ldy, &d))) return rc;
-    if ((rc = local_input(W, lw, &w))) return rc;
-    if (d.dtype != w.dtype) return SBP_ERR_DTYPE;
-    if (d.global && w.global && d.gcols != w.gcols) return SBP_ERR_SHAPE;
-    if (d.cols != w.cols) return SBP_ERR_SHAPE;
-    sbp_layout_t st[4];
-    states_of(s, ldy, st);
-    if ((rc = check_output(dX, d.rows, w.rows, d.dtype, st[2].kind, d, w))) return rc;
-    sbpi::Gemm g{sbpi::OR_BWD_DATA, d.dtype, dX->dtype, d.ptr, d.ld, w.ptr, w.ld,
-                 dX->data, dX->ld, d.rows, w.rows, d.cols};
     if ((rc = run(g, stream))) return rc;
-    if (ldx_out) *ldx_out = st[2];
+    if (ldx_out) *ldx_out = st;
     return SBP_OK;
 }
 
 int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *dY,
                           const sbp_layout_t *ldy, sbp_view_t *dW, sbp_layout_t *ldw_out,
                           hipStream_t stream) {
-    if (!X || !dY || !dW || !lx || !ldy) return SBP_ERR_NULL;
-    int rc = check_pair(lx, ldy);
+    sbpi::Gemm g;
+    sbp_layout_t st;
+    int rc = prep_bwd_weight(X, lx, dY, ldy, dW, &g, &st);
     if (rc) return rc;
-    Sig s = sig_from_xdy(lx, ldy);
-    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
-    Local x, d;
-    if ((rc = local_input(X, lx, &x))) return rc;
-    if ((rc = local_input(dY, ldy, &d))) return rc;
-    if (x.dtype != d.dtype) return SBP_ERR_DTYPE;
-    if (x.global && d.global && x.grows != d.grows) return SBP_ERR_SHAPE;
-    if (x.rows != d.rows) return SBP_ERR_SHAPE;
-    sbp_layout_t st[4];
-    states_of(s, lx, st);
-    if ((rc = check_output(dW, x.cols, d.cols, x.dtype, st[3].kind, x, d))) return rc;
-    sbpi::Gemm g{sbpi::OR_BWD_WEIGHT, x.dtype, dW->dtype, x.ptr, x.ld, d.ptr, d.ld,
-                 dW->data, dW->ld, x.cols, d.cols, x.rows};
     if ((rc = run(g, stream))) return rc;
-    if (ldw_out) *ldw_out = st[3];
+    if (ldw_out) *ldw_out = st;
+    return SBP_OK;
+}
+
+int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *X,
+                   const sbp_layout_t *lx, const sbp_view_t *W, const sbp_layout_t *lw,
+                   sbp_view_t *dX, sbp_layout_t *ldx_out, sbp_view_t *dW,
+                   sbp_layout_t *ldw_out, hipStream_t stream) {
+    if (!dY || !X || !W || !dX || !dW || !ldy || !lx || !lw) return SBP_ERR_NULL;
+    int rc = check_pair(lx, lw);
+    if (rc) return rc;
+    if ((rc = check_pair(ldy, lw))) return rc;
+    // the three input states must describe one signature
+    const Sig s = sig_from_xw(lx, lw);
+    if (s == SIG_NONE || sig_from_dyw(ldy, lw) != s || sig_from_xdy(lx, ldy) != s)
+        return SBP_ERR_SIGNATURE;
+    sbpi::Gemm gd, gw;
+    sbp_layout_t sd, sw;
+    if ((rc = prep_bwd_data(dY, ldy, W, lw, dX, &gd, &sd))) return rc;
+    if ((rc = prep_bwd_weight(X, lx, dY, ldy, dW, &gw, &sw))) return rc;
+    // no output may overlap the other output or the input it is not checked
+    // against above (dX vs X, dW vs W)
+    const auto ex = extent(dX->data, dX->rows, dX->cols, dX->ld, dX->dtype);
+    const auto ew = extent(dW->data, dW->rows, dW->cols, dW->ld, dW->dtype);
+    const auto xr = extent(gw.A, gw.k, gw.m, gw.lda, gw.in_dtype);   // X_r: k x m view
+    const auto wr = extent(gd.B, gd.n, gd.k, gd.ldb, gd.in_dtype);   // W_r: n x k view
+    if (overlaps(ex, ew) || overlaps(ex, xr) || overlaps(ew, wr)) return SBP_ERR_ALIAS;
+    if ((rc = run_pair(gd, gw, stream))) return rc;
+    if (ldx_out) *ldx_out = sd;
+    if (ldw_out) *ldw_out = sw;
     return SBP_OK;
 }
 
@@ -386,7 +474,30 @@ int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype, int32_t 
     *tile_m = p.bm;
     *tile_n = p.bn;
     *splits = p.splits;
-    *kernel = p.dma ? 1 : 2;
+    *kernel = p.dma ? (p.ns == 2 ? 4 : 1) : 2;
+    return SBP_OK;
+}
+
+int sbp_plan_bwd(int64_t md, int64_t nd, int64_t kd, int32_t out_d, int64_t mw, int64_t nw,
+                 int64_t kw, int32_t out_w, int32_t *grouped, int32_t *tile_m, int32_t *tile_n,
+                 int32_t *splits_d, int32_t *splits_w) {
+    if (!grouped || !tile_m || !tile_n || !splits_d || !splits_w) return SBP_ERR_NULL;
+    const int64_t dims[6] = {md, nd, kd, mw, nw, kw};
+    for (int64_t d : dims)
+        if (d < 0 || d > INT32_MAX) return SBP_ERR_SHAPE;
+    if ((out_d != SBP_BF16 && out_d != SBP_F32) || (out_w != SBP_BF16 && out_w != SBP_F32))
+        return SBP_ERR_DTYPE;
+    static const char aligned[16] __attribute__((aligned(16))) = {0};
+    sbpi::Gemm gd{sbpi::OR_BWD_DATA, SBP_BF16, out_d, aligned, kd, aligned, kd, nullptr, 0,
+                  md, nd, kd};
+    sbpi::Gemm gw{sbpi::OR_BWD_WEIGHT, SBP_BF16, out_w, aligned, mw, aligned, nw, nullptr, 0,
+                  mw, nw, kw};
+    sbpi::Plan pd, pw;
+    *grouped = sbpi::plan_bf16_bwd(gd, gw, &pd, &pw) ? 1 : 0;
+    *tile_m = pd.bm;
+    *tile_n = pd.bn;
+    *splits_d = pd.splits;
+    *splits_w = pw.splits;
     return SBP_OK;
 }
 
@@ -395,8 +506,9 @@ int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits, int32_
         sbpi::set_override(0, 0, 1, 0);
         return SBP_OK;
     }
-    if (kernel < 0 || kernel > 2) return SBP_ERR_SHAPE;
+    if (kernel < 0 || kernel > 4 || kernel == 3) return SBP_ERR_SHAPE;
     if (!sbpi::tile_supported(tile_m, tile_n, true) || splits < 1) return SBP_ERR_SHAPE;
+    if (kernel == 4 && (tile_m != 128 || tile_n != 128)) return SBP_ERR_SHAPE;
     sbpi::set_override(tile_m, tile_n, splits, kernel);
     return SBP_OK;
 }

@@ -9,6 +9,7 @@
 // loads of every slice when n is a multiple of 4, and stores that are
 // contiguous across the threads of a wave.
 #include "gemm.h"
+#include "profile.h"
 
 namespace sbpk {
 
@@ -59,12 +60,11 @@ hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipSt
     const int64_t groups = g.m * ((g.n + 3) / 4);
     const unsigned blocks = (unsigned)((groups + 255) / 256);
     if (g.out_dtype == DT_F32)
-        hipLaunchKernelGGL(sbpk::split_reduce_kernel<true>, dim3(blocks), dim3(256), 0, s, ws,
-                           (int)g.m, (int)g.n, splits, g.C, g.ldc);
-    else
-        hipLaunchKernelGGL(sbpk::split_reduce_kernel<false>, dim3(blocks), dim3(256), 0, s, ws,
-                           (int)g.m, (int)g.n, splits, g.C, g.ldc);
-    return hipGetLastError();
+        return launch_kernel(sbpk::split_reduce_kernel<true>, "split_reduce_kernel<true>",
+                             dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C,
+                             g.ldc);
+    return launch_kernel(sbpk::split_reduce_kernel<false>, "split_reduce_kernel<false>",
+                         dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C, g.ldc);
 }
 
 }  // namespace sbpi

@@ -79,6 +79,24 @@ def run(op: str, sig: str, p: int, r: int, X, W, dY, out, stream=None):
     raise ValueError(op)
 
 
+def run_bwd(sig: str, p: int, r: int, X, W, dY, dX, dW, stream=None):
+    """Both backward products of rank r in one call (sbp_linear_bwd); returns
+    the (dX, dW) states."""
+    L = layouts(sig, p, r)
+    return sbp.sbp_linear_bwd(sbp.view(dY), L["dy"], sbp.view(X), L["x"], sbp.view(W), L["w"],
+                              sbp.view(dX, sbp.SBP_LOCAL), sbp.view(dW, sbp.SBP_LOCAL), stream)
+
+
+def call_bwd(sig: str, p: int, r: int, X, W, dY, stream=None):
+    """Allocate dX and dW and run both backward products; returns (dX, dW, states)."""
+    M, K = X.shape
+    N = W.shape[1]
+    dX = alloc_out("bwd_data", sig, p, r, M, K, N, X.dtype, X.device)
+    dW = alloc_out("bwd_weight", sig, p, r, M, K, N, X.dtype, X.device)
+    st = run_bwd(sig, p, r, X, W, dY, dX, dW, stream)
+    return dX, dW, st
+
+
 def call(op: str, sig: str, p: int, r: int, X, W, dY, stream=None):
     """Allocate the output and run; returns (out, state)."""
     ref = X if X is not None else dY

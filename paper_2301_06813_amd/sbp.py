@@ -33,8 +33,8 @@ SBP_BF16, SBP_F32 = 0, 1
 SBP_GLOBAL, SBP_LOCAL = 0, 1
 
 EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd_data",
-           "sbp_linear_bwd_weight", "sbp_strerror", "sbp_last_hip_error", "sbp_plan",
-           "sbp_set_plan_override")
+           "sbp_linear_bwd_weight", "sbp_linear_bwd", "sbp_strerror", "sbp_last_hip_error", "sbp_plan",
+           "sbp_plan_bwd", "sbp_set_plan_override", "sbp_profile_begin", "sbp_profile_end")
 
 
 class sbp_layout_t(ctypes.Structure):
@@ -100,6 +100,10 @@ def lib():
             getattr(L, fn).argtypes = [P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
                                        P(sbp_layout_t), P(sbp_view_t), P(sbp_layout_t),
                                        ctypes.c_void_p]
+        L.sbp_linear_bwd.argtypes = [P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
+                                     P(sbp_layout_t), P(sbp_view_t), P(sbp_layout_t),
+                                     P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
+                                     P(sbp_layout_t), ctypes.c_void_p]
         L.sbp_strerror.argtypes = [ctypes.c_int]
         L.sbp_strerror.restype = ctypes.c_char_p
         L.sbp_last_hip_error.argtypes = []
@@ -107,6 +111,10 @@ def lib():
                                ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32),
                                P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_int32)]
         L.sbp_set_plan_override.argtypes = [ctypes.c_int32] * 4
+        L.sbp_profile_begin.argtypes = [ctypes.c_int]
+        L.sbp_profile_end.argtypes = [ctypes.c_void_p, ctypes.c_char_p, ctypes.c_int]
+        L.sbp_plan_bwd.argtypes = ([ctypes.c_int64] * 3 + [ctypes.c_int32] + [ctypes.c_int64] * 3 +
+                                   [ctypes.c_int32] + [P(ctypes.c_int32)] * 5)
         for fn in EXPORTS:
             if fn != "sbp_strerror":
                 getattr(L, fn).restype = ctypes.c_int
@@ -189,20 +197,57 @@ def sbp_linear_bwd_weight(X: sbp_view_t, lx: sbp_layout_t, dY: sbp_view_t, ldy: 
     return _compute("sbp_linear_bwd_weight", X, lx, dY, ldy, dW, stream)
 
 
+def sbp_linear_bwd(dY: sbp_view_t, ldy: sbp_layout_t, X: sbp_view_t, lx: sbp_layout_t,
+                   W: sbp_view_t, lw: sbp_layout_t, dX: sbp_view_t, dW: sbp_view_t,
+                   stream=None):
+    """dX_r = dY_r W_r^T and dW_r = X_r^T dY_r in one call; returns (dX state, dW state)."""
+    sx, sw = sbp_layout_t(), sbp_layout_t()
+    s = current_stream() if stream is None else stream
+    _check(lib().sbp_linear_bwd(ctypes.byref(dY), ctypes.byref(ldy), ctypes.byref(X),
+                                ctypes.byref(lx), ctypes.byref(W), ctypes.byref(lw),
+                                ctypes.byref(dX), ctypes.byref(sx), ctypes.byref(dW),
+                                ctypes.byref(sw), ctypes.c_void_p(s)))
+    return sx, sw
+
+
 def sbp_last_hip_error() -> int:
     return lib().sbp_last_hip_error()
 
 
-KERNEL_AUTO, KERNEL_PIPELINED, KERNEL_GENERIC, KERNEL_F32 = 0, 1, 2, 3
+KERNEL_AUTO, KERNEL_PIPELINED, KERNEL_GENERIC, KERNEL_F32, KERNEL_PIPELINED_2STAGE = 0, 1, 2, 3, 4
 
 
 def sbp_plan(op: int, m: int, n: int, k: int, in_dtype: int, out_dtype: int):
     """(tile_m, tile_n, splits, kernel) the library would launch for this product
-    with aligned operands; kernel is KERNEL_PIPELINED, KERNEL_GENERIC or KERNEL_F32."""
+    with aligned operands; kernel is KERNEL_PIPELINED, KERNEL_PIPELINED_2STAGE,
+    KERNEL_GENERIC or KERNEL_F32."""
     tm, tn, sp, kn = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     _check(lib().sbp_plan(op, m, n, k, in_dtype, out_dtype, ctypes.byref(tm), ctypes.byref(tn),
                           ctypes.byref(sp), ctypes.byref(kn)))
     return tm.value, tn.value, sp.value, kn.value
+
+
+def sbp_plan_bwd(md, nd, kd, out_d, mw, nw, kw, out_w):
+    """(grouped, tile_m, tile_n, splits_d, splits_w) of sbp_linear_bwd for aligned operands."""
+    v = [ctypes.c_int32() for _ in range(5)]
+    _check(lib().sbp_plan_bwd(md, nd, kd, out_d, mw, nw, kw, out_w, *(ctypes.byref(x) for x in v)))
+    return tuple(x.value for x in v)
+
+
+def sbp_profile_begin(capacity: int) -> None:
+    _check(lib().sbp_profile_begin(capacity))
+
+
+def sbp_profile_end(capacity: int):
+    """[(kernel name, microseconds)] of the kernels launched since sbp_profile_begin."""
+    us = (ctypes.c_float * max(capacity, 1))()
+    nl = 160
+    names = ctypes.create_string_buffer(max(capacity, 1) * nl)
+    n = lib().sbp_profile_end(us, names, nl)
+    if n < 0:
+        _check(n)
+    raw = names.raw
+    return [(raw[i * nl:(i + 1) * nl].split(b"\0", 1)[0].decode(), us[i]) for i in range(n)]
 
 
 def sbp_set_plan_override(tile_m: int, tile_n: int, splits: int, kernel: int = 0) -> None:

@@ -12,6 +12,8 @@ SIG_ID = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS}
 OP_ID = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
 TILES = [(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
 KERNELS = (1, 2)   # pipelined direct-to-LDS, generic
+# (tile, kernel) pairs beyond TILES x KERNELS: the two-stage pipelined 128x128
+EXTRA_TILE_KERNELS = [((128, 128), 4)]
 
 
 def say(*a):

@@ -7,7 +7,8 @@
   other pair of input states is rejected (Sec. 4.2 rule, Sec. 4.3 gradients);
 * every validation error is returned before any HIP call. Each case below
   has exactly one defect, so no call here ever reaches a kernel launch; the
-  fake device addresses are never dereferenced.
+  fake device addresses are never dereferenced, and the module is skipped
+  wherever a GPU is visible.
 """
 import os
 import re
@@ -19,6 +20,21 @@ import oracle
 from paper_2301_06813_amd import sbp
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+# These tests pass fake device addresses that must never reach a kernel. They
+# check host logic only, so they run where no GPU is visible; on a GPU machine a
+# mistaken case could launch a kernel on those addresses.
+pytestmark = pytest.mark.skipif(_gpu_visible(), reason="host-only ABI tests use fake device "
+                                "addresses; run them where no GPU is visible")
 
 
 @pytest.fixture(scope="module")
@@ -226,7 +242,7 @@ def test_strerror_and_plan(L):
     tm, tn, s, kn = sbp.sbp_plan(2, 1024, 384, 8192, sbp.SBP_BF16, sbp.SBP_BF16)
     assert (tm, tn) in {(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128),
                         (64, 64)}
-    assert s >= 1 and kn == sbp.KERNEL_PIPELINED
+    assert s >= 1 and kn in (sbp.KERNEL_PIPELINED, sbp.KERNEL_PIPELINED_2STAGE)
     # a reduction that is not a multiple of 8 cannot use the pipelined kernel
     assert sbp.sbp_plan(0, 256, 256, 125, BF, BF)[3] == sbp.KERNEL_GENERIC
     assert sbp.sbp_plan(0, 64, 64, 64, F32, F32)[3] == sbp.KERNEL_F32
@@ -242,4 +258,65 @@ def test_strerror_and_plan(L):
     assert sbp.sbp_plan(0, 128, 128, 1024, BF, BF) == (256, 256, 2, sbp.KERNEL_PIPELINED)
     with pytest.raises(sbp.SbpError):
         sbp.sbp_set_plan_override(512, 256, 1)
+    # the two-stage instance exists for 128x128 only
+    with pytest.raises(sbp.SbpError):
+        sbp.sbp_set_plan_override(256, 128, 1, sbp.KERNEL_PIPELINED_2STAGE)
+    with pytest.raises(sbp.SbpError):
+        sbp.sbp_set_plan_override(128, 128, 1, sbp.KERNEL_F32)
+    sbp.sbp_set_plan_override(128, 128, 3, sbp.KERNEL_PIPELINED_2STAGE)
+    assert sbp.sbp_plan(0, 512, 512, 1024, BF, BF) == (128, 128, 3,
+                                                       sbp.KERNEL_PIPELINED_2STAGE)
+    # operands the pipelined kernel cannot read fall back to the generic kernel
+    assert sbp.sbp_plan(0, 512, 512, 1001, BF, BF)[3] == sbp.KERNEL_GENERIC
     sbp.sbp_set_plan_override(0, 0, 1)
+
+
+def _bwd_code(dy, ldy, x, lx, w, lw, dx, dw):
+    import ctypes
+    a, b = sbp.sbp_layout_t(), sbp.sbp_layout_t()
+    return sbp.lib().sbp_linear_bwd(ctypes.byref(dy), ctypes.byref(ldy), ctypes.byref(x),
+                                    ctypes.byref(lx), ctypes.byref(w), ctypes.byref(lw),
+                                    ctypes.byref(dx), ctypes.byref(a), ctypes.byref(dw),
+                                    ctypes.byref(b), None)
+
+
+def test_grouped_backward_validation(L):
+    # DP, p=4, r=1: X 64x32 (S0), W 32x48 (B), dY 64x48 (S0); dX 16x32 bf16, dW 32x48 fp32
+    x = sbp.raw_view(XA, 64, 32, 32, BF)
+    w = sbp.raw_view(WA, 32, 48, 48, BF)
+    dy = sbp.raw_view(YA, 64, 48, 48, BF)
+    dx = sbp.raw_view(0x40000000, 16, 32, 32, BF, sbp.SBP_LOCAL)
+    dw = sbp.raw_view(0x50000000, 32, 48, 48, F32, sbp.SBP_LOCAL)
+    s0, b = sbp.split(0, 4, 1), sbp.broadcast(4, 1)
+    # dY given as B does not match the DP signature of (X, W)
+    assert _bwd_code(dy, b, x, s0, w, b, dx, dw) == sbp.SBP_ERR_SIGNATURE
+    # dX and dW overlapping
+    dw_ov = sbp.raw_view(0x40000000 + 64, 32, 48, 48, F32, sbp.SBP_LOCAL)
+    assert _bwd_code(dy, s0, x, s0, w, b, dx, dw_ov) == sbp.SBP_ERR_ALIAS
+    # dX written over rank 1's share of X (rows 16..31), the input only the
+    # weight product reads
+    dx_ov = sbp.raw_view(XA + 16 * 32 * 2 + 64, 16, 32, 32, BF, sbp.SBP_LOCAL)
+    assert _bwd_code(dy, s0, x, s0, w, b, dx_ov, dw) == sbp.SBP_ERR_ALIAS
+    # P dW must be fp32
+    dw_bf = sbp.raw_view(0x50000000, 32, 48, 48, BF, sbp.SBP_LOCAL)
+    assert _bwd_code(dy, s0, x, s0, w, b, dx, dw_bf) == sbp.SBP_ERR_DTYPE
+    # an empty rank (M = 3 rows over p = 4, r = 3) succeeds without launching
+    x3 = sbp.raw_view(XA, 3, 32, 32, BF)
+    dy3 = sbp.raw_view(YA, 3, 48, 48, BF)
+    dx0 = sbp.raw_view(None, 0, 32, 32, BF, sbp.SBP_LOCAL)
+    dw3 = sbp.raw_view(0x50000000, 32, 48, 48, F32, sbp.SBP_LOCAL)
+    s3, b3 = sbp.split(0, 4, 3), sbp.broadcast(4, 3)
+    # dW of an empty share is an all-zero output: a launch is needed, so only
+    # check the empty dX path through the data product alone
+    import ctypes
+    lo = sbp.sbp_layout_t()
+    assert sbp.lib().sbp_linear_bwd_data(ctypes.byref(dy3), ctypes.byref(s3), ctypes.byref(w),
+                                         ctypes.byref(b3), ctypes.byref(dx0), ctypes.byref(lo),
+                                         None) == sbp.SBP_OK
+
+
+def test_plan_bwd(L):
+    g, tm, tn, sd, sw = sbp.sbp_plan_bwd(1024, 1024, 3072, BF, 1024, 3072, 1024, F32)
+    assert g in (0, 1) and sd >= 1 and sw >= 1
+    assert (tm, tn) in {(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128),
+                        (64, 64)}

@@ -14,7 +14,8 @@ import torch
 import oracle
 from paper_2301_06813_amd import inputs, linear, sbp
 
-from helpers import KERNELS, TILES, decode, expect_state, oracle_full, out_bits, run_gpu, say
+from helpers import (EXTRA_TILE_KERNELS, KERNELS, TILES, decode, expect_state, oracle_full,
+                     out_bits, run_gpu, say)
 
 pytestmark = pytest.mark.gpu
 SIGS = ("DP", "COL", "KS")
@@ -52,8 +53,11 @@ def test_exact_all_signatures_default_plan(shape):
                     _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
 
 
-@pytest.mark.parametrize("kernel", KERNELS, ids=["pipelined", "generic"])
-@pytest.mark.parametrize("tile", TILES, ids=["%dx%d" % t for t in TILES])
+TILE_KERNELS = [(t, k) for k in KERNELS for t in TILES] + EXTRA_TILE_KERNELS
+TK_IDS = ["%dx%d-k%d" % (t[0], t[1], k) for t, k in TILE_KERNELS]
+
+
+@pytest.mark.parametrize("tile,kernel", TILE_KERNELS, ids=TK_IDS)
 def test_exact_every_tile_and_split(tile, kernel):
     # sizes are multiples of 8 (so the pipelined kernel is eligible) but not
     # of any tile: every dimension has a ragged last tile
@@ -68,6 +72,53 @@ def test_exact_every_tile_and_split(tile, kernel):
                 for op in OPS:
                     say("tile", tile, "kernel", kernel, "splits", splits, sig, op)
                     _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
+
+
+def _check_exact_bwd(sig, p, r, X, W, dY, Xh, Wh, dYh):
+    dX, dW, (sx, sw) = linear.call_bwd(sig, p, r, X, W, dY)
+    torch.cuda.synchronize()
+    expect_state("bwd_data", sig, p, r, sx)
+    expect_state("bwd_weight", sig, p, r, sw)
+    for op, out in (("bwd_data", dX), ("bwd_weight", dW)):
+        want = oracle_full(op, sig, p, r, Xh, Wh, dYh)
+        assert out.shape == want.shape
+        if out.dtype == torch.bfloat16:
+            assert np.array_equal(out_bits(out), oracle.round_bf16(want)), (op, sig, p, r)
+        else:
+            assert np.array_equal(decode(out), want), (op, sig, p, r)
+
+
+@pytest.mark.parametrize("shape", [(304, 1104, 272), (300, 1000, 270), (8192, 256, 1024)])
+def test_exact_grouped_backward_default_plan(shape):
+    # sbp_linear_bwd: one grouped launch when eligible (multiples of 8),
+    # separate launches otherwise; both outputs exact
+    M, K, N = shape
+    X, W, dY = _int_inputs(M, K, N, 800)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    for p in (1, 2, 8):
+        for r in sorted({0, p - 1}):
+            for sig in SIGS:
+                say("grouped bwd", shape, p, r, sig)
+                _check_exact_bwd(sig, p, r, X, W, dY, Xh, Wh, dYh)
+
+
+GROUP_TILES = [(t, 1) for t in TILES] + EXTRA_TILE_KERNELS
+
+
+@pytest.mark.parametrize("tile,kernel", GROUP_TILES,
+                         ids=["%dx%d-k%d" % (t[0], t[1], k) for t, k in GROUP_TILES])
+def test_exact_grouped_backward_every_tile(tile, kernel):
+    M, K, N = 304, 1104, 272
+    X, W, dY = _int_inputs(M, K, N, 900)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    try:
+        for splits in (1, 3):
+            sbp.sbp_set_plan_override(tile[0], tile[1], splits, kernel)
+            for sig in SIGS:
+                say("grouped bwd tile", tile, splits, sig)
+                _check_exact_bwd(sig, 2, 1, X, W, dY, Xh, Wh, dYh)
     finally:
         sbp.sbp_set_plan_override(0, 0, 1)
 
@@ -153,7 +204,7 @@ def test_guard_bands_untouched():
     # the guard stays NaN and every element of the share is written.
     M, K, N, p = 150, 200, 140, 3
     X, W, dY = _int_inputs(M, K, N, 700)
-    for tile, kernel in [(t, k) for t in TILES for k in KERNELS]:
+    for tile, kernel in TILE_KERNELS:
         sbp.sbp_set_plan_override(tile[0], tile[1], 2, kernel)
         try:
             for sig in SIGS:
