@@ -155,12 +155,13 @@ int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx,
                           hipStream_t stream);
 
 /* Both backward products of the linear, dX_r = dY_r W_r^T and
- * dW_r = X_r^T dY_r, in one call (usually one launch). The two products are
- * independent -- each reads dY and one of X, W (Sec. 4.2 backward path,
- * Sec. 4.3 gradient states) -- so they share the device: the longer work
- * items of one run while the shorter ones of the other fill the remaining
- * compute units. States, shapes, dtype rules and errors are those of
- * sbp_linear_bwd_data and sbp_linear_bwd_weight; the three input states
+ * dW_r = X_r^T dY_r, in one call (one grouped launch when the planner
+ * expects it to pay, else the two products in turn on `stream`). The two
+ * products are independent -- each reads dY and one of X, W (Sec. 4.2
+ * backward path, Sec. 4.3 gradient states) -- so in a grouped launch the
+ * longer work items of one run while the shorter ones of the other fill the
+ * remaining compute units. States, shapes, dtype rules and errors are those
+ * of sbp_linear_bwd_data and sbp_linear_bwd_weight; the three input states
  * must form one signature (else SBP_ERR_SIGNATURE), and dX and dW must not
  * overlap (SBP_ERR_ALIAS). Results equal the two separate calls up to fp32
  * summation order. */
@@ -184,8 +185,7 @@ int sbp_last_hip_error(void);
  * dimensions, for input dtype in_dtype, output dtype out_dtype and operand
  * orientation op (0 forward, 1 backward-data, 2 backward-weight). Writes
  * the tile rows and columns, the number of reduction splits and the kernel
- * (1 pipelined direct-to-LDS bf16, 2 generic bf16, 3 fp32, 4 pipelined
- * bf16 with two stages, two workgroups per compute unit). For benchmarks and
+ * (3 fp32, else the bf16 instance code of sbp_set_plan_override). For benchmarks and
  * tests; pure host function.
  * Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
 int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype,
@@ -217,16 +217,27 @@ int sbp_profile_end(float *us, char *names, int name_len);
 
 /* Thread-local override of the bf16 plan for subsequent calls on this
  * thread (tests and tuning). tile_m x tile_n is one of 256x256, 256x128,
- * 128x256, 128x128, 128x64, 64x128, 64x64; splits >= 1; kernel 0 = the
- * library's choice, 1 = pipelined direct-to-LDS, 2 = generic, 4 = pipelined
- * with two stages (128x128 only). A call whose operands the pipelined kernel
- * cannot read runs the generic kernel, where 256x256 becomes 256x128;
- * splits are clamped to the reduction blocks and to the workspace.
- * tile_m = 0 clears the override.
- * Errors: SBP_ERR_SHAPE for an unknown tile shape, splits < 1, kernel
- * outside {0, 1, 2, 4}, or kernel 4 with a tile other than 128x128. */
+ * 128x256, 128x128, 128x64, 64x128, 64x64; splits >= 1. kernel selects the
+ * instance:
+ *   0, 1  the tile's default pipelined direct-to-LDS instance;
+ *   2     the generic kernel;
+ *   4     pipelined with two stages (128x128);
+ *   5     pipelined, eight waves in two reduction groups, output staged in
+ *         LDS (256x128, 128x256, 128x128);
+ *   6     pipelined, row-quad epilogue: MFMA operands swapped so each lane
+ *         stores 4 consecutive outputs of a row from registers (256x256, and
+ *         128x128 with two stages);
+ *   7     as 5 with the row-quad epilogue (256x128, 128x256, 128x128).
+ * wgs_per_cu > 0 makes the launch persistent: at most wgs_per_cu workgroups
+ * per compute unit, each taking every G-th work item (0 = one workgroup per
+ * item; the grouped backward launch always runs one per item). A call whose
+ * operands the pipelined kernel cannot read runs the generic kernel, where
+ * 256x256 becomes 256x128; splits are clamped to the reduction blocks and to
+ * the workspace. tile_m = 0 clears the override.
+ * Errors: SBP_ERR_SHAPE for a (tile, kernel) pair not listed above,
+ * splits < 1, or wgs_per_cu outside [0, 8]. */
 int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits,
-                          int32_t kernel);
+                          int32_t kernel, int32_t wgs_per_cu);
 
 #ifdef __cplusplus
 }

@@ -35,7 +35,13 @@ struct Plan {
     int kblk_per_split;    // 64-wide reduction blocks per split
     bool dma;              // pipelined direct-to-LDS kernel (else the generic kernel)
     int ns = 0;            // pipelined kernel: stages (0 = the tile's default)
+    int kg = 1;            // pipelined kernel: reduction groups of waves (1 or 2)
+    int epi = 0;           // pipelined kernel: epilogue (sbpk::EPI_DIRECT / _STAGED / _ROWQ)
+    int occ = 0;           // persistent workgroups per compute unit (0: one per work item)
 };
+
+// Compute units of the current device (cached per device).
+int device_cus();
 
 // Whether the pipelined direct-to-LDS kernel can run this product: every
 // operand 16-byte aligned, leading dimensions and contiguous extents
@@ -51,6 +57,9 @@ constexpr size_t WS_FLOATS = size_t(32) << 20;   // 128 MiB
 Plan plan_bf16(const Gemm &g);
 bool tile_supported(int bm, int bn, bool dma);
 void set_override(int bm, int bn, int splits, int kernel);   // bm = 0 clears
+void set_override_occ(int occ);                              // 0: one workgroup per item
+bool override_supported(int bm, int bn, int kernel);
+int kernel_code(const Plan &p);   // kernel code of a plan, as sbp_plan reports it
 
 // GEMM of plan p; with p.splits > 1 it writes partials to ws and then runs
 // the split reduction into g.C.

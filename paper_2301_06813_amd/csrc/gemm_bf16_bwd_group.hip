@@ -7,27 +7,22 @@ namespace sbpi {
 namespace {
 
 template <bool OD, bool OW>
-hipError_t launch_group_tile(int bm, int bn, int ns, const sbpk::GemmArgs &d,
-                             const sbpk::GemmArgs &w, int data_first, int grid, hipStream_t s) {
-    char name[160];
+hipError_t launch_group_tile(const Plan &p, const sbpk::GemmArgs &d, const sbpk::GemmArgs &w,
+                             int data_first, int grid, hipStream_t s) {
+    char name[192];
     const char *tf[2] = {"false", "true"};
-#define SBP_BWD_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_)                                       \
-    if (bm == BM_ && bn == BN_ && (ns == 0 || ns == NS_)) {                                \
+#define SBP_BWD_TILE(BM_, BN_, NS_, WGM_, WGN_, KG_, EPI_)                                 \
+    if (p.bm == BM_ && p.bn == BN_ && (p.ns == 0 || p.ns == NS_) && p.kg == KG_ &&         \
+        p.epi == EPI_) {                                                                   \
         snprintf(name, sizeof(name),                                                       \
-                 "gemm_bf16_dma_bwd_kernel<%d, %d, %d, %d, %d, %d, %s, %s>", BM_, BN_,     \
-                 BKD_, NS_, WGM_, WGN_, tf[OD], tf[OW]);                                   \
+                 "gemm_bf16_dma_bwd_kernel<%d, %d, 64, %d, %d, %d, %d, %d, %s, %s>", BM_,  \
+                 BN_, NS_, WGM_, WGN_, KG_, EPI_, tf[OD], tf[OW]);                         \
         return launch_kernel(                                                              \
-            sbpk::gemm_bf16_dma_bwd_kernel<BM_, BN_, BKD_, NS_, WGM_, WGN_, OD, OW>, name, \
-            dim3(grid), dim3(64 * WGM_ * WGN_), s, d, w, data_first);                      \
+            sbpk::gemm_bf16_dma_bwd_kernel<BM_, BN_, 64, NS_, WGM_, WGN_, KG_, EPI_, OD,   \
+                                           OW>,                                            \
+            name, dim3(grid), dim3(64 * WGM_ * WGN_ * KG_), s, d, w, data_first);          \
     }
-    SBP_BWD_TILE(256, 256, 64, 2, 2, 4)
-    SBP_BWD_TILE(256, 128, 64, SBP_NS_256x128, 2, 2)
-    SBP_BWD_TILE(128, 256, 64, SBP_NS_256x128, 2, 2)
-    SBP_BWD_TILE(128, 128, 64, SBP_NS_128x128, 2, 2)
-    SBP_BWD_TILE(128, 128, 64, 2, 2, 2)
-    SBP_BWD_TILE(128, 64, 64, SBP_NS_128x64, 2, 2)
-    SBP_BWD_TILE(64, 128, 64, SBP_NS_128x64, 2, 2)
-    SBP_BWD_TILE(64, 64, 64, SBP_NS_64x64, 2, 2)
+    SBP_DMA_INSTANCES(SBP_BWD_TILE)
 #undef SBP_BWD_TILE
     return hipErrorInvalidValue;
 }
@@ -36,7 +31,8 @@ hipError_t launch_group_tile(int bm, int bn, int ns, const sbpk::GemmArgs &d,
 
 hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
                                  const Plan &pw, float *ws, hipStream_t s) {
-    if (pd.bm != pw.bm || pd.bn != pw.bn || pd.ns != pw.ns || !pd.dma || !pw.dma)
+    if (pd.bm != pw.bm || pd.bn != pw.bn || pd.ns != pw.ns || pd.kg != pw.kg || pd.epi != pw.epi ||
+        !pd.dma || !pw.dma)
         return hipErrorInvalidValue;
     float *ws_w = ws;
     if (pd.splits > 1) ws_w = ws + (size_t)pd.splits * (size_t)gd.m * (size_t)gd.n;
@@ -47,10 +43,10 @@ hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
     const bool od = gd.out_dtype == DT_F32 || pd.splits > 1;
     const bool ow = gw.out_dtype == DT_F32 || pw.splits > 1;
     hipError_t e;
-    if (od && ow) e = launch_group_tile<true, true>(pd.bm, pd.bn, pd.ns, d, w, data_first, grid, s);
-    else if (od) e = launch_group_tile<true, false>(pd.bm, pd.bn, pd.ns, d, w, data_first, grid, s);
-    else if (ow) e = launch_group_tile<false, true>(pd.bm, pd.bn, pd.ns, d, w, data_first, grid, s);
-    else e = launch_group_tile<false, false>(pd.bm, pd.bn, pd.ns, d, w, data_first, grid, s);
+    if (od && ow) e = launch_group_tile<true, true>(pd, d, w, data_first, grid, s);
+    else if (od) e = launch_group_tile<true, false>(pd, d, w, data_first, grid, s);
+    else if (ow) e = launch_group_tile<false, true>(pd, d, w, data_first, grid, s);
+    else e = launch_group_tile<false, false>(pd, d, w, data_first, grid, s);
     if (e != hipSuccess) return e;
     if (pd.splits > 1 && (e = launch_split_reduce(gd, pd.splits, ws, s)) != hipSuccess) return e;
     if (pw.splits > 1 && (e = launch_split_reduce(gw, pw.splits, ws_w, s)) != hipSuccess) return e;

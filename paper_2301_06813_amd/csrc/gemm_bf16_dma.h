@@ -31,6 +31,8 @@
 //     tile order and epilogue as in gemm_bf16_kernel.h.
 #pragma once
 
+#include <type_traits>
+
 #include "gemm_bf16_kernel.h"
 
 namespace sbpk {
@@ -180,24 +182,113 @@ struct DmaStage {
     static constexpr int BYTES = A_BYTES + B_BYTES;
 };
 
+// Output rows of the staged epilogue are padded by 8 floats: the two half-waves
+// of a 32 x 32 MFMA block write rows 4 apart, and 4 (BN + 8) = 32 mod 64
+// floats puts them on disjoint LDS banks.
+template <int BN>
+struct StageRow {
+    static constexpr int LD = BN + 8;   // floats per staged output row
+};
+
+// Stores the BM x BN fp32 tile staged in LDS (`tile`, row stride
+// StageRow<BN>::LD floats) to rows [m0, m0 + BM) x columns [n0, n0 + BN) of C
+// (ld `ldc`, clipped to m x n), by all NT threads: each thread moves whole
+// 16-byte chunks along a row -- 4 floats, or 8 values rounded to bf16 -- so a
+// wave writes whole contiguous row segments. `vec`: C's base and ldc allow
+// aligned 16-byte stores; otherwise (and at the right edge) elements are
+// stored one by one.
+template <int BM, int BN, int NT_, bool F32>
+__device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t ldc, int m,
+                                             int n, int m0, int n0, bool vec, int tid) {
+    constexpr int LD = StageRow<BN>::LD;
+    constexpr int EPC = F32 ? 4 : 8;             // output elements per 16-byte chunk
+    constexpr int CPR = BN / EPC;                // chunks per tile row
+    constexpr int ITER = BM * CPR / NT_;
+    static_assert((BM * CPR) % NT_ == 0, "tile not divisible among threads");
+#pragma unroll 4
+    for (int it = 0; it < ITER; ++it) {
+        const int q = it * NT_ + tid;
+        const int r = q / CPR, c = (q % CPR) * EPC;
+        const int row = m0 + r, col = n0 + c;
+        if (row >= m || col >= n) continue;
+        const float *src = tile + r * LD + c;
+        if constexpr (F32) {
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(src);
+            float *dst = reinterpret_cast<float *>(C) + (int64_t)row * ldc + col;
+            if (vec && col + 4 <= n) {
+                *reinterpret_cast<f32x4 *>(dst) = v;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (col + e < n) dst[e] = v[e];
+            }
+        } else {
+            const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
+            const f32x4 b = *reinterpret_cast<const f32x4 *>(src + 4);
+            uint16_t *dst = reinterpret_cast<uint16_t *>(C) + (int64_t)row * ldc + col;
+            if (vec && col + 8 <= n) {
+                u32x4 w;
+                w[0] = (uint32_t)f32_to_bf16_bits(a[0]) | ((uint32_t)f32_to_bf16_bits(a[1]) << 16);
+                w[1] = (uint32_t)f32_to_bf16_bits(a[2]) | ((uint32_t)f32_to_bf16_bits(a[3]) << 16);
+                w[2] = (uint32_t)f32_to_bf16_bits(b[0]) | ((uint32_t)f32_to_bf16_bits(b[1]) << 16);
+                w[3] = (uint32_t)f32_to_bf16_bits(b[2]) | ((uint32_t)f32_to_bf16_bits(b[3]) << 16);
+                *reinterpret_cast<u32x4 *>(dst) = w;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (col + e < n) dst[e] = f32_to_bf16_bits(e < 4 ? a[e] : b[e - 4]);
+            }
+        }
+    }
+}
+
+// Epilogue variants of the tile body.
+enum : int {
+    EPI_DIRECT = 0,   // each lane stores its MFMA elements (4-byte / 2-byte stores)
+    EPI_STAGED = 1,   // tile staged in LDS, stored as 16-byte row chunks by all threads
+    EPI_ROWQ = 2      // MFMA operands swapped so that each lane holds 4 consecutive
+                      // outputs of one row: 16-byte (fp32) / 8-byte (bf16) stores
+                      // straight from registers, no LDS and no wait
+};
+
 // One work item (an output tile and a reduction split) of a product, by the
-// whole workgroup: WGM x WGN waves (2 x 2, or 2 x 4 for the 256 x 256 tile:
-// 8 waves, two per SIMD, each owning 128 x 64 outputs). L is the item's
-// logical index in [0, tiles * splits).
-template <int BM, int BN, int BKD, int NS, int WGM, int WGN, bool A_KMAJ, bool B_KMAJ,
-          bool OUT_F32>
+// whole workgroup of KG x WGM x WGN waves. The WGM x WGN waves of a
+// reduction group own (BM / WGM) x (BN / WGN) outputs each; with KG = 2 the
+// two groups take alternate halves of every 64-wide reduction step (so each
+// SIMD holds two waves, one of each group, and one's MFMAs run while the
+// other waits on LDS), and their fp32 sums are added through LDS at the end.
+// L is the item's logical index in [0, tiles * splits). On return from the
+// staged and row-quad epilogues every wave is done reading the pipeline's
+// LDS, so the next item may refill it; after the direct epilogue the caller
+// must synchronise the workgroup first.
+template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool A_KMAJ,
+          bool B_KMAJ, bool OUT_F32>
 __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, char *smem) {
-    constexpr int NW = WGM * WGN;
+    constexpr int NSW = WGM * WGN;                // waves per reduction group
+    constexpr int NW = NSW * KG;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int MI = WM / 32, NI = WN / 32;
+    constexpr int KSG = BKD / 16 / KG;            // 16-wide sub-steps per group and step
     constexpr int A_BYTES = DmaStage<BM, BN, BKD, NS>::A_BYTES;
     constexpr int STAGE = DmaStage<BM, BN, BKD, NS>::BYTES;
     constexpr int LOADS = STAGE / 1024 / NW;                         // dma per thread per stage
+    constexpr bool SWAP = EPI == EPI_ROWQ;
+    static_assert(KG == 1 || KG == 2, "one or two reduction groups");
+    static_assert(BKD % (16 * KG) == 0, "reduction step not divisible among groups");
+    static_assert(EPI != EPI_STAGED || BM * StageRow<BN>::LD * 4 <= NS * STAGE,
+                  "staged output tile does not fit the pipeline's LDS");
+    static_assert(KG == 1 || NSW * MI * NI * 64 * 64 <= NS * STAGE,
+                  "group partial sums do not fit the pipeline's LDS");
+    static_assert(KG == 1 || EPI != EPI_DIRECT, "two reduction groups need a summing epilogue");
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave / WGN, wn = wave % WGN;
+    // wave < NW; with one group the compiler must see kg = 0 to keep the
+    // fragment addresses compile-time offsets
+    const int kg = KG == 1 ? 0 : wave / NSW;
+    const int sw = KG == 1 ? wave : wave % NSW;
+    const int wm = sw / WGN, wn = sw % WGN;
 
     const int tiles = g.tiles_m * g.tiles_n;
     const int split = L / tiles;
@@ -249,7 +340,8 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
 
         const char *cur = smem + (it % NS) * STAGE;
 #pragma unroll
-        for (int ks = 0; ks < BKD / 16; ++ks) {
+        for (int kk = 0; kk < KSG; ++kk) {
+            const int ks = kg * KSG + kk;
             bf16x8 af[MI], bfr[NI];
 #pragma unroll
             for (int i = 0; i < MI; ++i)
@@ -261,17 +353,155 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
             for (int i = 0; i < MI; ++i)
 #pragma unroll
                 for (int j = 0; j < NI; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = SWAP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i],
+                                                                               acc[i][j], 0, 0, 0)
+                                     : __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j],
+                                                                               acc[i][j], 0, 0, 0);
         }
     }
 
-    if (g.splits > 1) {
-        // Split reduction: this workgroup's fp32 partial goes to slice
-        // `split` of the workspace, laid out like the output (m x n, ld n);
-        // a separate kernel adds the slices in split order.
-        float *P = g.ws + (size_t)split * (size_t)g.m * (size_t)g.n;
+    // Split reduction: this workgroup's fp32 partial goes to slice `split`
+    // of the workspace, laid out like the output (m x n, ld n); a separate
+    // kernel adds the slices in split order.
+    const bool partial = g.splits > 1;
+    float *const ws_out = g.ws + (size_t)split * (size_t)g.m * (size_t)g.n;
+
+    if constexpr (EPI != EPI_DIRECT) __syncthreads();   // every wave is done with the pipeline's LDS
+
+    if constexpr (KG == 2 && EPI == EPI_ROWQ) {
+        // group 1 hands its sums to group 0 through LDS (lane-contiguous
+        // 16-byte slots, conflict free); group 0 stores the total
+        f32x4 *slot = reinterpret_cast<f32x4 *>(smem) + sw * (MI * NI * 4 * 64) + lane;
+        if (kg == 1) {
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                   acc[i][j][4 * q + 3]};
+                        slot[((i * NI + j) * 4 + q) * 64] = v;
+                    }
+        }
+        __syncthreads();
+        if (kg == 0) {
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const f32x4 v = slot[((i * NI + j) * 4 + q) * 64];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
+                    }
+        }
+        __syncthreads();   // the slots are free again
+        if (kg == 1) return;
+    }
+
+    if constexpr (EPI == EPI_ROWQ) {
+        // lane owns row r = lane % 32 of each 32 x 32 block and, for register
+        // quad q, columns 8 q + 4 (lane / 32) + 0..3
+        auto store_all = [&](auto f32_tag, void *out, int64_t ldo, bool vec) {
+            constexpr bool F32 = decltype(f32_tag)::value;
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int row = m0 + wm * WM + i * 32 + (lane & 31);
+                if (row >= g.m) continue;
+#pragma unroll
+                for (int j = 0; j < NI; ++j) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int col = n0 + wn * WN + j * 32 + 8 * q + 4 * (lane >> 5);
+                        if (col >= g.n) continue;
+                        if constexpr (F32) {
+                            float *dst = reinterpret_cast<float *>(out) + (int64_t)row * ldo + col;
+                            if (vec && col + 4 <= g.n) {
+                                f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1],
+                                           acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                                *reinterpret_cast<f32x4 *>(dst) = v;
+                            } else {
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    if (col + e < g.n) dst[e] = acc[i][j][4 * q + e];
+                            }
+                        } else {
+                            uint16_t *dst =
+                                reinterpret_cast<uint16_t *>(out) + (int64_t)row * ldo + col;
+                            if (vec && col + 4 <= g.n) {
+                                u32x2 w;
+                                w[0] = (uint32_t)f32_to_bf16_bits(acc[i][j][4 * q]) |
+                                       ((uint32_t)f32_to_bf16_bits(acc[i][j][4 * q + 1]) << 16);
+                                w[1] = (uint32_t)f32_to_bf16_bits(acc[i][j][4 * q + 2]) |
+                                       ((uint32_t)f32_to_bf16_bits(acc[i][j][4 * q + 3]) << 16);
+                                *reinterpret_cast<u32x2 *>(dst) = w;
+                            } else {
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    if (col + e < g.n)
+                                        dst[e] = f32_to_bf16_bits(acc[i][j][4 * q + e]);
+                            }
+                        }
+                    }
+                }
+            }
+        };
+        if (partial)
+            store_all(std::true_type{}, ws_out, (int64_t)g.n, g.n % 4 == 0);
+        else
+            store_all(std::integral_constant<bool, OUT_F32>{}, g.C, g.ldc, (bool)g.vec_c4);
+        return;
+    }
+
+    if constexpr (EPI == EPI_STAGED) {
+        constexpr int LD = StageRow<BN>::LD;
+        float *tile = reinterpret_cast<float *>(smem);
+        // element (r, c) of 32 x 32 block (i, j) of this wave, MFMA layout:
+        // c = lane % 32, r = 8 (q / 4) + 4 (lane / 32) + q % 4 for register q
+        const int cbase = wn * WN + (lane & 31);
+        const int rbase = wm * WM + 4 * (lane >> 5);
+        if (kg == KG - 1) {
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q)
+                        tile[(rbase + i * 32 + 8 * (q >> 2) + (q & 3)) * LD + cbase + j * 32] =
+                            acc[i][j][q];
+        }
+        if constexpr (KG == 2) {
+            __syncthreads();
+            if (kg == 0) {
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j)
+#pragma unroll
+                        for (int q = 0; q < 16; ++q) {
+                            float *e = &tile[(rbase + i * 32 + 8 * (q >> 2) + (q & 3)) * LD +
+                                             cbase + j * 32];
+                            *e = acc[i][j][q] + *e;
+                        }
+            }
+        }
+        __syncthreads();
+        if (partial)
+            store_staged<BM, BN, 64 * NW, true>(tile, ws_out, g.n, g.m, g.n, m0, n0,
+                                                g.n % 4 == 0, tid);
+        else
+            store_staged<BM, BN, 64 * NW, OUT_F32>(tile, g.C, g.ldc, g.m, g.n, m0, n0,
+                                                   OUT_F32 ? g.vec_c4 : g.vec_c8, tid);
+        __syncthreads();   // the staged tile is free again
+        return;
+    }
+
+    auto store_all = [&](auto f32_tag, void *out, int64_t ldo) {
+        constexpr bool F32 = decltype(f32_tag)::value;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
 #pragma unroll
             for (int j = 0; j < NI; ++j) {
                 const int col = n0 + wn * WN + j * 32 + (lane & 31);
@@ -280,46 +510,44 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const int row = rbase + 8 * (r >> 2) + (r & 3);
-                        if (row < g.m) P[(int64_t)row * g.n + col] = acc[i][j][r];
-                    }
-                }
-            }
-        return;
-    }
-
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-            const int col = n0 + wn * WN + j * 32 + (lane & 31);
-            const int rbase = m0 + wm * WM + i * 32 + 4 * (lane >> 5);
-            if (col < g.n) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int row = rbase + 8 * (r >> 2) + (r & 3);
-                    if (row < g.m) {
-                        if constexpr (OUT_F32) {
-                            float *C = reinterpret_cast<float *>(g.C);
-                            C[(int64_t)row * g.ldc + col] = acc[i][j][r];
-                        } else {
-                            uint16_t *C = reinterpret_cast<uint16_t *>(g.C);
-                            C[(int64_t)row * g.ldc + col] = f32_to_bf16_bits(acc[i][j][r]);
+                        if (row < g.m) {
+                            if constexpr (F32)
+                                reinterpret_cast<float *>(out)[(int64_t)row * ldo + col] =
+                                    acc[i][j][r];
+                            else
+                                reinterpret_cast<uint16_t *>(out)[(int64_t)row * ldo + col] =
+                                    f32_to_bf16_bits(acc[i][j][r]);
                         }
                     }
                 }
             }
         }
-    }
+    };
+    if (partial)
+        store_all(std::true_type{}, ws_out, (int64_t)g.n);
+    else
+        store_all(std::integral_constant<bool, OUT_F32>{}, g.C, g.ldc);
 }
 
 
-template <int BM, int BN, int BKD, int NS, int WGM, int WGN, bool A_KMAJ, bool B_KMAJ,
-          bool OUT_F32>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_kernel(GemmArgs g) {
+// A grid of `gridDim.x` workgroups works through the product's
+// tiles * splits items: workgroup b takes items b, b + G, b + 2G, ...
+// (G = gridDim.x, a multiple of 8 when smaller than the item count, so that
+// every item of one workgroup maps to the same XCD under remap_xcd). With a
+// grid smaller than the item count, one item's output stores drain while
+// the next item's operand loads are in flight.
+template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool A_KMAJ,
+          bool B_KMAJ, bool OUT_F32>
+__global__ __launch_bounds__(64 * WGM * WGN * KG, 1) void gemm_bf16_dma_kernel(GemmArgs g) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
     const int total = g.tiles_m * g.tiles_n * g.splits;
-    dma_tile_body<BM, BN, BKD, NS, WGM, WGN, A_KMAJ, B_KMAJ, OUT_F32>(
-        g, remap_xcd(blockIdx.x, total), smem);
+    for (int v = blockIdx.x; v < total; v += gridDim.x) {
+        // a later item refills the pipeline's LDS: every wave must be done
+        // reading it (the direct epilogue does not end with a barrier)
+        if (EPI == EPI_DIRECT && v != (int)blockIdx.x) __syncthreads();
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, A_KMAJ, B_KMAJ, OUT_F32>(
+            g, remap_xcd(v, total), smem);
+    }
 }
 
 // The two backward products of one linear in one launch: gd is the
@@ -328,10 +556,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_kernel(GemmAr
 // of X, W), so their work items share the grid; the product whose work
 // items are longer is dispatched first (data_first) so that the short items
 // of the other fill the machine behind them.
-template <int BM, int BN, int BKD, int NS, int WGM, int WGN, bool OUTD_F32, bool OUTW_F32>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_bwd_kernel(GemmArgs gd,
-                                                                             GemmArgs gw,
-                                                                             int data_first) {
+template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool OUTD_F32,
+          bool OUTW_F32>
+__global__ __launch_bounds__(64 * WGM * WGN * KG, 1) void gemm_bf16_dma_bwd_kernel(GemmArgs gd,
+                                                                                  GemmArgs gw,
+                                                                                  int data_first) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
     const int wd = gd.tiles_m * gd.tiles_n * gd.splits;
     const int ww = gw.tiles_m * gw.tiles_n * gw.splits;
@@ -339,12 +568,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_dma_bwd_kernel(Ge
     const bool is_data = data_first ? (b < wd) : (b >= ww);
     if (is_data) {
         const int local = data_first ? b : b - ww;
-        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, true, true, OUTD_F32>(gd, remap_xcd(local, wd),
-                                                                      smem);
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, true, true, OUTD_F32>(
+            gd, remap_xcd(local, wd), smem);
     } else {
         const int local = data_first ? b - wd : b;
-        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, false, false, OUTW_F32>(gw, remap_xcd(local, ww),
-                                                                        smem);
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, false, false, OUTW_F32>(
+            gw, remap_xcd(local, ww), smem);
     }
 }
 

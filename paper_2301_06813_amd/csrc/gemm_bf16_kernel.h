@@ -51,6 +51,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 64;          // reduction step (elements)
 constexpr int NT = 256;         // threads per workgroup
@@ -67,6 +68,8 @@ struct GemmArgs {
     int32_t kchunk;             // reduction elements per split (a multiple of 64)
     float *ws;                  // split partials: splits slices of m x n floats
     int32_t vec_a, vec_b;       // operand base and ld allow aligned 16-byte loads
+    int32_t vec_c4, vec_c8;     // C's base and ldc allow aligned 16-byte stores of
+                                // 4 fp32 / 8 bf16 elements
 };
 
 // Byte offset of 16-byte chunk c (0..7) of LDS row `row`.

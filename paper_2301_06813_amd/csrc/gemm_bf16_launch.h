@@ -3,6 +3,8 @@
 // the three orientations compile in parallel.
 #pragma once
 
+#include <algorithm>
+
 #include "gemm.h"
 #include "gemm_bf16_dma.h"
 #include "profile.h"
@@ -23,26 +25,58 @@
 
 namespace sbpi {
 
+// Instances of the pipelined kernel: tile, stages, wave layout, reduction
+// groups and epilogue. The macro list is shared by the single-product and
+// the grouped backward launchers.
+#define SBP_DMA_INSTANCES(X)                                    \
+    X(256, 256, 2, 2, 4, 1, sbpk::EPI_DIRECT)                   \
+    X(256, 256, 2, 2, 4, 1, sbpk::EPI_ROWQ)                     \
+    X(256, 128, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
+    X(128, 256, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
+    X(128, 128, SBP_NS_128x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
+    X(128, 128, 2, 2, 2, 1, sbpk::EPI_DIRECT)                   \
+    X(128, 128, 2, 2, 2, 1, sbpk::EPI_ROWQ)                     \
+    X(128, 64, SBP_NS_128x64, 2, 2, 1, sbpk::EPI_DIRECT)        \
+    X(64, 128, SBP_NS_128x64, 2, 2, 1, sbpk::EPI_DIRECT)        \
+    X(64, 64, SBP_NS_64x64, 2, 2, 1, sbpk::EPI_DIRECT)          \
+    X(256, 128, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_STAGED)      \
+    X(128, 256, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_STAGED)      \
+    X(128, 128, SBP_NS_128x128, 2, 2, 2, sbpk::EPI_STAGED)      \
+    X(256, 128, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_ROWQ)        \
+    X(128, 256, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_ROWQ)        \
+    X(128, 128, SBP_NS_128x128, 2, 2, 2, sbpk::EPI_ROWQ)
+
+// Grid of a launch of `items` work items under plan p: one workgroup per item,
+// or (persistent plans) at most occ workgroups per compute unit, a multiple of 8.
+static inline int grid_of(const Plan &p, int items) {
+    if (p.occ <= 0) return items;
+    const int cap = p.occ * device_cus();
+    if (items <= cap) return items;
+    return std::max(8, cap / 8 * 8);
+}
+
 template <bool AK, bool BK_, bool OUTF>
-static hipError_t launch_tile(int bm, int bn, int ns, bool dma, const sbpk::GemmArgs &a,
-                              int grid, hipStream_t s) {
-    char name[160];
+static hipError_t launch_tile(const Plan &p, const sbpk::GemmArgs &a, int items, hipStream_t s) {
+    char name[192];
     const char *tf[2] = {"false", "true"};
+    const int grid = grid_of(p, items);
 #define SBP_TILE(BM_, BN_)                                                                  \
-    if (!dma && bm == BM_ && bn == BN_) {                                                   \
+    if (!p.dma && p.bm == BM_ && p.bn == BN_) {                                             \
         snprintf(name, sizeof(name), "gemm_bf16_kernel<%d, %d, %s, %s, %s>", BM_, BN_,     \
                  tf[AK], tf[BK_], tf[OUTF]);                                                \
         return launch_kernel(sbpk::gemm_bf16_kernel<BM_, BN_, AK, BK_, OUTF>, name,         \
-                             dim3(grid), dim3(sbpk::NT), s, a);                             \
+                             dim3(items), dim3(sbpk::NT), s, a);                            \
     }
-#define SBP_DMA_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_)                                       \
-    if (dma && bm == BM_ && bn == BN_ && (ns == 0 || ns == NS_)) {                          \
+#define SBP_DMA_TILE(BM_, BN_, NS_, WGM_, WGN_, KG_, EPI_)                                  \
+    if (p.dma && p.bm == BM_ && p.bn == BN_ && (p.ns == 0 || p.ns == NS_) && p.kg == KG_ && \
+        p.epi == EPI_) {                                                                    \
         snprintf(name, sizeof(name),                                                        \
-                 "gemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %s, %s, %s>", BM_, BN_,      \
-                 BKD_, NS_, WGM_, WGN_, tf[AK], tf[BK_], tf[OUTF]);                         \
+                 "gemm_bf16_dma_kernel<%d, %d, 64, %d, %d, %d, %d, %d, %s, %s, %s>", BM_,   \
+                 BN_, NS_, WGM_, WGN_, KG_, EPI_, tf[AK], tf[BK_], tf[OUTF]);               \
         return launch_kernel(                                                               \
-            sbpk::gemm_bf16_dma_kernel<BM_, BN_, BKD_, NS_, WGM_, WGN_, AK, BK_, OUTF>,     \
-            name, dim3(grid), dim3(64 * WGM_ * WGN_), s, a);                                \
+            sbpk::gemm_bf16_dma_kernel<BM_, BN_, 64, NS_, WGM_, WGN_, KG_, EPI_, AK, BK_,   \
+                                       OUTF>,                                               \
+            name, dim3(grid), dim3(64 * WGM_ * WGN_ * KG_), s, a);                          \
     }
     SBP_TILE(256, 128)
     SBP_TILE(128, 256)
@@ -50,14 +84,7 @@ static hipError_t launch_tile(int bm, int bn, int ns, bool dma, const sbpk::Gemm
     SBP_TILE(128, 64)
     SBP_TILE(64, 128)
     SBP_TILE(64, 64)
-    SBP_DMA_TILE(256, 256, 64, 2, 2, 4)
-    SBP_DMA_TILE(256, 128, 64, SBP_NS_256x128, 2, 2)
-    SBP_DMA_TILE(128, 256, 64, SBP_NS_256x128, 2, 2)
-    SBP_DMA_TILE(128, 128, 64, SBP_NS_128x128, 2, 2)
-    SBP_DMA_TILE(128, 128, 64, 2, 2, 2)
-    SBP_DMA_TILE(128, 64, 64, SBP_NS_128x64, 2, 2)
-    SBP_DMA_TILE(64, 128, 64, SBP_NS_128x64, 2, 2)
-    SBP_DMA_TILE(64, 64, 64, SBP_NS_64x64, 2, 2)
+    SBP_DMA_INSTANCES(SBP_DMA_TILE)
 #undef SBP_TILE
 #undef SBP_DMA_TILE
     return hipErrorInvalidValue;
@@ -82,17 +109,20 @@ static inline sbpk::GemmArgs make_args(const Gemm &g, const Plan &p, float *ws) 
     a.ws = ws;
     a.vec_a = ((reinterpret_cast<uintptr_t>(g.A) & 15) == 0) && (g.lda % 8 == 0);
     a.vec_b = ((reinterpret_cast<uintptr_t>(g.B) & 15) == 0) && (g.ldb % 8 == 0);
+    const bool c16 = (reinterpret_cast<uintptr_t>(g.C) & 15) == 0;
+    a.vec_c4 = c16 && (g.ldc % 4 == 0);
+    a.vec_c8 = c16 && (g.ldc % 8 == 0);
     return a;
 }
 
 template <bool AK, bool BK_>
 static hipError_t launch_orient(const Gemm &g, const Plan &p, float *ws, hipStream_t s) {
     const sbpk::GemmArgs a = make_args(g, p, ws);
-    const int grid = a.tiles_m * a.tiles_n * a.splits;
+    const int items = a.tiles_m * a.tiles_n * a.splits;
     // with splits the GEMM writes fp32 partials, whatever the output dtype
     hipError_t e = (g.out_dtype == DT_F32 || p.splits > 1)
-                       ? launch_tile<AK, BK_, true>(p.bm, p.bn, p.ns, p.dma, a, grid, s)
-                       : launch_tile<AK, BK_, false>(p.bm, p.bn, p.ns, p.dma, a, grid, s);
+                       ? launch_tile<AK, BK_, true>(p, a, items, s)
+                       : launch_tile<AK, BK_, false>(p, a, items, s);
     if (e != hipSuccess || p.splits == 1) return e;
     return launch_split_reduce(g, p.splits, ws, s);
 }

@@ -23,6 +23,9 @@ struct TileClass {
     int occ;      // workgroups that fit one compute unit (LDS-limited)
     double eff;   // rate factor of the tile's operand stream (see model below)
     int ns;       // pipelined kernel stages (0 = default instance)
+    int kg = 1;   // pipelined kernel reduction groups (2: eight waves)
+    int epi = 0;  // pipelined kernel epilogue
+    int occ_persist = 0;   // persistent workgroups per CU (0: one per item)
 };
 
 // Generic kernel (register-staged, one step ahead): slower per byte.
@@ -51,7 +54,29 @@ constexpr double kHbm = 5.0e12;                 // sustained HBM bytes/s (mixed 
 constexpr double kRoundLatency = 2.0e-6;        // pipeline fill + epilogue per wave
 constexpr double kLaunch = 2.0e-6;              // extra launch (reduce kernel)
 
-thread_local int ov_bm = 0, ov_bn = 0, ov_splits = 1, ov_kernel = 0;
+thread_local int ov_bm = 0, ov_bn = 0, ov_splits = 1, ov_kernel = 0, ov_occ = 0;
+
+// Pipelined instances reachable through the plan override, by kernel code
+// (see sbp_set_plan_override): code, tile, stages (0 = the tile's default),
+// reduction groups, epilogue.
+struct Instance {
+    int code, bm, bn, ns, kg, epi;
+};
+constexpr int E_DIRECT = 0, E_STAGED = 1, E_ROWQ = 2;   // = sbpk::EPI_*
+const Instance kInstances[] = {
+    {1, 256, 256, 0, 1, E_DIRECT}, {1, 256, 128, 0, 1, E_DIRECT}, {1, 128, 256, 0, 1, E_DIRECT},
+    {1, 128, 128, 0, 1, E_DIRECT}, {1, 128, 64, 0, 1, E_DIRECT},  {1, 64, 128, 0, 1, E_DIRECT},
+    {1, 64, 64, 0, 1, E_DIRECT},   {4, 128, 128, 2, 1, E_DIRECT}, {5, 256, 128, 0, 2, E_STAGED},
+    {5, 128, 256, 0, 2, E_STAGED}, {5, 128, 128, 0, 2, E_STAGED}, {6, 256, 256, 0, 1, E_ROWQ},
+    {6, 128, 128, 2, 1, E_ROWQ},   {7, 256, 128, 0, 2, E_ROWQ},   {7, 128, 256, 0, 2, E_ROWQ},
+    {7, 128, 128, 0, 2, E_ROWQ},
+};
+
+const Instance *find_instance(int code, int bm, int bn) {
+    for (const Instance &i : kInstances)
+        if (i.code == code && i.bm == bm && i.bn == bn) return &i;
+    return nullptr;
+}
 
 int kblocks(int64_t k) { return (int)((k + 63) / 64); }
 
@@ -131,6 +156,22 @@ bool tile_supported(int bm, int bn, bool dma) {
     return false;
 }
 
+bool override_supported(int bm, int bn, int kernel) {
+    if (kernel == 0 || kernel == 2) return tile_supported(bm, bn, true);
+    return find_instance(kernel, bm, bn) != nullptr;
+}
+
+int kernel_code(const Plan &p) {
+    if (!p.dma) return 2;
+    for (const Instance &i : kInstances)
+        if (i.bm == p.bm && i.bn == p.bn && i.kg == p.kg && i.epi == p.epi &&
+            (i.ns == p.ns || (i.ns == 0 && p.ns == 0)))
+            return i.code;
+    return 1;
+}
+
+void set_override_occ(int occ) { ov_occ = occ < 0 ? 0 : occ; }
+
 void set_override(int bm, int bn, int splits, int kernel) {
     ov_bm = bm;
     ov_bn = bn;
@@ -154,6 +195,20 @@ bool dma_eligible(const Gemm &g) {
 
 static Plan plan_uncached(const Gemm &g);
 
+int device_cus() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
+}
+
 namespace {
 struct Key {
     int64_t v[9];
@@ -172,7 +227,7 @@ struct KeyHash {
 };
 Key key_of(const Gemm &g, bool dma) {
     return Key{{g.orient, g.in_dtype, g.out_dtype, g.m, g.n, g.k, dma ? 1 : 0,
-                ov_bm * 1000 + ov_bn, ov_splits * 10 + ov_kernel}};
+                ov_bm * 1000 + ov_bn, (ov_splits * 100 + ov_kernel) * 100 + ov_occ}};
 }
 thread_local std::unordered_map<Key, Plan, KeyHash> plan_cache;
 }  // namespace
@@ -197,14 +252,19 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
         pw->bm = pd->bm;
         pw->bn = pd->bn;
         pw->ns = pd->ns;
+        pw->kg = pd->kg;
+        pw->epi = pd->epi;
+        pd->occ = pw->occ = 0;   // the grouped launch runs one workgroup per item
         return pd->dma && pw->dma &&
                (double)pd->splits * gd.m * gd.n + (double)pw->splits * gw.m * gw.n <=
                    (double)WS_FLOATS;
     }
     const TileClass *sep_d = nullptr, *sep_w = nullptr;
     for (const TileClass &t : kDma) {
-        if (t.bm == pd->bm && t.bn == pd->bn && t.ns == pd->ns) sep_d = &t;
-        if (t.bm == pw->bm && t.bn == pw->bn && t.ns == pw->ns) sep_w = &t;
+        if (t.bm == pd->bm && t.bn == pd->bn && t.ns == pd->ns && t.kg == pd->kg && t.epi == pd->epi)
+            sep_d = &t;
+        if (t.bm == pw->bm && t.bn == pw->bn && t.ns == pw->ns && t.kg == pw->kg && t.epi == pw->epi)
+            sep_w = &t;
     }
     if (!sep_d || !sep_w) return false;
     double best = model_time(gd, *sep_d, pd->splits, pd->kblk_per_split) +
@@ -233,8 +293,8 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
                 if (tm < best * 0.97) {
                     best = tm;
                     grouped = true;
-                    *pd = Plan{t.bm, t.bn, sd, perd, true, t.ns};
-                    *pw = Plan{t.bm, t.bn, sw, perw, true, t.ns};
+                    *pd = Plan{t.bm, t.bn, sd, perd, true, t.ns, t.kg, t.epi};
+                    *pw = Plan{t.bm, t.bn, sw, perw, true, t.ns, t.kg, t.epi};
                 }
             }
         }
@@ -247,11 +307,21 @@ static Plan plan_uncached(const Gemm &g) {
     const bool dma = dma_eligible(g);
     Plan best{128, 128, 1, std::max(1, kb_total), dma};
     if (ov_bm != 0) {
-        // kernel: 0 either, 1 pipelined (if eligible), 2 generic, 4 pipelined
-        // two-stage 128 x 128 (if eligible)
+        // kernel: 0 or 1 the tile's default pipelined instance (if eligible),
+        // 2 generic, other codes the instance of kInstances (if eligible);
+        // a product the pipelined kernel cannot read runs the generic kernel
         const bool use_dma = dma && ov_kernel != 2;
-        Plan p{ov_bm, ov_bn, 1, 1, use_dma, (use_dma && ov_kernel == 4) ? 2 : 0};
-        if (!tile_supported(p.bm, p.bn, use_dma)) p.bn = 128;   // 256x256 only pipelined
+        Plan p{ov_bm, ov_bn, 1, 1, use_dma};
+        if (use_dma) {
+            const Instance *in = find_instance(ov_kernel == 0 ? 1 : ov_kernel, ov_bm, ov_bn);
+            if (!in) in = find_instance(1, ov_bm, ov_bn);
+            p.ns = in->ns;
+            p.kg = in->kg;
+            p.epi = in->epi;
+            p.occ = ov_occ;
+        } else if (!tile_supported(p.bm, p.bn, false)) {
+            p.bn = 128;   // 256x256 only pipelined
+        }
         split_of(kb_total, ov_splits, &p.splits, &p.kblk_per_split);
         while (p.splits > 1 && !fits_ws(g, p.splits))
             split_of(kb_total, p.splits - 1, &p.splits, &p.kblk_per_split);
@@ -274,7 +344,7 @@ static Plan plan_uncached(const Gemm &g) {
             const double tm = model_time(g, t, splits, per);
             if (tm < best_t * 0.999) {
                 best_t = tm;
-                best = Plan{t.bm, t.bn, splits, per, dma, t.ns};
+                best = Plan{t.bm, t.bn, splits, per, dma, t.ns, t.kg, t.epi, t.occ_persist};
             }
         }
     }

@@ -302,6 +302,11 @@ int prep_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_
 
 // Both backward products: one grouped launch when the planner finds it
 // faster, else two launches. An empty product is skipped.
+int hip_fail(hipError_t e) {
+    g_last_hip = (int)e;
+    return SBP_ERR_HIP;
+}
+
 int run_pair(const sbpi::Gemm &gd, const sbpi::Gemm &gw, hipStream_t s) {
     const bool ed = gd.m == 0 || gd.n == 0, ew = gw.m == 0 || gw.n == 0;
     if (gd.in_dtype == SBP_BF16 && !ed && !ew) {
@@ -313,10 +318,7 @@ int run_pair(const sbpi::Gemm &gd, const sbpi::Gemm &gw, hipStream_t s) {
                 if (rc) return rc;
             }
             hipError_t e = sbpi::launch_bf16_bwd_group(gd, pd, gw, pw, w.ws, s);
-            if (e != hipSuccess) {
-                g_last_hip = (int)e;
-                return SBP_ERR_HIP;
-            }
+            if (e != hipSuccess) return hip_fail(e);
             return SBP_OK;
         }
     }
@@ -474,7 +476,7 @@ int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype, int32_t 
     *tile_m = p.bm;
     *tile_n = p.bn;
     *splits = p.splits;
-    *kernel = p.dma ? (p.ns == 2 ? 4 : 1) : 2;
+    *kernel = sbpi::kernel_code(p);
     return SBP_OK;
 }
 
@@ -501,15 +503,17 @@ int sbp_plan_bwd(int64_t md, int64_t nd, int64_t kd, int32_t out_d, int64_t mw, 
     return SBP_OK;
 }
 
-int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits, int32_t kernel) {
+int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits, int32_t kernel,
+                          int32_t wgs_per_cu) {
     if (tile_m == 0) {
         sbpi::set_override(0, 0, 1, 0);
+        sbpi::set_override_occ(0);
         return SBP_OK;
     }
-    if (kernel < 0 || kernel > 4 || kernel == 3) return SBP_ERR_SHAPE;
-    if (!sbpi::tile_supported(tile_m, tile_n, true) || splits < 1) return SBP_ERR_SHAPE;
-    if (kernel == 4 && (tile_m != 128 || tile_n != 128)) return SBP_ERR_SHAPE;
+    if (splits < 1 || wgs_per_cu < 0 || wgs_per_cu > 8) return SBP_ERR_SHAPE;
+    if (!sbpi::override_supported(tile_m, tile_n, kernel)) return SBP_ERR_SHAPE;
     sbpi::set_override(tile_m, tile_n, splits, kernel);
+    sbpi::set_override_occ(wgs_per_cu);
     return SBP_OK;
 }
 

@@ -110,7 +110,7 @@ def lib():
         L.sbp_plan.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32),
                                P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_int32)]
-        L.sbp_set_plan_override.argtypes = [ctypes.c_int32] * 4
+        L.sbp_set_plan_override.argtypes = [ctypes.c_int32] * 5
         L.sbp_profile_begin.argtypes = [ctypes.c_int]
         L.sbp_profile_end.argtypes = [ctypes.c_void_p, ctypes.c_char_p, ctypes.c_int]
         L.sbp_plan_bwd.argtypes = ([ctypes.c_int64] * 3 + [ctypes.c_int32] + [ctypes.c_int64] * 3 +
@@ -215,12 +215,13 @@ def sbp_last_hip_error() -> int:
 
 
 KERNEL_AUTO, KERNEL_PIPELINED, KERNEL_GENERIC, KERNEL_F32, KERNEL_PIPELINED_2STAGE = 0, 1, 2, 3, 4
+KERNEL_GROUPS_STAGED, KERNEL_ROWQ, KERNEL_GROUPS_ROWQ = 5, 6, 7
 
 
 def sbp_plan(op: int, m: int, n: int, k: int, in_dtype: int, out_dtype: int):
     """(tile_m, tile_n, splits, kernel) the library would launch for this product
-    with aligned operands; kernel is KERNEL_PIPELINED, KERNEL_PIPELINED_2STAGE,
-    KERNEL_GENERIC or KERNEL_F32."""
+    with aligned operands; kernel is KERNEL_F32 or one of the bf16 instance codes
+    of sbp_set_plan_override (KERNEL_PIPELINED ... KERNEL_GROUPS_ROWQ)."""
     tm, tn, sp, kn = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     _check(lib().sbp_plan(op, m, n, k, in_dtype, out_dtype, ctypes.byref(tm), ctypes.byref(tn),
                           ctypes.byref(sp), ctypes.byref(kn)))
@@ -250,5 +251,6 @@ def sbp_profile_end(capacity: int):
     return [(raw[i * nl:(i + 1) * nl].split(b"\0", 1)[0].decode(), us[i]) for i in range(n)]
 
 
-def sbp_set_plan_override(tile_m: int, tile_n: int, splits: int, kernel: int = 0) -> None:
-    _check(lib().sbp_set_plan_override(tile_m, tile_n, splits, kernel))
+def sbp_set_plan_override(tile_m: int, tile_n: int, splits: int, kernel: int = 0,
+                          wgs_per_cu: int = 0) -> None:
+    _check(lib().sbp_set_plan_override(tile_m, tile_n, splits, kernel, wgs_per_cu))

@@ -12,8 +12,12 @@ SIG_ID = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS}
 OP_ID = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
 TILES = [(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
 KERNELS = (1, 2)   # pipelined direct-to-LDS, generic
-# (tile, kernel) pairs beyond TILES x KERNELS: the two-stage pipelined 128x128
-EXTRA_TILE_KERNELS = [((128, 128), 4)]
+# (tile, kernel) pairs beyond TILES x KERNELS: the two-stage pipelined 128x128,
+# the eight-wave instances with two reduction groups (staged and row-quad
+# epilogues) and the row-quad instances with one group
+EXTRA_TILE_KERNELS = [((128, 128), 4), ((128, 128), 5), ((256, 128), 5), ((128, 256), 5),
+                      ((256, 256), 6), ((128, 128), 6), ((128, 128), 7), ((256, 128), 7),
+                      ((128, 256), 7)]
 
 
 def say(*a):

@@ -238,3 +238,36 @@ def test_split_reduction_is_deterministic():
             assert torch.equal(a, b)
     finally:
         sbp.sbp_set_plan_override(0, 0, 1)
+
+
+PERSISTENT = [((128, 128), 1), ((256, 256), 6), ((128, 128), 6), ((128, 128), 7),
+              ((256, 128), 7), ((128, 256), 7)]
+
+
+def test_exact_persistent_launches():
+    # grids capped at one workgroup per compute unit: each workgroup takes
+    # several work items in turn (more items than compute units), reusing its
+    # LDS pipeline and leaving each item's stores in flight
+    M, K, N = 4096, 200, 2176
+    X, W, dY = _int_inputs(M, K, N, 1300)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    cases = [("DP", 1, 0), ("KS", 2, 1)]
+    want = {(sig, op, p, r): oracle_full(op, sig, p, r, Xh, Wh, dYh)
+            for sig, p, r in cases for op in OPS}
+    try:
+        for tile, kernel in PERSISTENT:
+            for splits in (1, 5):
+                sbp.sbp_set_plan_override(tile[0], tile[1], splits, kernel, 1)
+                for sig, p, r in cases:
+                    for op in OPS:
+                        say("persistent", tile, kernel, splits, sig, p, r, op)
+                        out, st = run_gpu(op, sig, p, r, X, W, dY)
+                        expect_state(op, sig, p, r, st)
+                        w = want[(sig, op, p, r)]
+                        if out.dtype == torch.bfloat16:
+                            assert np.array_equal(out_bits(out), oracle.round_bf16(w)), \
+                                (tile, kernel, splits, sig, op)
+                        else:
+                            assert np.array_equal(decode(out), w), (tile, kernel, splits, sig, op)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
