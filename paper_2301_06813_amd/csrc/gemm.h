@@ -38,6 +38,7 @@ struct Plan {
     int kg = 1;            // pipelined kernel: reduction groups of waves (1 or 2)
     int epi = 0;           // pipelined kernel: epilogue (sbpk::EPI_DIRECT / _STAGED / _ROWQ)
     int occ = 0;           // persistent workgroups per compute unit (0: one per work item)
+    int bk = 64;           // pipelined kernel: reduction elements per stage (64 or 32)
 };
 
 // Compute units of the current device (cached per device).

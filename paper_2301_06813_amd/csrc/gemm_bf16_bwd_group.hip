@@ -11,14 +11,14 @@ hipError_t launch_group_tile(const Plan &p, const sbpk::GemmArgs &d, const sbpk:
                              int data_first, int grid, hipStream_t s) {
     char name[192];
     const char *tf[2] = {"false", "true"};
-#define SBP_BWD_TILE(BM_, BN_, NS_, WGM_, WGN_, KG_, EPI_)                                 \
-    if (p.bm == BM_ && p.bn == BN_ && (p.ns == 0 || p.ns == NS_) && p.kg == KG_ &&         \
-        p.epi == EPI_) {                                                                   \
+#define SBP_BWD_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_)                           \
+    if (p.bm == BM_ && p.bn == BN_ && p.bk == BKD_ && (p.ns == 0 || p.ns == NS_) &&         \
+        p.kg == KG_ && p.epi == EPI_) {                                                    \
         snprintf(name, sizeof(name),                                                       \
-                 "gemm_bf16_dma_bwd_kernel<%d, %d, 64, %d, %d, %d, %d, %d, %s, %s>", BM_,  \
-                 BN_, NS_, WGM_, WGN_, KG_, EPI_, tf[OD], tf[OW]);                         \
+                 "gemm_bf16_dma_bwd_kernel<%d, %d, %d, %d, %d, %d, %d, %d, %s, %s>", BM_,  \
+                 BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, tf[OD], tf[OW]);                   \
         return launch_kernel(                                                              \
-            sbpk::gemm_bf16_dma_bwd_kernel<BM_, BN_, 64, NS_, WGM_, WGN_, KG_, EPI_, OD,   \
+            sbpk::gemm_bf16_dma_bwd_kernel<BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, OD, \
                                            OW>,                                            \
             name, dim3(grid), dim3(64 * WGM_ * WGN_ * KG_), s, d, w, data_first);          \
     }
@@ -31,7 +31,8 @@ hipError_t launch_group_tile(const Plan &p, const sbpk::GemmArgs &d, const sbpk:
 
 hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
                                  const Plan &pw, float *ws, hipStream_t s) {
-    if (pd.bm != pw.bm || pd.bn != pw.bn || pd.ns != pw.ns || pd.kg != pw.kg || pd.epi != pw.epi ||
+    if (pd.bm != pw.bm || pd.bn != pw.bn || pd.bk != pw.bk || pd.ns != pw.ns || pd.kg != pw.kg ||
+        pd.epi != pw.epi ||
         !pd.dma || !pw.dma)
         return hipErrorInvalidValue;
     float *ws_w = ws;

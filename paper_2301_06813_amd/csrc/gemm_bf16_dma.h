@@ -182,25 +182,26 @@ struct DmaStage {
     static constexpr int BYTES = A_BYTES + B_BYTES;
 };
 
-// Output rows of the staged epilogue are padded by 8 floats: the two half-waves
-// of a 32 x 32 MFMA block write rows 4 apart, and 4 (BN + 8) = 32 mod 64
-// floats puts them on disjoint LDS banks.
-template <int BN>
+// Output rows of the staged epilogue are padded by 8 floats where the LDS
+// allows: the two half-waves of a 32 x 32 MFMA block write rows 4 apart, and
+// 4 (BN + 8) = 32 mod 64 floats puts them on disjoint LDS banks (unpadded, the
+// two halves share banks: a 2-way conflict on those writes).
+template <int BN, int BM = 0, int BYTES = 1 << 30>
 struct StageRow {
-    static constexpr int LD = BN + 8;   // floats per staged output row
+    // floats per staged output row: padded when the padded tile fits
+    static constexpr int LD = (BM * (BN + 8) * 4 <= BYTES) ? BN + 8 : BN;
 };
 
 // Stores the BM x BN fp32 tile staged in LDS (`tile`, row stride
-// StageRow<BN>::LD floats) to rows [m0, m0 + BM) x columns [n0, n0 + BN) of C
-// (ld `ldc`, clipped to m x n), by all NT threads: each thread moves whole
+// LD floats) to rows [m0, m0 + BM) x columns [n0, n0 + BN) of C
+// (ld `ldc`, clipped to m x n), by all NT_ threads: each thread moves whole
 // 16-byte chunks along a row -- 4 floats, or 8 values rounded to bf16 -- so a
 // wave writes whole contiguous row segments. `vec`: C's base and ldc allow
 // aligned 16-byte stores; otherwise (and at the right edge) elements are
 // stored one by one.
-template <int BM, int BN, int NT_, bool F32>
+template <int BM, int BN, int LD, int NT_, bool F32>
 __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t ldc, int m,
                                              int n, int m0, int n0, bool vec, int tid) {
-    constexpr int LD = StageRow<BN>::LD;
     constexpr int EPC = F32 ? 4 : 8;             // output elements per 16-byte chunk
     constexpr int CPR = BN / EPC;                // chunks per tile row
     constexpr int ITER = BM * CPR / NT_;
@@ -275,7 +276,8 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     constexpr bool SWAP = EPI == EPI_ROWQ;
     static_assert(KG == 1 || KG == 2, "one or two reduction groups");
     static_assert(BKD % (16 * KG) == 0, "reduction step not divisible among groups");
-    static_assert(EPI != EPI_STAGED || BM * StageRow<BN>::LD * 4 <= NS * STAGE,
+    constexpr int SLD = StageRow<BN, BM, NS * STAGE>::LD;
+    static_assert(EPI != EPI_STAGED || BM * SLD * 4 <= NS * STAGE,
                   "staged output tile does not fit the pipeline's LDS");
     static_assert(KG == 1 || NSW * MI * NI * 64 * 64 <= NS * STAGE,
                   "group partial sums do not fit the pipeline's LDS");
@@ -456,7 +458,7 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     }
 
     if constexpr (EPI == EPI_STAGED) {
-        constexpr int LD = StageRow<BN>::LD;
+        constexpr int LD = SLD;
         float *tile = reinterpret_cast<float *>(smem);
         // element (r, c) of 32 x 32 block (i, j) of this wave, MFMA layout:
         // c = lane % 32, r = 8 (q / 4) + 4 (lane / 32) + q % 4 for register q
@@ -489,11 +491,11 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         }
         __syncthreads();
         if (partial)
-            store_staged<BM, BN, 64 * NW, true>(tile, ws_out, g.n, g.m, g.n, m0, n0,
-                                                g.n % 4 == 0, tid);
+            store_staged<BM, BN, LD, 64 * NW, true>(tile, ws_out, g.n, g.m, g.n, m0, n0,
+                                                    g.n % 4 == 0, tid);
         else
-            store_staged<BM, BN, 64 * NW, OUT_F32>(tile, g.C, g.ldc, g.m, g.n, m0, n0,
-                                                   OUT_F32 ? g.vec_c4 : g.vec_c8, tid);
+            store_staged<BM, BN, LD, 64 * NW, OUT_F32>(tile, g.C, g.ldc, g.m, g.n, m0, n0,
+                                                       OUT_F32 ? g.vec_c4 : g.vec_c8, tid);
         __syncthreads();   // the staged tile is free again
         return;
     }

@@ -29,22 +29,27 @@ namespace sbpi {
 // groups and epilogue. The macro list is shared by the single-product and
 // the grouped backward launchers.
 #define SBP_DMA_INSTANCES(X)                                    \
-    X(256, 256, 2, 2, 4, 1, sbpk::EPI_DIRECT)                   \
-    X(256, 256, 2, 2, 4, 1, sbpk::EPI_ROWQ)                     \
-    X(256, 128, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
-    X(128, 256, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
-    X(128, 128, SBP_NS_128x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
-    X(128, 128, 2, 2, 2, 1, sbpk::EPI_DIRECT)                   \
-    X(128, 128, 2, 2, 2, 1, sbpk::EPI_ROWQ)                     \
-    X(128, 64, SBP_NS_128x64, 2, 2, 1, sbpk::EPI_DIRECT)        \
-    X(64, 128, SBP_NS_128x64, 2, 2, 1, sbpk::EPI_DIRECT)        \
-    X(64, 64, SBP_NS_64x64, 2, 2, 1, sbpk::EPI_DIRECT)          \
-    X(256, 128, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_STAGED)      \
-    X(128, 256, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_STAGED)      \
-    X(128, 128, SBP_NS_128x128, 2, 2, 2, sbpk::EPI_STAGED)      \
-    X(256, 128, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_ROWQ)        \
-    X(128, 256, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_ROWQ)        \
-    X(128, 128, SBP_NS_128x128, 2, 2, 2, sbpk::EPI_ROWQ)
+    X(256, 256, 64, 2, 2, 4, 1, sbpk::EPI_DIRECT)               \
+    X(256, 256, 64, 2, 2, 4, 1, sbpk::EPI_ROWQ)                     \
+    X(256, 128, 64, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
+    X(128, 256, 64, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
+    X(128, 128, 64, SBP_NS_128x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
+    X(128, 128, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)                   \
+    X(128, 128, 64, 2, 2, 2, 1, sbpk::EPI_ROWQ)                     \
+    X(128, 64, 64, SBP_NS_128x64, 2, 2, 1, sbpk::EPI_DIRECT)        \
+    X(64, 128, 64, SBP_NS_128x64, 2, 2, 1, sbpk::EPI_DIRECT)        \
+    X(64, 64, 64, SBP_NS_64x64, 2, 2, 1, sbpk::EPI_DIRECT)          \
+    X(256, 128, 64, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_STAGED)      \
+    X(128, 256, 64, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_STAGED)      \
+    X(128, 128, 64, SBP_NS_128x128, 2, 2, 2, sbpk::EPI_STAGED)      \
+    X(256, 128, 64, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_ROWQ)        \
+    X(128, 256, 64, SBP_NS_256x128, 2, 2, 2, sbpk::EPI_ROWQ)        \
+    X(128, 128, 64, SBP_NS_128x128, 2, 2, 2, sbpk::EPI_ROWQ) \
+    X(256, 256, 32, 5, 2, 4, 1, sbpk::EPI_DIRECT)               \
+    X(256, 128, 32, 6, 2, 2, 2, sbpk::EPI_STAGED)               \
+    X(128, 256, 32, 6, 2, 2, 2, sbpk::EPI_STAGED)               \
+    X(128, 128, 32, 8, 2, 2, 2, sbpk::EPI_STAGED)               \
+    X(128, 128, 64, 2, 2, 2, 2, sbpk::EPI_STAGED)
 
 // Grid of a launch of `items` work items under plan p: one workgroup per item,
 // or (persistent plans) at most occ workgroups per compute unit, a multiple of 8.
@@ -67,14 +72,14 @@ static hipError_t launch_tile(const Plan &p, const sbpk::GemmArgs &a, int items,
         return launch_kernel(sbpk::gemm_bf16_kernel<BM_, BN_, AK, BK_, OUTF>, name,         \
                              dim3(items), dim3(sbpk::NT), s, a);                            \
     }
-#define SBP_DMA_TILE(BM_, BN_, NS_, WGM_, WGN_, KG_, EPI_)                                  \
-    if (p.dma && p.bm == BM_ && p.bn == BN_ && (p.ns == 0 || p.ns == NS_) && p.kg == KG_ && \
-        p.epi == EPI_) {                                                                    \
+#define SBP_DMA_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_)                            \
+    if (p.dma && p.bm == BM_ && p.bn == BN_ && p.bk == BKD_ &&                               \
+        (p.ns == 0 || p.ns == NS_) && p.kg == KG_ && p.epi == EPI_) {                       \
         snprintf(name, sizeof(name),                                                        \
-                 "gemm_bf16_dma_kernel<%d, %d, 64, %d, %d, %d, %d, %d, %s, %s, %s>", BM_,   \
-                 BN_, NS_, WGM_, WGN_, KG_, EPI_, tf[AK], tf[BK_], tf[OUTF]);               \
+                 "gemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %d, %s, %s, %s>", BM_,   \
+                 BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, tf[AK], tf[BK_], tf[OUTF]);         \
         return launch_kernel(                                                               \
-            sbpk::gemm_bf16_dma_kernel<BM_, BN_, 64, NS_, WGM_, WGN_, KG_, EPI_, AK, BK_,   \
+            sbpk::gemm_bf16_dma_kernel<BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, AK, BK_, \
                                        OUTF>,                                               \
             name, dim3(grid), dim3(64 * WGM_ * WGN_ * KG_), s, a);                          \
     }

@@ -1,0 +1,196 @@
+"""Plan tuner: times every kernel plan the library can run for each local
+product shape of the workloads on this GPU, and writes the fastest as the
+library's tuned plan table (csrc/tuned_plans.inc).
+
+    python -m paper_2301_06813_amd.tune [--out PATH] [--workloads 2,3,4,5]
+
+A plan is (output tile, kernel instance, reduction splits, persistent
+workgroups per compute unit); candidates are set with sbp_set_plan_override
+and timed through the C ABI on the real shard views of every rank (so operand
+alignment, and with it the eligible kernels, is that of the real calls),
+replayed from a HIP graph over rotating input sets larger than the 256 MB
+Infinity Cache. The table is keyed the way the planner looks plans up:
+(orientation, output dtype, m, n, k, pipelined-kernel eligibility). Products
+of other shapes keep the planner's analytic model. Rebuild the library after
+writing a new table.
+"""
+from __future__ import annotations
+
+import argparse
+import os
+import sys
+import time
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+TILES = [(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
+CODES = (1, 4, 5, 6, 7, 8, 9, 10)   # pipelined instances; 2 (generic) for the rest
+SPLITS = (1, 2, 3, 4, 6, 8, 12, 16)
+ORIENT = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def product_cases(wl_ids):
+    """{key: (workload, linear, op, rank)} for every distinct local product."""
+    import torch
+    from . import linear, sbp, workloads
+    wls = {2: workloads.ffn_shard, 3: workloads.attention_dp, 4: workloads.vgg_head,
+           5: workloads.transformer_step}
+    cases = {}
+    for c in wl_ids:
+        wl = wls[c]()
+        for lin in wl.linears:
+            for r in wl.ranks:
+                L = linear.layouts(lin.sig, wl.p, r)
+                for op in ("fwd", "bwd_data", "bwd_weight"):
+                    rows, cols = linear.out_shape(op, L, lin.M, lin.K, lin.N)
+                    k = {"fwd": sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols,
+                         "bwd_data": sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols,
+                         "bwd_weight": sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows}[op]
+                    f32 = linear.out_dtype(op, L, wl.dtype) == torch.float32
+                    key = (ORIENT[op], int(f32), rows, cols, k, _eligible(op, L, lin, wl.p))
+                    cases.setdefault(key, (wl, lin, op, r))
+    return cases
+
+
+def _eligible(op, L, lin, p):
+    """Whether the pipelined kernel can read rank r's operand views: 16-byte
+    aligned shard offsets, and leading dimensions and contiguous extents (the
+    columns of a row-major share) that are multiples of 8 elements."""
+    from . import sbp
+
+    def ok(layout, rows, cols):
+        s = sbp.sbp_shard_index(layout, rows, cols)
+        return (s.row_off * cols + s.col_off) % 8 == 0 and cols % 8 == 0 and s.cols % 8 == 0
+
+    M, K, N = lin.M, lin.K, lin.N
+    if op == "fwd":
+        return int(ok(L["x"], M, K) and ok(L["w"], K, N))
+    if op == "bwd_data":
+        return int(ok(L["dy"], M, N) and ok(L["w"], K, N))
+    return int(ok(L["x"], M, K) and ok(L["dy"], M, N))
+
+
+def valid_candidates(sbp, key, tiles_n_items):
+    """(tile_m, tile_n, splits, kernel, wgs_per_cu) plans to time for key (the
+    argument order of sbp_set_plan_override)."""
+    orient, f32, m, n, k, dma = key
+    kblocks = max(1, (k + 63) // 64)
+    out = []
+    codes = CODES if dma else (2,)
+    for (bm, bn) in TILES:
+        tiles = ((m + bm - 1) // bm) * ((n + bn - 1) // bn)
+        for code in codes:
+            try:
+                sbp.sbp_set_plan_override(bm, bn, 1, code, 0)
+            except sbp.SbpError:
+                continue
+            last = 0
+            for s in SPLITS:
+                per = -(-kblocks // min(s, kblocks))
+                eff = -(-kblocks // per)
+                if eff == last or (eff > 1 and per < 2):
+                    continue
+                last = eff
+                items = tiles * eff
+                if items > 8192 or (eff > 1 and items > 4096):
+                    continue
+                occs = (0,) if (code == 2 or items <= 256) else (0, 1, 2)
+                for occ in occs:
+                    out.append((bm, bn, eff, code, occ))
+    sbp.sbp_set_plan_override(0, 0, 1)
+    return out
+
+
+def time_plan(torch, sbp, fn, plan, reps, stream):
+    sbp.sbp_set_plan_override(*plan)
+    try:
+        with torch.cuda.stream(stream):
+            fn()           # first call on this stream may allocate the workspace
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                for _ in range(reps):
+                    fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        # replay() runs on the current stream: bracket it there
+        e0.record()
+        for _ in range(3):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (3 * reps)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--out", default=os.path.join(HERE, "csrc", "tuned_plans.inc"))
+    ap.add_argument("--workloads", default="2,3,4,5")
+    ap.add_argument("--reps", type=int, default=10)
+    args = ap.parse_args()
+
+    import torch
+    from . import linear, sbp, workloads
+    torch.cuda.set_device(0)
+    sbp.lib()
+    cases = product_cases([int(c) for c in args.workloads.split(",")])
+    log("%d distinct local products" % len(cases))
+    stream = torch.cuda.Stream()
+    rows = []
+    t_start = time.time()
+    for key, (wl, lin, op, r) in sorted(cases.items()):
+        orient, f32, m, n, k, dma = key
+        per_set = 2 * (lin.M * lin.K + lin.K * lin.N + lin.M * lin.N)
+        nsets = max(2, min(6, -(-600 * 2 ** 20 // per_set)))
+        sets = []
+        for i in range(nsets):
+            X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
+            out = linear.alloc_out(op, lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype, "cuda")
+            sets.append((X, W, dY, out))
+        it = [0]
+
+        def fn():
+            X, W, dY, out = sets[it[0] % nsets]
+            it[0] += 1
+            linear.run(op, lin.sig, wl.p, r, X, W, dY, out, stream.cuda_stream)
+
+        cands = valid_candidates(sbp, key, None)
+        best = None
+        for plan in cands:
+            try:
+                us = time_plan(torch, sbp, fn, plan, args.reps, stream)
+            except sbp.SbpError as e:
+                log("  plan %s failed: %s" % (plan, e))
+                continue
+            if best is None or us < best[0]:
+                best = (us, plan)
+        auto = time_plan(torch, sbp, fn, (0, 0, 1, 0, 0), args.reps, stream)
+        bm, bn, splits, code, occ = best[1]
+        log("%s %-10s m %5d n %5d k %5d f32 %d dma %d: best %6.1f us %s (model plan %6.1f us), "
+            "%d candidates" % (lin.sig, op, m, n, k, f32, dma, best[0], best[1], auto, len(cands)))
+        rows.append((key, best[1], best[0], auto))
+        del sets
+        torch.cuda.empty_cache()
+    log("tuned in %.0f s" % (time.time() - t_start))
+    dev = torch.cuda.get_device_properties(0)
+    with open(args.out, "w") as f:
+        f.write("// Tuned bf16 plans: generated by paper_2301_06813_amd/tune.py on %s (%d CUs).\n"
+                % (dev.name, dev.multi_processor_count))
+        f.write("// orient, out_f32, m, n, k, pipelined-eligible -> tile_m, tile_n, kernel, "
+                "splits, persistent workgroups per CU; fastest measured, us (model's plan, us)\n")
+        for (orient, f32, m, n, k, dma), (bm, bn, splits, code, occ), us, auto in rows:
+            f.write("{%d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d},  // %.1f (%.1f)\n"
+                    % (orient, f32, m, n, k, dma, bm, bn, code, splits, occ, us, auto))
+    log("wrote %s" % args.out)
+
+
+if __name__ == "__main__":
+    main()

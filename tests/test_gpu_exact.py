@@ -241,7 +241,7 @@ def test_split_reduction_is_deterministic():
 
 
 PERSISTENT = [((128, 128), 1), ((256, 256), 6), ((128, 128), 6), ((128, 128), 7),
-              ((256, 128), 7), ((128, 256), 7)]
+              ((256, 128), 7), ((128, 256), 7), ((256, 256), 8), ((128, 128), 9)]
 
 
 def test_exact_persistent_launches():
