@@ -243,6 +243,15 @@ int sbp_profile_end(float *us, char *names, int name_len);
 int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits,
                           int32_t kernel, int32_t wgs_per_cu);
 
+/* Thread-local choice of how sbp_linear_bwd runs its two products (tuning):
+ * mode 0 = the library's choice, 1 = two launches, one per product, 2 = one
+ * grouped launch on the tile and kernel of sbp_set_plan_override (which must
+ * be set, else mode 2 acts as 0), with that override's splits for the
+ * backward-data product and splits_w for the backward-weight product.
+ * Clearing the plan override (tile_m = 0) also resets this to mode 0.
+ * Errors: SBP_ERR_SHAPE for a mode outside [0, 2] or splits_w < 1. */
+int sbp_set_bwd_override(int32_t mode, int32_t splits_w);
+
 #ifdef __cplusplus
 }
 #endif

@@ -59,6 +59,7 @@ Plan plan_bf16(const Gemm &g);
 bool tile_supported(int bm, int bn, bool dma);
 void set_override(int bm, int bn, int splits, int kernel);   // bm = 0 clears
 void set_override_occ(int occ);                              // 0: one workgroup per item
+void set_bwd_override(int mode, int splits_w);   // 0 default, 1 separate, 2 grouped
 bool override_supported(int bm, int bn, int kernel);
 int kernel_code(const Plan &p);   // kernel code of a plan, as sbp_plan reports it
 

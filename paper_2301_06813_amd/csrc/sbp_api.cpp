@@ -508,12 +508,19 @@ int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits, int32_
     if (tile_m == 0) {
         sbpi::set_override(0, 0, 1, 0);
         sbpi::set_override_occ(0);
+        sbpi::set_bwd_override(0, 1);
         return SBP_OK;
     }
     if (splits < 1 || wgs_per_cu < 0 || wgs_per_cu > 8) return SBP_ERR_SHAPE;
     if (!sbpi::override_supported(tile_m, tile_n, kernel)) return SBP_ERR_SHAPE;
     sbpi::set_override(tile_m, tile_n, splits, kernel);
     sbpi::set_override_occ(wgs_per_cu);
+    return SBP_OK;
+}
+
+int sbp_set_bwd_override(int32_t mode, int32_t splits_w) {
+    if (mode < 0 || mode > 2 || splits_w < 1) return SBP_ERR_SHAPE;
+    sbpi::set_bwd_override(mode, splits_w);
     return SBP_OK;
 }
 

@@ -34,7 +34,8 @@ SBP_GLOBAL, SBP_LOCAL = 0, 1
 
 EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd_data",
            "sbp_linear_bwd_weight", "sbp_linear_bwd", "sbp_strerror", "sbp_last_hip_error", "sbp_plan",
-           "sbp_plan_bwd", "sbp_set_plan_override", "sbp_profile_begin", "sbp_profile_end")
+           "sbp_plan_bwd", "sbp_set_plan_override", "sbp_set_bwd_override", "sbp_profile_begin",
+           "sbp_profile_end")
 
 
 class sbp_layout_t(ctypes.Structure):
@@ -111,6 +112,7 @@ def lib():
                                ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32),
                                P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_int32)]
         L.sbp_set_plan_override.argtypes = [ctypes.c_int32] * 5
+        L.sbp_set_bwd_override.argtypes = [ctypes.c_int32] * 2
         L.sbp_profile_begin.argtypes = [ctypes.c_int]
         L.sbp_profile_end.argtypes = [ctypes.c_void_p, ctypes.c_char_p, ctypes.c_int]
         L.sbp_plan_bwd.argtypes = ([ctypes.c_int64] * 3 + [ctypes.c_int32] + [ctypes.c_int64] * 3 +
@@ -250,6 +252,12 @@ def sbp_profile_end(capacity: int):
         _check(n)
     raw = names.raw
     return [(raw[i * nl:(i + 1) * nl].split(b"\0", 1)[0].decode(), us[i]) for i in range(n)]
+
+
+def sbp_set_bwd_override(mode: int, splits_w: int = 1) -> None:
+    """How sbp_linear_bwd runs its products: 0 library's choice, 1 two launches,
+    2 one grouped launch (plan override's tile/kernel; splits_w for dW)."""
+    _check(lib().sbp_set_bwd_override(mode, splits_w))
 
 
 def sbp_set_plan_override(tile_m: int, tile_n: int, splits: int, kernel: int = 0,

@@ -3,6 +3,13 @@ product shape of the workloads on this GPU, and writes the fastest as the
 library's tuned plan table (csrc/tuned_plans.inc).
 
     python -m paper_2301_06813_amd.tune [--out PATH] [--workloads 2,3,4,5]
+    python -m paper_2301_06813_amd.tune --bwd [--out PATH]
+
+The second form tunes the backward pair of each linear (sbp_linear_bwd):
+one grouped launch of both products on a shared instance, against the two
+separate launches of their tuned plans, and writes csrc/tuned_bwd_plans.inc
+with the pairs whose grouped launch was faster (run it on a library built
+with the single-product table).
 
 A plan is (output tile, kernel instance, reduction splits, persistent
 workgroups per compute unit); candidates are set with sbp_set_plan_override
@@ -105,8 +112,11 @@ def valid_candidates(sbp, key, tiles_n_items):
     return out
 
 
-def time_plan(torch, sbp, fn, plan, reps, stream):
-    sbp.sbp_set_plan_override(*plan)
+def time_plan(torch, sbp, fn, plan, reps, stream, keep=False):
+    """Mean time of fn under plan (set here, and cleared after, unless keep:
+    then the caller has set the overrides)."""
+    if not keep:
+        sbp.sbp_set_plan_override(*plan)
     try:
         with torch.cuda.stream(stream):
             fn()           # first call on this stream may allocate the workspace
@@ -127,23 +137,126 @@ def time_plan(torch, sbp, fn, plan, reps, stream):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (3 * reps)
     finally:
-        sbp.sbp_set_plan_override(0, 0, 1)
+        if not keep:
+            sbp.sbp_set_plan_override(0, 0, 1)
+
+
+GROUP_INSTANCES = [((128, 128), 1), ((128, 128), 4), ((128, 128), 5), ((256, 128), 5),
+                   ((128, 256), 5), ((64, 64), 1), ((128, 64), 1), ((64, 128), 1),
+                   ((256, 256), 1)]
+
+
+def bwd_pairs(wl_ids):
+    """{(key_d, key_w): (workload, linear, rank)} for every distinct backward pair."""
+    import torch
+    from . import linear, sbp, workloads
+    pairs = {}
+    for c in wl_ids:
+        wl = {2: workloads.ffn_shard, 3: workloads.attention_dp, 4: workloads.vgg_head,
+              5: workloads.transformer_step}[c]()
+        for lin in wl.linears:
+            for r in wl.ranks:
+                L = linear.layouts(lin.sig, wl.p, r)
+                keys = []
+                for op in ("bwd_data", "bwd_weight"):
+                    rows, cols = linear.out_shape(op, L, lin.M, lin.K, lin.N)
+                    k = (sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols if op == "bwd_data"
+                         else sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows)
+                    f32 = linear.out_dtype(op, L, wl.dtype) == torch.float32
+                    keys.append((ORIENT[op], int(f32), rows, cols, k, _eligible(op, L, lin, wl.p)))
+                if keys[0][5] and keys[1][5]:
+                    pairs.setdefault(tuple(keys), (wl, lin, r))
+    return pairs
+
+
+def tune_bwd(args, torch, sbp, linear, workloads, stream):
+    pairs = bwd_pairs([int(c) for c in args.workloads.split(",")])
+    log("%d distinct backward pairs" % len(pairs))
+    rows = []
+    for (kd, kw), (wl, lin, r) in sorted(pairs.items()):
+        per_set = 2 * (2 * lin.M * lin.K + lin.K * lin.N + 2 * lin.M * lin.N)
+        nsets = max(2, min(6, -(-600 * 2 ** 20 // per_set)))
+        sets = []
+        for i in range(nsets):
+            X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
+            dX = linear.alloc_out("bwd_data", lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype, "cuda")
+            dW = linear.alloc_out("bwd_weight", lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype,
+                                  "cuda")
+            sets.append((X, W, dY, dX, dW))
+        it = [0]
+
+        def fn():
+            X, W, dY, dX, dW = sets[it[0] % nsets]
+            it[0] += 1
+            linear.run_bwd(lin.sig, wl.p, r, X, W, dY, dX, dW, stream.cuda_stream)
+
+        def timed(plan, mode, sw):
+            sbp.sbp_set_plan_override(*plan)
+            sbp.sbp_set_bwd_override(mode, sw)
+            try:
+                return time_plan(torch, sbp, fn, plan, args.reps, stream, keep=True)
+            finally:
+                sbp.sbp_set_plan_override(0, 0, 1)
+
+        sbp.sbp_set_bwd_override(1, 1)
+        try:
+            sep = time_plan(torch, sbp, fn, (0, 0, 1, 0, 0), args.reps, stream, keep=True)
+        finally:
+            sbp.sbp_set_bwd_override(0, 1)
+        best = None
+        kbd, kbw = max(1, (kd[4] + 63) // 64), max(1, (kw[4] + 63) // 64)
+        for (bm, bn), code in GROUP_INSTANCES:
+            for sd in (1, 2, 4, 8, 16):
+                if sd > 1 and kbd // sd < 2:
+                    continue
+                for sw in (1, 2, 4, 8, 16):
+                    if sw > 1 and kbw // sw < 2:
+                        continue
+                    try:
+                        us = timed((bm, bn, sd, code, 0), 2, sw)
+                    except sbp.SbpError:
+                        continue
+                    if best is None or us < best[0]:
+                        best = (us, (bm, bn, code, sd, sw))
+        log("%s %s d %s w %s: separate %6.1f us, best grouped %6.1f us %s"
+            % (lin.sig, lin.name, kd[2:5], kw[2:5], sep, best[0] if best else -1,
+               best[1] if best else None))
+        if best and best[0] < 0.97 * sep:
+            rows.append((kd, kw, best[1], best[0], sep))
+        del sets
+        torch.cuda.empty_cache()
+    with open(args.out, "w") as f:
+        f.write("// Tuned grouped backward pairs: generated by paper_2301_06813_amd/tune.py --bwd.\n")
+        f.write("// dX m, n, k, fp32, dW m, n, k, fp32 -> tile_m, tile_n, kernel, splits dX, "
+                "splits dW; grouped us (separate us)\n")
+        for kd, kw, (bm, bn, code, sd, sw), us, sep in rows:
+            f.write("{%d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d},  // %.1f (%.1f)\n"
+                    % (kd[2], kd[3], kd[4], kd[1], kw[2], kw[3], kw[4], kw[1], bm, bn, code,
+                       sd, sw, us, sep))
+    log("wrote %s" % args.out)
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--out", default=os.path.join(HERE, "csrc", "tuned_plans.inc"))
+    ap.add_argument("--out", default=None)
     ap.add_argument("--workloads", default="2,3,4,5")
     ap.add_argument("--reps", type=int, default=10)
+    ap.add_argument("--bwd", action="store_true", help="tune grouped backward pairs")
     args = ap.parse_args()
+    if args.out is None:
+        args.out = os.path.join(HERE, "csrc",
+                                "tuned_bwd_plans.inc" if args.bwd else "tuned_plans.inc")
 
     import torch
     from . import linear, sbp, workloads
     torch.cuda.set_device(0)
     sbp.lib()
+    stream = torch.cuda.Stream()
+    if args.bwd:
+        tune_bwd(args, torch, sbp, linear, workloads, stream)
+        return
     cases = product_cases([int(c) for c in args.workloads.split(",")])
     log("%d distinct local products" % len(cases))
-    stream = torch.cuda.Stream()
     rows = []
     t_start = time.time()
     for key, (wl, lin, op, r) in sorted(cases.items()):

@@ -242,7 +242,7 @@ def test_strerror_and_plan(L):
     tm, tn, s, kn = sbp.sbp_plan(2, 1024, 384, 8192, sbp.SBP_BF16, sbp.SBP_BF16)
     assert (tm, tn) in {(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128),
                         (64, 64)}
-    assert s >= 1 and kn in (sbp.KERNEL_PIPELINED, sbp.KERNEL_PIPELINED_2STAGE)
+    assert s >= 1 and kn in (1, 4, 5, 6, 7, 8, 9, 10)   # pipelined bf16 instances
     # a reduction that is not a multiple of 8 cannot use the pipelined kernel
     assert sbp.sbp_plan(0, 256, 256, 125, BF, BF)[3] == sbp.KERNEL_GENERIC
     assert sbp.sbp_plan(0, 64, 64, 64, F32, F32)[3] == sbp.KERNEL_F32
@@ -268,7 +268,29 @@ def test_strerror_and_plan(L):
                                                        sbp.KERNEL_PIPELINED_2STAGE)
     # operands the pipelined kernel cannot read fall back to the generic kernel
     assert sbp.sbp_plan(0, 512, 512, 1001, BF, BF)[3] == sbp.KERNEL_GENERIC
+    # every listed (tile, instance) pair is accepted and reported back
+    for tile, code in (((128, 128), 5), ((256, 128), 5), ((128, 256), 5), ((256, 256), 6),
+                       ((128, 128), 6), ((128, 128), 7), ((256, 128), 7), ((128, 256), 7),
+                       ((256, 256), 8), ((256, 128), 9), ((128, 256), 9), ((128, 128), 9),
+                       ((128, 128), 10)):
+        sbp.sbp_set_plan_override(tile[0], tile[1], 2, code, 1)
+        assert sbp.sbp_plan(0, 2048, 2048, 1024, BF, BF) == (tile[0], tile[1], 2, code)
+    for tile, code in (((64, 64), 6), ((256, 256), 7), ((64, 128), 9), ((256, 128), 10),
+                       ((128, 128), 3), ((128, 128), 11)):
+        with pytest.raises(sbp.SbpError):
+            sbp.sbp_set_plan_override(tile[0], tile[1], 1, code)
+    with pytest.raises(sbp.SbpError):
+        sbp.sbp_set_plan_override(128, 128, 1, 1, 9)     # at most 8 workgroups per CU
+    with pytest.raises(sbp.SbpError):
+        sbp.sbp_set_plan_override(128, 128, 0, 1)        # splits >= 1
     sbp.sbp_set_plan_override(0, 0, 1)
+    # backward override: modes 0..2, splits_w >= 1
+    for mode in (0, 1, 2):
+        sbp.sbp_set_bwd_override(mode, 3)
+    for mode, sw in ((3, 1), (-1, 1), (2, 0)):
+        with pytest.raises(sbp.SbpError):
+            sbp.sbp_set_bwd_override(mode, sw)
+    sbp.sbp_set_bwd_override(0, 1)
 
 
 def _bwd_code(dy, ldy, x, lx, w, lw, dx, dw):

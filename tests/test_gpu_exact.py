@@ -271,3 +271,22 @@ def test_exact_persistent_launches():
                             assert np.array_equal(decode(out), w), (tile, kernel, splits, sig, op)
     finally:
         sbp.sbp_set_plan_override(0, 0, 1)
+
+
+@pytest.mark.parametrize("tile,kernel", [((128, 128), 1), ((128, 128), 5), ((64, 64), 1),
+                                         ((256, 128), 5)],
+                         ids=["128x128-k1", "128x128-k5", "64x64-k1", "256x128-k5"])
+def test_exact_grouped_backward_own_splits(tile, kernel):
+    # one grouped launch whose two products use different reduction splits
+    M, K, N = 304, 1104, 272
+    X, W, dY = _int_inputs(M, K, N, 1400)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    try:
+        for sd, sw in ((1, 5), (3, 1), (2, 4)):
+            sbp.sbp_set_plan_override(tile[0], tile[1], sd, kernel)
+            sbp.sbp_set_bwd_override(2, sw)
+            for sig in SIGS:
+                say("grouped own splits", tile, kernel, sd, sw, sig)
+                _check_exact_bwd(sig, 2, 1, X, W, dY, Xh, Wh, dYh)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
