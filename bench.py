@@ -276,28 +276,42 @@ def main():
     log("per-kernel profile pass")
     n = len(step.calls)
     ksteps = max(1, min(args.steps, 5))
-    per_call = [collections.defaultdict(float) for _ in range(n)]
+    per_call = [None] * n          # per call: [[name, us], ...] in launch order
     with torch.cuda.stream(stream):
         for _ in range(ksteps):
             for i, ks in enumerate(step.profile(sid)):
-                for name, us in ks:
-                    per_call[i][name] += us / ksteps
+                if per_call[i] is None:
+                    per_call[i] = [[name, 0.0] for name, _ in ks]
+                for j, (name, us) in enumerate(ks):
+                    per_call[i][j][1] += us / ksteps
     by_kernel = collections.defaultdict(lambda: [0.0, 0.0, 0.0, 0])
     by_sig = collections.defaultdict(lambda: [0.0, 0.0])
     launches = []
     for m, ks in zip(step.meta, per_call):
-        t_call = sum(ks.values()) * 1e-6
+        t_call = sum(us for _, us in ks) * 1e-6
         by_sig[m["sig"]][0] += t_call
         by_sig[m["sig"]][1] += m["flops"]
-        for name, us in ks.items():
+        gemm_ks = [name for name, _ in ks if name.startswith("gemm")]
+        # the call's product(s) belong to its GEMM kernel(s): one kernel (a
+        # single product, or both backward products grouped) takes them all;
+        # two kernels are the backward-data then the backward-weight product
+        if len(gemm_ks) == 2:
+            shares = {0: m["data"], 1: m["weight"]}
+        else:
+            shares = {0: m}
+        g = 0
+        kd = collections.OrderedDict()
+        for name, us in ks:
             b = by_kernel[name]
             b[0] += us * 1e-6
             b[3] += 1
             if name.startswith("gemm"):
-                # the product(s) of the call belong to its GEMM kernel
-                b[1] += m["flops"]
-                b[2] += m["bytes"]
-        launches.append(dict(m, kernels=dict(ks), us=sum(ks.values())))
+                sh = shares.get(g, {"flops": 0.0, "bytes": 0.0})
+                b[1] += sh["flops"]
+                b[2] += sh["bytes"]
+                g += 1
+            kd[name] = kd.get(name, 0.0) + us
+        launches.append(dict(m, kernels=kd, us=sum(us for _, us in ks)))
     if args.dump:
         with open(args.dump, "w") as f:
             json.dump(launches, f)
@@ -305,15 +319,19 @@ def main():
     dom, (kt, kf, kb, kn) = max(gemms.items(), key=lambda kv: kv[1][0])
     intensity = kf / kb
     if intensity >= RIDGE:
-        roof = {"bound": "mfma", "achieved": kf / kt / 1e12, "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s"}
+        roof = {"bound": "mfma", "achieved": kf / kn / (kt / kn) / 1e12,
+                "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
     else:
-        roof = {"bound": "hbm", "achieved": kb / kt / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+        roof = {"bound": "hbm", "achieved": kb / kn / (kt / kn) / 1e9, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    hbm = counted_traffic(dom)
-    roof["traffic"] = None if hbm is None else {
-        "hbm_bytes_per_launch": hbm, "algorithmic_bytes_per_launch": kb / kn,
-        "ratio": hbm / (kb / kn), "source": "profiles/gemm_bf16_transformer_step_hbm_counters.md"}
+    # HBM bytes per launch of the dominant kernel, from the committed counter
+    # summary (null if it was taken from other kernel sources)
+    roof["traffic"] = counted_traffic(dom)
+    roof["traffic_source"] = ("profiles/gemm_bf16_transformer_step_hbm_counters.md"
+                              if roof["traffic"] is not None else None)
+    roof["algorithmic_bytes_per_launch"] = kb / kn
+    roof["algorithmic_flops_per_launch"] = kf / kn
     roof["kernel"] = dom
     roof["launches_per_step"] = kn
     roof["avg_launch_us"] = kt / kn * 1e6
