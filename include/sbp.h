@@ -221,7 +221,8 @@ int sbp_profile_end(float *us, char *names, int name_len);
  * instance:
  *   0, 1  the tile's default pipelined direct-to-LDS instance;
  *   2     the generic kernel;
- *   4     pipelined with two stages (128x128);
+ *   4     pipelined with two stages (128x128, 128x64, 64x128, 64x64: two or
+ *         more workgroups per compute unit);
  *   5     pipelined, eight waves in two reduction groups, output staged in
  *         LDS (256x128, 128x256, 128x128);
  *   6     pipelined, row-quad epilogue: MFMA operands swapped so each lane

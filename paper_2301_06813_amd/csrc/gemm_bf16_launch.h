@@ -49,7 +49,10 @@ namespace sbpi {
     X(256, 128, 32, 6, 2, 2, 2, sbpk::EPI_STAGED)               \
     X(128, 256, 32, 6, 2, 2, 2, sbpk::EPI_STAGED)               \
     X(128, 128, 32, 8, 2, 2, 2, sbpk::EPI_STAGED)               \
-    X(128, 128, 64, 2, 2, 2, 2, sbpk::EPI_STAGED)
+    X(128, 128, 64, 2, 2, 2, 2, sbpk::EPI_STAGED)               \
+    X(128, 64, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)                \
+    X(64, 128, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)                \
+    X(64, 64, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)
 
 // Grid of a launch of `items` work items under plan p: one workgroup per item,
 // or (persistent plans) at most occ workgroups per compute unit, a multiple of 8.

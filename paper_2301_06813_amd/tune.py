@@ -169,7 +169,10 @@ def bwd_pairs(wl_ids):
     return pairs
 
 
-def tune_bwd(args, torch, sbp, linear, workloads, stream):
+def tune_bwd(args, torch, sbp, linear, workloads, stream, single_best=None):
+    """Grouped launch of each backward pair against its two products run
+    separately: the sum of their tuned times (single_best, from the same run),
+    else a measured pair of launches of the compiled-in plans."""
     pairs = bwd_pairs([int(c) for c in args.workloads.split(",")])
     log("%d distinct backward pairs" % len(pairs))
     rows = []
@@ -198,12 +201,16 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream):
             finally:
                 sbp.sbp_set_plan_override(0, 0, 1)
 
-        sbp.sbp_set_bwd_override(1, 1)
-        try:
-            sep = time_plan(torch, sbp, fn, (0, 0, 1, 0, 0), args.reps, stream, keep=True)
-        finally:
-            sbp.sbp_set_bwd_override(0, 1)
-        best = None
+        if single_best and kd in single_best and kw in single_best:
+            sep = single_best[kd] + single_best[kw]
+        else:
+            sbp.sbp_set_bwd_override(1, 1)
+            try:
+                sep = time_plan(torch, sbp, fn, (0, 0, 1, 0, 0), 3 * args.reps, stream,
+                                keep=True)
+            finally:
+                sbp.sbp_set_bwd_override(0, 1)
+        timings = []
         kbd, kbw = max(1, (kd[4] + 63) // 64), max(1, (kw[4] + 63) // 64)
         for (bm, bn), code in GROUP_INSTANCES:
             for sd in (1, 2, 4, 8, 16):
@@ -213,11 +220,20 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream):
                     if sw > 1 and kbw // sw < 2:
                         continue
                     try:
-                        us = timed((bm, bn, sd, code, 0), 2, sw)
+                        timings.append((timed((bm, bn, sd, code, 0), 2, sw),
+                                        (bm, bn, code, sd, sw)))
                     except sbp.SbpError:
                         continue
-                    if best is None or us < best[0]:
-                        best = (us, (bm, bn, code, sd, sw))
+
+        def retime(pl):
+            bm, bn, code, sd, sw = pl
+            sbp.sbp_set_plan_override(bm, bn, sd, code, 0)
+            sbp.sbp_set_bwd_override(2, sw)
+            try:
+                return time_plan(torch, sbp, fn, None, 3 * args.reps, stream, keep=True)
+            finally:
+                sbp.sbp_set_plan_override(0, 0, 1)
+        best = pick(timings, retime) if timings else None
         log("%s %s d %s w %s: separate %6.1f us, best grouped %6.1f us %s"
             % (lin.sig, lin.name, kd[2:5], kw[2:5], sep, best[0] if best else -1,
                best[1] if best else None))
@@ -236,12 +252,26 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream):
     log("wrote %s" % args.out)
 
 
+def pick(timings, retime, top=5, rounds=3):
+    """Best plan of [(us, plan)]: the `top` fastest of the sweep are timed again
+    `rounds` times at higher repetition and ranked by their median."""
+    cands = [p for _, p in sorted(timings)[:top]]
+    med = []
+    for p in cands:
+        ts = sorted(retime(p) for _ in range(rounds))
+        med.append((ts[len(ts) // 2], p))
+    return min(med)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--out", default=None)
     ap.add_argument("--workloads", default="2,3,4,5")
     ap.add_argument("--reps", type=int, default=10)
-    ap.add_argument("--bwd", action="store_true", help="tune grouped backward pairs")
+    ap.add_argument("--bwd", action="store_true", help="tune grouped backward pairs only")
+    ap.add_argument("--all", action="store_true",
+                    help="tune single products, then backward pairs against their sums")
+    ap.add_argument("--out-bwd", default=os.path.join(HERE, "csrc", "tuned_bwd_plans.inc"))
     args = ap.parse_args()
     if args.out is None:
         args.out = os.path.join(HERE, "csrc",
@@ -257,6 +287,7 @@ def main():
         return
     cases = product_cases([int(c) for c in args.workloads.split(",")])
     log("%d distinct local products" % len(cases))
+    single_best = {}
     rows = []
     t_start = time.time()
     for key, (wl, lin, op, r) in sorted(cases.items()):
@@ -276,16 +307,15 @@ def main():
             linear.run(op, lin.sig, wl.p, r, X, W, dY, out, stream.cuda_stream)
 
         cands = valid_candidates(sbp, key, None)
-        best = None
+        timings = []
         for plan in cands:
             try:
-                us = time_plan(torch, sbp, fn, plan, args.reps, stream)
+                timings.append((time_plan(torch, sbp, fn, plan, args.reps, stream), plan))
             except sbp.SbpError as e:
                 log("  plan %s failed: %s" % (plan, e))
-                continue
-            if best is None or us < best[0]:
-                best = (us, plan)
-        auto = time_plan(torch, sbp, fn, (0, 0, 1, 0, 0), args.reps, stream)
+        best = pick(timings, lambda p: time_plan(torch, sbp, fn, p, 3 * args.reps, stream))
+        auto = time_plan(torch, sbp, fn, (0, 0, 1, 0, 0), 3 * args.reps, stream)
+        single_best[key] = best[0]
         bm, bn, splits, code, occ = best[1]
         log("%s %-10s m %5d n %5d k %5d f32 %d dma %d: best %6.1f us %s (model plan %6.1f us), "
             "%d candidates" % (lin.sig, op, m, n, k, f32, dma, best[0], best[1], auto, len(cands)))
@@ -303,6 +333,9 @@ def main():
             f.write("{%d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d},  // %.1f (%.1f)\n"
                     % (orient, f32, m, n, k, dma, bm, bn, code, splits, occ, us, auto))
     log("wrote %s" % args.out)
+    if args.all:
+        args.out = args.out_bwd
+        tune_bwd(args, torch, sbp, linear, workloads, stream, single_best)
 
 
 if __name__ == "__main__":

@@ -18,7 +18,8 @@ KERNELS = (1, 2)   # pipelined direct-to-LDS, generic
 EXTRA_TILE_KERNELS = [((128, 128), 4), ((128, 128), 5), ((256, 128), 5), ((128, 256), 5),
                       ((256, 256), 6), ((128, 128), 6), ((128, 128), 7), ((256, 128), 7),
                       ((128, 256), 7), ((256, 256), 8), ((256, 128), 9), ((128, 256), 9),
-                      ((128, 128), 9), ((128, 128), 10)]
+                      ((128, 128), 9), ((128, 128), 10), ((128, 64), 4), ((64, 128), 4),
+                      ((64, 64), 4)]
 
 
 def say(*a):

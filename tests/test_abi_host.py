@@ -258,7 +258,7 @@ def test_strerror_and_plan(L):
     assert sbp.sbp_plan(0, 128, 128, 1024, BF, BF) == (256, 256, 2, sbp.KERNEL_PIPELINED)
     with pytest.raises(sbp.SbpError):
         sbp.sbp_set_plan_override(512, 256, 1)
-    # the two-stage instance exists for 128x128 only
+    # the two-stage instances exist for tiles up to 128x128 only
     with pytest.raises(sbp.SbpError):
         sbp.sbp_set_plan_override(256, 128, 1, sbp.KERNEL_PIPELINED_2STAGE)
     with pytest.raises(sbp.SbpError):
