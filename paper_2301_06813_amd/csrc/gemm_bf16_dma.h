@@ -182,6 +182,18 @@ struct DmaStage {
     static constexpr int BYTES = A_BYTES + B_BYTES;
 };
 
+// Workgroups per compute unit an instance is compiled for: as many as its
+// LDS pipeline allows (160 KB per CU), at most four waves per SIMD, and one
+// for eight-wave groups. The compiler then budgets registers so that many
+// fit (e.g. two 128 x 128 two-stage workgroups, not one).
+template <int BM, int BN, int BKD, int NS, int NWAVES, int KG>
+struct Occupancy {
+    static constexpr int BY_LDS = 163840 / (NS * DmaStage<BM, BN, BKD, NS>::BYTES);
+    static constexpr int BY_WAVES = 16 / NWAVES;
+    static constexpr int V0 = BY_LDS < BY_WAVES ? BY_LDS : BY_WAVES;
+    static constexpr int VALUE = (KG > 1 || V0 < 1) ? 1 : V0;
+};
+
 // Output rows of the staged epilogue are padded by 8 floats where the LDS
 // allows: the two half-waves of a 32 x 32 MFMA block write rows 4 apart, and
 // 4 (BN + 8) = 32 mod 64 floats puts them on disjoint LDS banks (unpadded, the
@@ -540,7 +552,9 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
 // the next item's operand loads are in flight.
 template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool A_KMAJ,
           bool B_KMAJ, bool OUT_F32>
-__global__ __launch_bounds__(64 * WGM * WGN * KG, 1) void gemm_bf16_dma_kernel(GemmArgs g) {
+__global__ __launch_bounds__(64 * WGM * WGN * KG,
+                             (Occupancy<BM, BN, BKD, NS, WGM * WGN * KG, KG>::VALUE))
+void gemm_bf16_dma_kernel(GemmArgs g) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
     const int total = g.tiles_m * g.tiles_n * g.splits;
     for (int v = blockIdx.x; v < total; v += gridDim.x) {
@@ -560,9 +574,9 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG, 1) void gemm_bf16_dma_kernel(G
 // of the other fill the machine behind them.
 template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool OUTD_F32,
           bool OUTW_F32>
-__global__ __launch_bounds__(64 * WGM * WGN * KG, 1) void gemm_bf16_dma_bwd_kernel(GemmArgs gd,
-                                                                                  GemmArgs gw,
-                                                                                  int data_first) {
+__global__ __launch_bounds__(64 * WGM * WGN * KG,
+                             (Occupancy<BM, BN, BKD, NS, WGM * WGN * KG, KG>::VALUE))
+void gemm_bf16_dma_bwd_kernel(GemmArgs gd, GemmArgs gw, int data_first) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
     const int wd = gd.tiles_m * gd.tiles_n * gd.splits;
     const int ww = gw.tiles_m * gw.tiles_n * gw.splits;
