@@ -202,6 +202,86 @@ def cpu_baseline(wl, seconds):
                       % (nrows, fl / 1e9, t)}
 
 
+def report_workload(cid, ranks, reps):
+    """Per-call throughput of workload cid (2: Transformer FFN shard, 3: attention
+    projections, 4: VGG head) on the given ranks: each call (the forward product,
+    or both backward products in one sbp_linear_bwd call) is replayed from a HIP
+    graph over three rotating sets of its global inputs (more than the 256 MB
+    Infinity Cache for the larger workloads). Returns one dict for the JSON line."""
+    import torch
+    from paper_2301_06813_amd import linear, sbp, workloads
+    wl = {2: workloads.ffn_shard, 3: workloads.attention_dp, 4: workloads.vgg_head}[cid]()
+    stream = torch.cuda.Stream()
+    rows = []
+    for lin in wl.linears:
+        sets = []
+        for _ in range(3):
+            X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
+            sets.append((X, W, dY))
+        for r in ranks:
+            L = linear.layouts(lin.sig, wl.p, r)
+            outs = [{op: linear.alloc_out(op, lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype,
+                                          "cuda") for op in OPS} for _ in sets]
+            for kind in ("fwd", "bwd"):
+                it = [0]
+
+                def call():
+                    i = it[0] % len(sets)
+                    it[0] += 1
+                    X, W, dY = sets[i]
+                    o = outs[i]
+                    if kind == "fwd":
+                        linear.run("fwd", lin.sig, wl.p, r, X, W, dY, o["fwd"], stream.cuda_stream)
+                    else:
+                        linear.run_bwd(lin.sig, wl.p, r, X, W, dY, o["bwd_data"],
+                                       o["bwd_weight"], stream.cuda_stream)
+                with torch.cuda.stream(stream):
+                    call()
+                    torch.cuda.synchronize()
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=stream):
+                        for _ in range(reps):
+                            call()
+                g.replay()
+                torch.cuda.synchronize()
+                t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                t0.record()
+                for _ in range(3):
+                    g.replay()
+                t1.record()
+                torch.cuda.synchronize()
+                us = t0.elapsed_time(t1) * 1e3 / (3 * reps)
+                ops = ("fwd",) if kind == "fwd" else ("bwd_data", "bwd_weight")
+                prods, fl, by = [], 0.0, 0.0
+                for op in ops:
+                    m, n = outs[0][op].shape
+                    k = {"fwd": sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols,
+                         "bwd_data": sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols,
+                         "bwd_weight": sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows}[op]
+                    ob = 4 if outs[0][op].dtype == torch.float32 else 2
+                    prods.append("%s %dx%dx%d%s" % (op, m, n, k, " fp32" if ob == 4 else ""))
+                    fl += 2.0 * m * n * k
+                    by += 2.0 * (m * k + k * n) + ob * m * n
+                rows.append({"linear": lin.name, "sig": lin.sig, "rank": r, "call": kind,
+                             "products": prods, "us": us, "tflops": fl / us / 1e6,
+                             "pct_of_bf16_peak": 100.0 * fl / us / 1e6 / BF16_PEAK_TFLOPS,
+                             "algorithmic_gbs": by / us / 1e3,
+                             "roofline_min_us": max(fl / BF16_PEAK_TFLOPS / 1e6,
+                                                    by / HBM_PEAK_GBS / 1e3)})
+                log("%-4s %-4s r%d %-3s %7.1f us %6.0f TFLOP/s %s" % (
+                    lin.name, lin.sig, r, kind, us, fl / us / 1e6, ", ".join(prods)))
+        del sets
+        torch.cuda.empty_cache()
+    tot_us = sum(x["us"] for x in rows if x["rank"] == ranks[0])
+    tot_fl = sum(x["tflops"] * x["us"] * 1e6 for x in rows if x["rank"] == ranks[0])
+    return {"metric": "local-shard GEMM TFLOP/s (fwd+bwd) per SBP signature; % of bf16 MFMA peak",
+            "value": tot_fl / tot_us / 1e6, "unit": "TFLOP/s", "n_gpus": 1,
+            "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": wl.name, "p": wl.p, "ranks": list(ranks),
+                       "mode": "per-call hip_graph replay"},
+            "calls": rows}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -213,6 +293,9 @@ def main():
     ap.add_argument("--dump", default=None, help="write per-launch shapes and durations (JSON)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (scale for HBM counters)")
+    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 4, 5),
+                    help="5 (default): the 24-layer step; 2-4: per-call report of that "
+                         "workload's local products")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build measures rank r's local products on a "
@@ -233,6 +316,10 @@ def main():
                           "copies": 5}))
         return
     sbp.lib()
+    if args.workload != 5:
+        ranks = (0, 1) if args.workload == 4 else (0,)
+        print(json.dumps(report_workload(args.workload, ranks, reps=10)))
+        return
     wl = workloads.transformer_step()
     log("building step: %d linears, p=%d, rank 0" % (len(wl.linears), wl.p))
     step = Step(wl, 0)
