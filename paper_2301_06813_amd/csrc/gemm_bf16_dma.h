@@ -15,9 +15,8 @@
 //     allows) are in flight: the loads of step t + NS - 1 are issued while
 //     step t computes, hiding HBM latency behind NS - 1 steps of MFMA work.
 //     Chunks outside the operand get an out-of-range offset and read as 0.
-//   * The reduction step BKD is a template parameter (64 for every instance;
-//     32 is supported for deeper pipelines but its row swizzle is not yet free
-//     of bank conflicts on gfx950).
+//   * The reduction step BKD is a template parameter: 64, or 32 for deeper
+//     pipelines (more stages in the same LDS).
 //   * k-major operand tiles keep their storage order in LDS: one row of BKD
 //     reduction values per output row, 16-byte chunks XOR-swizzled by row;
 //     fragments are read with ds_read_b128.
@@ -75,7 +74,8 @@ __device__ __forceinline__ void dma16(i32x4 r, char *lds, int voff) {
 // LDS: BMN rows x RB bytes (RB = 2 BK: 64 reduction values in 8 chunks of
 // 16 B, or 32 in 4). Chunk c of row r sits at r*RB + 16*(c ^ f(r)); f makes
 // the 16-byte fragment reads of 8 consecutive rows (32 banks) and of 16
-// (64 banks) hit distinct banks.
+// (64 banks) hit distinct banks: with 64-byte rows, 16 aligned rows cover
+// the 16 bank quads once as 4 (r % 4) + (c ^ (r / 4 % 4)).
 template <int BMN, int NW, int BK_>
 struct KTileDma {
     static constexpr int RB = BK_ * 2;            // bytes per row
@@ -86,7 +86,7 @@ struct KTileDma {
     static_assert(SEGS % NW == 0, "tile too small for the wave count");
 
     __device__ __forceinline__ static int swz(int row) {
-        return CPR == 8 ? ((row & 7) ^ ((row >> 3) & 7)) : (((row >> 1) ^ (row >> 3)) & 3);
+        return CPR == 8 ? ((row & 7) ^ ((row >> 3) & 7)) : ((row >> 2) & 3);
     }
     __device__ __forceinline__ static int off(int row, int c) {
         return row * RB + ((c ^ swz(row)) << 4);
@@ -173,7 +173,20 @@ using DmaTileOf =
 
 template <int N>
 __device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N <= 63, "vmcnt holds 6 bits");
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait until at most `ahead` of this thread's stages (LOADS loads each) are
+// still in flight; `ahead` <= K.
+template <int K, int LOADS>
+__device__ __forceinline__ void wait_stages(int ahead) {
+    if constexpr (K <= 0) {
+        wait_vm<0>();
+    } else {
+        if (ahead >= K) wait_vm<K * LOADS>();
+        else wait_stages<K - 1, LOADS>(ahead);
+    }
 }
 
 template <int BM, int BN, int BKD, int NS>
@@ -345,10 +358,7 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
 
     for (int it = 0; it < nkb; ++it) {
         // wait for this thread's loads of step `it`; later steps may stay in flight
-        const int ahead = min(NS - 2, nkb - 1 - it);
-        if (ahead >= 2) wait_vm<2 * LOADS>();
-        else if (ahead == 1) wait_vm<LOADS>();
-        else wait_vm<0>();
+        wait_stages<NS - 2, LOADS>(min(NS - 2, nkb - 1 - it));
         __syncthreads();
         if (it + NS - 1 < nkb) issue(it + NS - 1, (it + NS - 1) % NS);
 
