@@ -67,6 +67,9 @@ int kernel_code(const Plan &p);   // kernel code of a plan, as sbp_plan reports 
 // the split reduction into g.C.
 hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, hipStream_t s);
 hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipStream_t s);
+// Both split reductions of a grouped backward launch, in one launch.
+hipError_t launch_split_reduce_pair(const Gemm &gd, int sd, const float *wsd, const Gemm &gw,
+                                    int sw, const float *wsw, hipStream_t s);
 
 // Backward-data (gd) and backward-weight (gw) products of one linear. If
 // plan_bf16_bwd returns true, *pd and *pw share a pipelined tile and

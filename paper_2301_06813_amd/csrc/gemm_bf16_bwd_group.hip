@@ -49,6 +49,8 @@ hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
     else if (ow) e = launch_group_tile<false, true>(pd, d, w, data_first, grid, s);
     else e = launch_group_tile<false, false>(pd, d, w, data_first, grid, s);
     if (e != hipSuccess) return e;
+    if (pd.splits > 1 && pw.splits > 1)
+        return launch_split_reduce_pair(gd, pd.splits, ws, gw, pw.splits, ws_w, s);
     if (pd.splits > 1 && (e = launch_split_reduce(gd, pd.splits, ws, s)) != hipSuccess) return e;
     if (pw.splits > 1 && (e = launch_split_reduce(gw, pw.splits, ws_w, s)) != hipSuccess) return e;
     return hipSuccess;

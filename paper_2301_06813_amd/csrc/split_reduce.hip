@@ -15,11 +15,12 @@ namespace sbpk {
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
+// Sums the S slices of one product's 4-column group gidx (row gidx /
+// groups_per_row) in split order and stores it; out-of-range ids do nothing.
 template <bool OUT_F32>
-__global__ __launch_bounds__(256) void split_reduce_kernel(const float *ws, int m, int n, int S,
-                                                           void *C, int64_t ldc) {
+__device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int S, void *C,
+                                             int64_t ldc, int64_t gidx) {
     const int groups_per_row = (n + 3) / 4;
-    const int64_t gidx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (gidx >= (int64_t)m * groups_per_row) return;
     const int row = (int)(gidx / groups_per_row);
     const int col = (int)(gidx % groups_per_row) * 4;
@@ -52,6 +53,33 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float *ws, int 
     }
 }
 
+template <bool OUT_F32>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float *ws, int m, int n, int S,
+                                                           void *C, int64_t ldc) {
+    reduce_group<OUT_F32>(ws, m, n, S, C, ldc, (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+}
+
+// The split reductions of the two backward products of one linear in one
+// launch: blocks [0, blocks_d) reduce the backward-data product, the rest the
+// backward-weight product.
+struct ReduceJob {
+    const float *ws;
+    int m, n, S;
+    void *C;
+    int64_t ldc;
+};
+
+template <bool OD, bool OW>
+__global__ __launch_bounds__(256) void split_reduce_pair_kernel(ReduceJob d, ReduceJob w,
+                                                                int blocks_d) {
+    const int b = blockIdx.x;
+    if (b < blocks_d)
+        reduce_group<OD>(d.ws, d.m, d.n, d.S, d.C, d.ldc, (int64_t)b * blockDim.x + threadIdx.x);
+    else
+        reduce_group<OW>(w.ws, w.m, w.n, w.S, w.C, w.ldc,
+                         (int64_t)(b - blocks_d) * blockDim.x + threadIdx.x);
+}
+
 }  // namespace sbpk
 
 namespace sbpi {
@@ -65,6 +93,29 @@ hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipSt
                              g.ldc);
     return launch_kernel(sbpk::split_reduce_kernel<false>, "split_reduce_kernel<false>",
                          dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C, g.ldc);
+}
+
+static unsigned reduce_blocks(const Gemm &g) {
+    const int64_t groups = g.m * ((g.n + 3) / 4);
+    return (unsigned)((groups + 255) / 256);
+}
+
+hipError_t launch_split_reduce_pair(const Gemm &gd, int sd, const float *wsd, const Gemm &gw,
+                                    int sw, const float *wsw, hipStream_t s) {
+    const sbpk::ReduceJob d{wsd, (int)gd.m, (int)gd.n, sd, gd.C, gd.ldc};
+    const sbpk::ReduceJob w{wsw, (int)gw.m, (int)gw.n, sw, gw.C, gw.ldc};
+    const unsigned bd = reduce_blocks(gd), bw = reduce_blocks(gw);
+    const bool od = gd.out_dtype == DT_F32, ow = gw.out_dtype == DT_F32;
+#define SBP_PAIR(OD_, OW_, NAME)                                                             \
+    if (od == OD_ && ow == OW_)                                                              \
+        return launch_kernel(sbpk::split_reduce_pair_kernel<OD_, OW_>, NAME, dim3(bd + bw),  \
+                             dim3(256), s, d, w, (int)bd);
+    SBP_PAIR(true, true, "split_reduce_pair_kernel<true, true>")
+    SBP_PAIR(true, false, "split_reduce_pair_kernel<true, false>")
+    SBP_PAIR(false, true, "split_reduce_pair_kernel<false, true>")
+    SBP_PAIR(false, false, "split_reduce_pair_kernel<false, false>")
+#undef SBP_PAIR
+    return hipErrorInvalidValue;
 }
 
 }  // namespace sbpi
