@@ -224,15 +224,18 @@ int sbp_profile_end(float *us, char *names, int name_len);
  *   4     pipelined with two stages (128x128, 128x64, 64x128, 64x64: two or
  *         more workgroups per compute unit);
  *   5     pipelined, eight waves in two reduction groups, output staged in
- *         LDS (256x128, 128x256, 128x128);
+ *         LDS (256x128, 128x256, 128x128, 128x64, 64x128, 64x64);
  *   6     pipelined, row-quad epilogue: MFMA operands swapped so each lane
  *         stores 4 consecutive outputs of a row from registers (256x256, and
  *         128x128 with two stages);
- *   7     as 5 with the row-quad epilogue (256x128, 128x256, 128x128);
+ *   7     as 5 with the row-quad epilogue (256x128, 128x256, 128x128, 128x64,
+ *         64x128, 64x64);
  *   8     pipelined with 32-wide reduction stages, five in LDS (256x256);
  *   9     as 5 with 32-wide reduction stages, six (256x128, 128x256) or
  *         eight (128x128) in LDS;
- *   10    as 5 with two stages, two workgroups per compute unit (128x128).
+ *   10    as 5 with two stages, two workgroups per compute unit (128x128);
+ *   11    pipelined with deep prefetch for operand streams that HBM latency
+ *         bounds: six stages (128x64, 64x128) or eight (64x64) in LDS.
  * wgs_per_cu > 0 makes the launch persistent: at most wgs_per_cu workgroups
  * per compute unit, each taking every G-th work item (0 = one workgroup per
  * item; the grouped backward launch always runs one per item). A call whose

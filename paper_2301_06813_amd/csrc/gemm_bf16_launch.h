@@ -52,7 +52,16 @@ namespace sbpi {
     X(128, 128, 64, 2, 2, 2, 2, sbpk::EPI_STAGED)               \
     X(128, 64, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)                \
     X(64, 128, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)                \
-    X(64, 64, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)
+    X(64, 64, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)                 \
+    X(128, 64, 64, 6, 2, 2, 1, sbpk::EPI_DIRECT)                \
+    X(64, 128, 64, 6, 2, 2, 1, sbpk::EPI_DIRECT)                \
+    X(64, 64, 64, 8, 2, 2, 1, sbpk::EPI_DIRECT)                 \
+    X(128, 64, 64, SBP_NS_128x64, 2, 2, 2, sbpk::EPI_STAGED)       \
+    X(64, 128, 64, SBP_NS_128x64, 2, 2, 2, sbpk::EPI_STAGED)       \
+    X(64, 64, 64, SBP_NS_64x64, 2, 2, 2, sbpk::EPI_STAGED)         \
+    X(128, 64, 64, SBP_NS_128x64, 2, 2, 2, sbpk::EPI_ROWQ)         \
+    X(64, 128, 64, SBP_NS_128x64, 2, 2, 2, sbpk::EPI_ROWQ)         \
+    X(64, 64, 64, SBP_NS_64x64, 2, 2, 2, sbpk::EPI_ROWQ)
 
 // Grid of a launch of `items` work items under plan p: one workgroup per item,
 // or (persistent plans) at most occ workgroups per compute unit, a multiple of 8.

@@ -19,7 +19,9 @@ EXTRA_TILE_KERNELS = [((128, 128), 4), ((128, 128), 5), ((256, 128), 5), ((128, 
                       ((256, 256), 6), ((128, 128), 6), ((128, 128), 7), ((256, 128), 7),
                       ((128, 256), 7), ((256, 256), 8), ((256, 128), 9), ((128, 256), 9),
                       ((128, 128), 9), ((128, 128), 10), ((128, 64), 4), ((64, 128), 4),
-                      ((64, 64), 4)]
+                      ((64, 64), 4), ((128, 64), 11), ((64, 128), 11), ((64, 64), 11),
+                      ((128, 64), 5), ((64, 128), 5), ((64, 64), 5), ((128, 64), 7),
+                      ((64, 128), 7), ((64, 64), 7)]
 
 
 def say(*a):
