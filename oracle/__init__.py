@@ -8,9 +8,11 @@ module only builds it, loads it and marshals numpy arrays.
 
 What it computes follows AutoDDL Sec. 4.2 (the SBP matrix multiplication and
 its local matmul) and Sec. 4.3 (a broadcast weight receives partial-sum
-gradients); see the header of ``oracle.c``.
+gradients), on a 1-D mesh of p devices and on d-dimensional meshes (one state
+per mesh axis, the ``nd_*`` functions); see the header of ``oracle.c``.
 
-Parity status: pinned by ``tests/test_oracle_pins.py`` (reassembly
+Parity status: pinned by ``tests/test_oracle_pins.py`` and, for meshes,
+``tests/test_oracle_nd_pins.py`` (reassembly
 invariant against brute-force global products, exact integer inputs, closed
 forms, the p = 1 textbook case, Listing 1 shard shapes, bf16 rounding against
 a library conversion). ``orc_round_bf16`` does not model bf16 subnormals
@@ -80,6 +82,22 @@ class Oracle:
         lib.orc_linear_samples.restype = ctypes.c_int
         lib.orc_round_bf16.argtypes = [vp, vp, i64]
         lib.orc_round_bf16.restype = None
+        ci = ctypes.c_int
+        lib.orc_mesh_coord.argtypes = [ci, p32, p32, i64, i64, p32]
+        lib.orc_mesh_coord.restype = ci
+        lib.orc_nd_tags.argtypes = [ci, p32, p32, p32, p32, p32, p32]
+        lib.orc_nd_tags.restype = ci
+        lib.orc_nd_share.argtypes = [ci, p32, p32, p32, p32, i64, i64, p64]
+        lib.orc_nd_share.restype = ci
+        lib.orc_nd_out_shape.argtypes = [ci, i64, i64, i64, ci, p32, p32, p32, p32, p32, p32,
+                                         p64, p64, p32, p32]
+        lib.orc_nd_out_shape.restype = ci
+        lib.orc_nd_linear_block.argtypes = [ci, ci, i64, i64, i64, ci, p32, p32, p32, p32, p32,
+                                            p32, vp, vp, vp, i64, i64, i64, i64, vp]
+        lib.orc_nd_linear_block.restype = ci
+        lib.orc_nd_linear_samples.argtypes = [ci, ci, i64, i64, i64, ci, p32, p32, p32, p32, p32,
+                                              p32, vp, vp, vp, i64, vp, vp, vp]
+        lib.orc_nd_linear_samples.restype = ci
         self.lib = lib
 
     def split(self, D: int, p: int, r: int) -> tuple[int, int]:
@@ -143,6 +161,90 @@ class Oracle:
             raise ValueError("bad oracle arguments")
         return out
 
+    # --------------------------------------------------------- meshes
+    def mesh_coord(self, nodes, gpus=None, node=0, gpu=0) -> list[int]:
+        """Mesh coordinate of device (node, gpu); gpus None means one GPU per node."""
+        d = len(nodes)
+        gpus = [1] * d if gpus is None else list(gpus)
+        c = (ctypes.c_int32 * d)()
+        if self.lib.orc_mesh_coord(d, _i32(nodes), _i32(gpus), node, gpu, c) != 0:
+            raise ValueError("bad mesh or device")
+        return list(c)
+
+    def nd_tags(self, xstates, wstates) -> list[list[tuple[int, int]]]:
+        """Per tensor (X, W, Y, dY, dX, dW), the per-mesh-axis (kind, axis)
+        states for X and W in the given per-axis (kind, axis) states."""
+        d = len(xstates)
+        kinds = (ctypes.c_int32 * (6 * d))()
+        axes = (ctypes.c_int32 * (6 * d))()
+        xk, xa = zip(*xstates)
+        wk, wa = zip(*wstates)
+        if self.lib.orc_nd_tags(d, _i32(xk), _i32(xa), _i32(wk), _i32(wa), kinds, axes) != 0:
+            raise ValueError("no nd signature for these states")
+        return [[(kinds[t * d + a], axes[t * d + a]) for a in range(d)] for t in range(6)]
+
+    def nd_share(self, states, mesh, coord, rows, cols) -> tuple[int, int, int, int]:
+        """(row offset, col offset, rows, cols) of the device's share."""
+        d = len(mesh)
+        k, a = zip(*states)
+        out = (ctypes.c_int64 * 4)()
+        if self.lib.orc_nd_share(d, _i32(k), _i32(a), _i32(mesh), _i32(coord), rows, cols,
+                                 out) != 0:
+            raise ValueError("bad nd layout")
+        return tuple(out)
+
+    def _nd_args(self, xstates, wstates, mesh, coord):
+        xk, xa = zip(*xstates)
+        wk, wa = zip(*wstates)
+        return (len(mesh), _i32(mesh), _i32(coord), _i32(xk), _i32(xa), _i32(wk), _i32(wa))
+
+    def nd_out_shape(self, op, M, K, N, xstates, wstates, mesh, coord):
+        """(rows, cols, per-axis (kind, axis) states) of the device's output of op."""
+        d = len(mesh)
+        rows, cols = ctypes.c_int64(), ctypes.c_int64()
+        kind, axis = (ctypes.c_int32 * d)(), (ctypes.c_int32 * d)()
+        rc = self.lib.orc_nd_out_shape(op, M, K, N, *self._nd_args(xstates, wstates, mesh, coord),
+                                       ctypes.byref(rows), ctypes.byref(cols), kind, axis)
+        if rc != 0:
+            raise ValueError("bad nd oracle arguments")
+        return rows.value, cols.value, list(zip(kind, axis))
+
+    def nd_linear(self, op, X, W, dY, xstates, wstates, mesh, coord, rows=None, cols=None,
+                  M=None, K=None, N=None) -> np.ndarray:
+        """The device's output of op (fp64) for X and W in per-axis states
+        xstates and wstates ((kind, axis) per mesh axis) on mesh `mesh`, at
+        mesh coordinate `coord`. Inputs as for linear()."""
+        (X, W, dY), enc = _prep(X, W, dY)
+        M, K, N = _dims(X, W, dY, M, K, N)
+        orow, ocol, _ = self.nd_out_shape(op, M, K, N, xstates, wstates, mesh, coord)
+        rows = range(orow) if rows is None else rows
+        cols = range(ocol) if cols is None else cols
+        out = np.empty((len(rows), len(cols)), dtype=np.float64)
+        rc = self.lib.orc_nd_linear_block(op, enc, M, K, N,
+                                          *self._nd_args(xstates, wstates, mesh, coord),
+                                          _ptr(X), _ptr(W), _ptr(dY), rows.start,
+                                          rows.start + len(rows), cols.start,
+                                          cols.start + len(cols), out.ctypes.data)
+        if rc != 0:
+            raise ValueError("bad nd oracle arguments")
+        return out
+
+    def nd_linear_samples(self, op, X, W, dY, xstates, wstates, mesh, coord, ii, jj,
+                          M=None, K=None, N=None) -> np.ndarray:
+        """Single elements (ii[s], jj[s]) of the device's output of op, as fp64."""
+        (X, W, dY), enc = _prep(X, W, dY)
+        M, K, N = _dims(X, W, dY, M, K, N)
+        ii = np.ascontiguousarray(ii, dtype=np.int64)
+        jj = np.ascontiguousarray(jj, dtype=np.int64)
+        out = np.empty(ii.shape[0], dtype=np.float64)
+        rc = self.lib.orc_nd_linear_samples(op, enc, M, K, N,
+                                            *self._nd_args(xstates, wstates, mesh, coord),
+                                            _ptr(X), _ptr(W), _ptr(dY), ii.shape[0],
+                                            ii.ctypes.data, jj.ctypes.data, out.ctypes.data)
+        if rc != 0:
+            raise ValueError("bad nd oracle arguments")
+        return out
+
     def round_bf16(self, x) -> np.ndarray:
         """Round fp64 values to bf16 (nearest, ties to even); returns uint16 bit patterns."""
         x = np.ascontiguousarray(x, dtype=np.float64)
@@ -189,6 +291,11 @@ def _ptr(a):
     return None if a is None else a.ctypes.data
 
 
+def _i32(vals):
+    vals = list(vals)
+    return (ctypes.c_int32 * max(1, len(vals)))(*vals)
+
+
 _default = None
 
 
@@ -224,6 +331,33 @@ def linear_samples(sig, op, X, W, dY, p, r, ii, jj, M=None, K=None, N=None):
 
 def round_bf16(x) -> np.ndarray:
     return default().round_bf16(x)
+
+
+def mesh_coord(nodes, gpus=None, node=0, gpu=0):
+    return default().mesh_coord(nodes, gpus, node, gpu)
+
+
+def nd_tags(xstates, wstates):
+    return default().nd_tags(xstates, wstates)
+
+
+def nd_share(states, mesh, coord, rows, cols):
+    return default().nd_share(states, mesh, coord, rows, cols)
+
+
+def nd_out_shape(op, M, K, N, xstates, wstates, mesh, coord):
+    return default().nd_out_shape(op, M, K, N, xstates, wstates, mesh, coord)
+
+
+def nd_linear(op, X, W, dY, xstates, wstates, mesh, coord, rows=None, cols=None,
+              M=None, K=None, N=None):
+    return default().nd_linear(op, X, W, dY, xstates, wstates, mesh, coord, rows, cols, M, K, N)
+
+
+def nd_linear_samples(op, X, W, dY, xstates, wstates, mesh, coord, ii, jj, M=None, K=None,
+                      N=None):
+    return default().nd_linear_samples(op, X, W, dY, xstates, wstates, mesh, coord, ii, jj,
+                                       M, K, N)
 
 
 def bf16_to_f64(bits) -> np.ndarray:

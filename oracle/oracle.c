@@ -34,9 +34,14 @@
  * fp32 values are exact in fp64, so the result is the exact product rounded
  * only by the fp64 running sum.
  *
+ * The nd-SBP section below extends this to device meshes (one state per
+ * mesh axis).
+ *
  * Parity status: pinned (reassembly invariant against brute-force global
  * products, exact integer cases, closed forms, p = 1 textbook case, bf16
- * rounding against a library conversion); see tests/test_oracle_*.py.
+ * rounding against a library conversion; for meshes, Listing 1's blocks,
+ * the heterogeneous GPU mapping example and the mesh reassembly invariant);
+ * see tests/test_oracle_*.py.
  */
 #include <stdint.h>
 #include <string.h>
@@ -124,15 +129,9 @@ static double decode(const void *base, int enc, int64_t idx)
  */
 typedef struct { orc_share x, w, dy; int64_t out_rows, out_cols; } orc_plan;
 
-static int make_plan(int sig, int op, int64_t M, int64_t K, int64_t N,
-                     int64_t p, int64_t r, orc_plan *pl)
+/* Output shape of op from the operand shares already in pl. */
+static void set_out_shape(int op, orc_plan *pl)
 {
-    int32_t kd[6], ax[6];
-    if (orc_tags(sig, kd, ax) != 0) return -1;
-    if (op < 0 || op > 2 || p < 1 || r < 0 || r >= p) return -1;
-    pl->x = share_of(kd[0], ax[0], M, K, p, r);
-    pl->w = share_of(kd[1], ax[1], K, N, p, r);
-    pl->dy = share_of(kd[3], ax[3], M, N, p, r);
     if (op == ORC_FWD) {          /* Y_r = X_r W_r            : (x.nr) x (w.nc) */
         pl->out_rows = pl->x.nr;
         pl->out_cols = pl->w.nc;
@@ -143,6 +142,18 @@ static int make_plan(int sig, int op, int64_t M, int64_t K, int64_t N,
         pl->out_rows = pl->x.nc;
         pl->out_cols = pl->dy.nc;
     }
+}
+
+static int make_plan(int sig, int op, int64_t M, int64_t K, int64_t N,
+                     int64_t p, int64_t r, orc_plan *pl)
+{
+    int32_t kd[6], ax[6];
+    if (orc_tags(sig, kd, ax) != 0) return -1;
+    if (op < 0 || op > 2 || p < 1 || r < 0 || r >= p) return -1;
+    pl->x = share_of(kd[0], ax[0], M, K, p, r);
+    pl->w = share_of(kd[1], ax[1], K, N, p, r);
+    pl->dy = share_of(kd[3], ax[3], M, N, p, r);
+    set_out_shape(op, pl);
     return 0;
 }
 
@@ -196,6 +207,47 @@ static double element(const orc_plan *pl, int op, int enc, int64_t K, int64_t N,
  * argument (unknown signature/op, rank out of range, block outside the
  * output).
  */
+/* Fills block [i0, i1) x [j0, j1) of the output described by pl. */
+static int run_block(const orc_plan *pl, int op, int enc, int64_t K, int64_t N,
+                     const void *X, const void *W, const void *dY, int64_t i0,
+                     int64_t i1, int64_t j0, int64_t j1, double *out)
+{
+    if (enc != ORC_IN_BF16 && enc != ORC_IN_F32) return -1;
+    if (i0 < 0 || j0 < 0 || i1 < i0 || j1 < j0 || i1 > pl->out_rows ||
+        j1 > pl->out_cols)
+        return -1;
+    int64_t w = j1 - j0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = i0; i < i1; ++i)
+        for (int64_t j = j0; j < j1; ++j)
+            out[(i - i0) * w + (j - j0)] =
+                element(pl, op, enc, K, N, X, W, dY, i, j);
+    return 0;
+}
+
+/* Fills out[s] with element (ii[s], jj[s]) of the output described by pl. */
+static int run_samples(const orc_plan *pl, int op, int enc, int64_t K, int64_t N,
+                       const void *X, const void *W, const void *dY, int64_t n,
+                       const int64_t *ii, const int64_t *jj, double *out)
+{
+    if (enc != ORC_IN_BF16 && enc != ORC_IN_F32) return -1;
+    for (int64_t s = 0; s < n; ++s)
+        if (ii[s] < 0 || ii[s] >= pl->out_rows || jj[s] < 0 || jj[s] >= pl->out_cols)
+            return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t s = 0; s < n; ++s)
+        out[s] = element(pl, op, enc, K, N, X, W, dY, ii[s], jj[s]);
+    return 0;
+}
+
+/*
+ * Block [i0, i1) x [j0, j1) of rank r's output of operation op, as fp64,
+ * written row-major into out ((i1-i0) x (j1-j0)). Inputs are the global,
+ * contiguous row-major X (M x K), W (K x N) and dY (M x N); only the tensors
+ * the operation reads need to be non-null. Returns 0, or -1 on a bad
+ * argument (unknown signature/op, rank out of range, block outside the
+ * output).
+ */
 int orc_linear_block(int sig, int op, int enc, int64_t M, int64_t K, int64_t N,
                      int64_t p, int64_t r, const void *X, const void *W,
                      const void *dY, int64_t i0, int64_t i1, int64_t j0,
@@ -203,17 +255,7 @@ int orc_linear_block(int sig, int op, int enc, int64_t M, int64_t K, int64_t N,
 {
     orc_plan pl;
     if (make_plan(sig, op, M, K, N, p, r, &pl) != 0) return -1;
-    if (enc != ORC_IN_BF16 && enc != ORC_IN_F32) return -1;
-    if (i0 < 0 || j0 < 0 || i1 < i0 || j1 < j0 || i1 > pl.out_rows ||
-        j1 > pl.out_cols)
-        return -1;
-    int64_t w = j1 - j0;
-#pragma omp parallel for schedule(dynamic, 1)
-    for (int64_t i = i0; i < i1; ++i)
-        for (int64_t j = j0; j < j1; ++j)
-            out[(i - i0) * w + (j - j0)] =
-                element(&pl, op, enc, K, N, X, W, dY, i, j);
-    return 0;
+    return run_block(&pl, op, enc, K, N, X, W, dY, i0, i1, j0, j1, out);
 }
 
 /* n single elements (ii[s], jj[s]) of rank r's output, as fp64. */
@@ -224,14 +266,208 @@ int orc_linear_samples(int sig, int op, int enc, int64_t M, int64_t K,
 {
     orc_plan pl;
     if (make_plan(sig, op, M, K, N, p, r, &pl) != 0) return -1;
-    if (enc != ORC_IN_BF16 && enc != ORC_IN_F32) return -1;
-    for (int64_t s = 0; s < n; ++s)
-        if (ii[s] < 0 || ii[s] >= pl.out_rows || jj[s] < 0 || jj[s] >= pl.out_cols)
-            return -1;
-#pragma omp parallel for schedule(dynamic, 16)
-    for (int64_t s = 0; s < n; ++s)
-        out[s] = element(&pl, op, enc, K, N, X, W, dY, ii[s], jj[s]);
+    return run_samples(&pl, op, enc, K, N, X, W, dY, n, ii, jj, out);
+}
+
+/* -------------------------------------- nd-SBP on device meshes ------- */
+/*
+ * On a d-dimensional device mesh (Sec. 4.1, Listing 1: one SBP state per
+ * level of the placement hierarchy) a tensor has one state per mesh axis,
+ * and a device is named by its mesh coordinate c[0..d-1].
+ *
+ * Share. The splits nest in mesh-axis order: mesh axis 0 cuts the tensor
+ * axis it splits into p[0] balanced blocks and keeps block c[0]; every later
+ * mesh axis that splits the same tensor axis cuts the block kept so far
+ * with the same balanced rule. Broadcast and Partial-sum axes keep the
+ * block. (Reading: the paper gives the composition through shapes only --
+ * Listing 1's 2 x 2 blocks -- and writes merged splits as one split over
+ * p1*p2; the nesting order makes (S1:p1, S1:p2) the split over p1*p2 with
+ * block c1*p2 + c2 whenever p1*p2 divides the extent.)
+ *
+ * Signature. Each mesh axis carries one 1-D factor of the table above (the
+ * 3-D rule of Sec. 4.2 is DP on mesh axis 0, COL on axis 1, KS on axis 2),
+ * or Broadcast for both X and W: such an axis replicates the whole product
+ * and all six tensors are Broadcast on it.
+ *
+ * Mesh coordinate of a device (Sec. 4.2, heterogeneous networks). Mesh axis
+ * a spans nodes[a] nodes x gpus[a] GPUs per node. The node index and the
+ * GPU index are each read as mixed-radix numbers with mesh axis 0 as the
+ * lowest digit, and c[a] = (node digit a) * gpus[a] + (GPU digit a). The
+ * paper's example (S0:(1,2), B:(2,2)) -- split 0 of the data on GPUs
+ * (0,0), (0,2), (1,0), (1,2) -- fixes the GPU-level digit order; putting
+ * the node digit above the GPU digit within one mesh axis is a reading.
+ */
+#define ORC_MAXD 4
+#define ORC_BB 3   /* replicated mesh axis: X and W both Broadcast */
+
+int orc_mesh_coord(int d, const int32_t *nodes, const int32_t *gpus,
+                   int64_t node, int64_t gpu, int32_t *c)
+{
+    if (d < 1 || d > ORC_MAXD) return -1;
+    int64_t node_stride = 1, gpu_stride = 1;
+    for (int a = 0; a < d; ++a) {
+        if (nodes[a] < 1 || gpus[a] < 1) return -1;
+        int64_t n_digit = (node / node_stride) % nodes[a];
+        int64_t g_digit = (gpu / gpu_stride) % gpus[a];
+        c[a] = (int32_t)(n_digit * gpus[a] + g_digit);
+        node_stride *= nodes[a];
+        gpu_stride *= gpus[a];
+    }
+    if (node < 0 || node >= node_stride || gpu < 0 || gpu >= gpu_stride) return -1;
     return 0;
+}
+
+/* Factor of one mesh axis from the (kind, axis) states of X and W on it. */
+static int axis_factor(int32_t xk, int32_t xa, int32_t wk, int32_t wa)
+{
+    int32_t kd[6], ax[6];
+    for (int sig = 0; sig < 3; ++sig) {
+        orc_tags(sig, kd, ax);
+        if (kd[0] == xk && ax[0] == xa && kd[1] == wk && ax[1] == wa) return sig;
+    }
+    if (xk == ORC_BCAST && xa == -1 && wk == ORC_BCAST && wa == -1) return ORC_BB;
+    return -1;
+}
+
+/*
+ * Per mesh axis, the (kind, axis) states of X, W, Y, dY, dX, dW for the
+ * given states of X and W (d entries each). kinds and axes receive 6*d
+ * entries, tensor-major: tensor t on mesh axis a at [t*d + a]. Returns 0, or
+ * -1 when some mesh axis carries no factor.
+ */
+int orc_nd_tags(int d, const int32_t *xk, const int32_t *xa, const int32_t *wk,
+                const int32_t *wa, int32_t *kinds, int32_t *axes)
+{
+    if (d < 1 || d > ORC_MAXD) return -1;
+    for (int a = 0; a < d; ++a) {
+        int f = axis_factor(xk[a], xa[a], wk[a], wa[a]);
+        int32_t kd[6], ax[6];
+        if (f < 0) return -1;
+        if (f == ORC_BB) {
+            for (int t = 0; t < 6; ++t) { kd[t] = ORC_BCAST; ax[t] = -1; }
+        } else {
+            orc_tags(f, kd, ax);
+        }
+        for (int t = 0; t < 6; ++t) {
+            kinds[t * d + a] = kd[t];
+            axes[t * d + a] = ax[t];
+        }
+    }
+    return 0;
+}
+
+static int valid_mesh(int d, const int32_t *p, const int32_t *c)
+{
+    if (d < 1 || d > ORC_MAXD) return 0;
+    for (int a = 0; a < d; ++a)
+        if (p[a] < 1 || c[a] < 0 || c[a] >= p[a]) return 0;
+    return 1;
+}
+
+/* The device's share of a rows x cols tensor with states (k[a], ax[a]). */
+static orc_share nd_share_of(int d, const int32_t *k, const int32_t *ax,
+                             const int32_t *p, const int32_t *c, int64_t rows,
+                             int64_t cols)
+{
+    orc_share s = {0, rows, 0, cols};
+    for (int a = 0; a < d; ++a) {
+        int64_t off, len;
+        if (k[a] != ORC_SPLIT) continue;
+        if (ax[a] == 0) {
+            orc_split(s.nr, p[a], c[a], &off, &len);
+            s.r0 += off;
+            s.nr = len;
+        } else {
+            orc_split(s.nc, p[a], c[a], &off, &len);
+            s.c0 += off;
+            s.nc = len;
+        }
+    }
+    return s;
+}
+
+/*
+ * Share (row offset, col offset, rows, cols) of a rows x cols tensor in
+ * per-axis states (k, ax) for the device at c on mesh p. Returns 0, or -1
+ * for a bad mesh, coordinate or state.
+ */
+int orc_nd_share(int d, const int32_t *k, const int32_t *ax, const int32_t *p,
+                 const int32_t *c, int64_t rows, int64_t cols, int64_t out[4])
+{
+    if (!valid_mesh(d, p, c) || rows < 0 || cols < 0) return -1;
+    for (int a = 0; a < d; ++a) {
+        if (k[a] == ORC_SPLIT && (ax[a] == 0 || ax[a] == 1)) continue;
+        if ((k[a] == ORC_BCAST || k[a] == ORC_PARTIAL) && ax[a] == -1) continue;
+        return -1;
+    }
+    orc_share s = nd_share_of(d, k, ax, p, c, rows, cols);
+    out[0] = s.r0;
+    out[1] = s.c0;
+    out[2] = s.nr;
+    out[3] = s.nc;
+    return 0;
+}
+
+/* Operand shares and output shape of op for the device at c. */
+static int make_nd_plan(int op, int64_t M, int64_t K, int64_t N, int d,
+                        const int32_t *p, const int32_t *c, const int32_t *xk,
+                        const int32_t *xa, const int32_t *wk, const int32_t *wa,
+                        orc_plan *pl, int32_t *kinds, int32_t *axes)
+{
+    if (op < 0 || op > 2 || !valid_mesh(d, p, c)) return -1;
+    if (orc_nd_tags(d, xk, xa, wk, wa, kinds, axes) != 0) return -1;
+    pl->x = nd_share_of(d, kinds + 0 * d, axes + 0 * d, p, c, M, K);
+    pl->w = nd_share_of(d, kinds + 1 * d, axes + 1 * d, p, c, K, N);
+    pl->dy = nd_share_of(d, kinds + 3 * d, axes + 3 * d, p, c, M, N);
+    set_out_shape(op, pl);
+    return 0;
+}
+
+/* Output shape of op and its per-axis states (d entries each). */
+int orc_nd_out_shape(int op, int64_t M, int64_t K, int64_t N, int d,
+                     const int32_t *p, const int32_t *c, const int32_t *xk,
+                     const int32_t *xa, const int32_t *wk, const int32_t *wa,
+                     int64_t *rows, int64_t *cols, int32_t *kind, int32_t *axis)
+{
+    orc_plan pl;
+    int32_t kinds[6 * ORC_MAXD], axes[6 * ORC_MAXD];
+    if (make_nd_plan(op, M, K, N, d, p, c, xk, xa, wk, wa, &pl, kinds, axes) != 0)
+        return -1;
+    int t = (op == ORC_FWD) ? 2 : (op == ORC_BWD_DATA ? 4 : 5);
+    *rows = pl.out_rows;
+    *cols = pl.out_cols;
+    for (int a = 0; a < d; ++a) {
+        kind[a] = kinds[t * d + a];
+        axis[a] = axes[t * d + a];
+    }
+    return 0;
+}
+
+/* nd forms of orc_linear_block and orc_linear_samples. */
+int orc_nd_linear_block(int op, int enc, int64_t M, int64_t K, int64_t N, int d,
+                        const int32_t *p, const int32_t *c, const int32_t *xk,
+                        const int32_t *xa, const int32_t *wk, const int32_t *wa,
+                        const void *X, const void *W, const void *dY, int64_t i0,
+                        int64_t i1, int64_t j0, int64_t j1, double *out)
+{
+    orc_plan pl;
+    int32_t kinds[6 * ORC_MAXD], axes[6 * ORC_MAXD];
+    if (make_nd_plan(op, M, K, N, d, p, c, xk, xa, wk, wa, &pl, kinds, axes) != 0)
+        return -1;
+    return run_block(&pl, op, enc, K, N, X, W, dY, i0, i1, j0, j1, out);
+}
+
+int orc_nd_linear_samples(int op, int enc, int64_t M, int64_t K, int64_t N, int d,
+                          const int32_t *p, const int32_t *c, const int32_t *xk,
+                          const int32_t *xa, const int32_t *wk, const int32_t *wa,
+                          const void *X, const void *W, const void *dY, int64_t n,
+                          const int64_t *ii, const int64_t *jj, double *out)
+{
+    orc_plan pl;
+    int32_t kinds[6 * ORC_MAXD], axes[6 * ORC_MAXD];
+    if (make_nd_plan(op, M, K, N, d, p, c, xk, xa, wk, wa, &pl, kinds, axes) != 0)
+        return -1;
+    return run_samples(&pl, op, enc, K, N, X, W, dY, n, ii, jj, out);
 }
 
 /*
