@@ -204,13 +204,15 @@ def cpu_baseline(wl, seconds):
 
 def report_workload(cid, ranks, reps):
     """Per-call throughput of workload cid (2: Transformer FFN shard, 3: attention
-    projections, 4: VGG head) on the given ranks: each call (the forward product,
+    projections, 4: VGG head, 6: a Transformer layer under the 3-D rule on a
+    2 x 2 x 2 mesh; its ranks are mesh coordinates) on the given ranks: each call (the forward product,
     or both backward products in one sbp_linear_bwd call) is replayed from a HIP
     graph over three rotating sets of its global inputs (more than the 256 MB
     Infinity Cache for the larger workloads). Returns one dict for the JSON line."""
     import torch
     from paper_2301_06813_amd import linear, sbp, workloads
-    wl = {2: workloads.ffn_shard, 3: workloads.attention_dp, 4: workloads.vgg_head}[cid]()
+    wl = {2: workloads.ffn_shard, 3: workloads.attention_dp, 4: workloads.vgg_head,
+          6: workloads.transformer_3d}[cid]()
     stream = torch.cuda.Stream()
     rows = []
     for lin in wl.linears:
@@ -219,9 +221,9 @@ def report_workload(cid, ranks, reps):
             X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
             sets.append((X, W, dY))
         for r in ranks:
-            L = linear.layouts(lin.sig, wl.p, r)
-            outs = [{op: linear.alloc_out(op, lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype,
-                                          "cuda") for op in OPS} for _ in sets]
+            L = linear.layouts_for(lin, wl, r)
+            outs = [{op: linear.alloc_out_L(op, L, lin.M, lin.K, lin.N, wl.dtype, "cuda")
+                     for op in OPS} for _ in sets]
             for kind in ("fwd", "bwd"):
                 it = [0]
 
@@ -231,10 +233,10 @@ def report_workload(cid, ranks, reps):
                     X, W, dY = sets[i]
                     o = outs[i]
                     if kind == "fwd":
-                        linear.run("fwd", lin.sig, wl.p, r, X, W, dY, o["fwd"], stream.cuda_stream)
+                        linear.run_L("fwd", L, X, W, dY, o["fwd"], stream.cuda_stream)
                     else:
-                        linear.run_bwd(lin.sig, wl.p, r, X, W, dY, o["bwd_data"],
-                                       o["bwd_weight"], stream.cuda_stream)
+                        linear.run_bwd_L(L, X, W, dY, o["bwd_data"], o["bwd_weight"],
+                                         stream.cuda_stream)
                 with torch.cuda.stream(stream):
                     call()
                     torch.cuda.synchronize()
@@ -255,29 +257,34 @@ def report_workload(cid, ranks, reps):
                 prods, fl, by = [], 0.0, 0.0
                 for op in ops:
                     m, n = outs[0][op].shape
-                    k = {"fwd": sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols,
-                         "bwd_data": sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols,
-                         "bwd_weight": sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows}[op]
+                    k = {"fwd": linear.shard(L["x"], lin.M, lin.K).cols,
+                         "bwd_data": linear.shard(L["dy"], lin.M, lin.N).cols,
+                         "bwd_weight": linear.shard(L["x"], lin.M, lin.K).rows}[op]
                     ob = 4 if outs[0][op].dtype == torch.float32 else 2
                     prods.append("%s %dx%dx%d%s" % (op, m, n, k, " fp32" if ob == 4 else ""))
                     fl += 2.0 * m * n * k
                     by += 2.0 * (m * k + k * n) + ob * m * n
-                rows.append({"linear": lin.name, "sig": lin.sig, "rank": r, "call": kind,
+                rank = list(r) if wl.mesh else r
+                rows.append({"linear": lin.name, "sig": lin.sig, "rank": rank, "call": kind,
                              "products": prods, "us": us, "tflops": fl / us / 1e6,
                              "pct_of_bf16_peak": 100.0 * fl / us / 1e6 / BF16_PEAK_TFLOPS,
                              "algorithmic_gbs": by / us / 1e3,
                              "roofline_min_us": max(fl / BF16_PEAK_TFLOPS / 1e6,
                                                     by / HBM_PEAK_GBS / 1e3)})
-                log("%-4s %-4s r%d %-3s %7.1f us %6.0f TFLOP/s %s" % (
+                log("%-4s %-4s r%s %-3s %7.1f us %6.0f TFLOP/s %s" % (
                     lin.name, lin.sig, r, kind, us, fl / us / 1e6, ", ".join(prods)))
         del sets
         torch.cuda.empty_cache()
-    tot_us = sum(x["us"] for x in rows if x["rank"] == ranks[0])
-    tot_fl = sum(x["tflops"] * x["us"] * 1e6 for x in rows if x["rank"] == ranks[0])
+    first = list(ranks[0]) if wl.mesh else ranks[0]
+    tot_us = sum(x["us"] for x in rows if x["rank"] == first)
+    tot_fl = sum(x["tflops"] * x["us"] * 1e6 for x in rows if x["rank"] == first)
     return {"metric": "local-shard GEMM TFLOP/s (fwd+bwd) per SBP signature; % of bf16 MFMA peak",
             "value": tot_fl / tot_us / 1e6, "unit": "TFLOP/s", "n_gpus": 1,
             "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
-            "config": {"workload": wl.name, "p": wl.p, "ranks": list(ranks),
+            "config": {"workload": wl.name, "p": wl.p,
+                       "ranks": [list(r) for r in ranks] if wl.mesh else list(ranks),
+                       **({"mesh": list(wl.mesh),
+                           "factors": list(wl.linears[0].factors)} if wl.mesh else {}),
                        "mode": "per-call hip_graph replay"},
             "calls": rows}
 
@@ -293,7 +300,7 @@ def main():
     ap.add_argument("--dump", default=None, help="write per-launch shapes and durations (JSON)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (scale for HBM counters)")
-    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 4, 5),
+    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 4, 5, 6),
                     help="5 (default): the 24-layer step; 2-4: per-call report of that "
                          "workload's local products")
     args = ap.parse_args()
@@ -317,7 +324,7 @@ def main():
         return
     sbp.lib()
     if args.workload != 5:
-        ranks = (0, 1) if args.workload == 4 else (0,)
+        ranks = {4: (0, 1), 6: ((0, 0, 0),)}.get(args.workload, (0,))
         print(json.dumps(report_workload(args.workload, ranks, reps=10)))
         return
     wl = workloads.transformer_step()

@@ -171,6 +171,97 @@ int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy,
                    sbp_layout_t *ldx_out, sbp_view_t *dW, sbp_layout_t *ldw_out,
                    hipStream_t stream);
 
+/* ------------------------------------------- nd-SBP on device meshes --- */
+
+/* Mesh axes an nd layout may have. */
+#define SBP_MAX_MESH_DIMS 4
+
+/* SBP state of a tensor on a d-dimensional device mesh, seen from the
+ * device at mesh coordinate c: one Split / Broadcast / Partial-sum state
+ * per mesh axis (Sec. 4.1, Listing 1: a placement hierarchy such as
+ * (2, 3, 4) with one state per hierarchy level; Sec. 4.2: the 3-D rule
+ * (S0:p0, B:p1, S1:p2) x (B:p0, S1:p1, S0:p2) -> (S0:p0, S1:p1, P:p2)).
+ *   ndim     mesh axes d, 1..SBP_MAX_MESH_DIMS; entries a >= d are ignored
+ *   kind[a]  sbp_kind_t on mesh axis a
+ *   axis[a]  tensor axis (0 or 1) for SBP_SPLIT, else -1
+ *   p[a]     devices along mesh axis a (>= 1)
+ *   c[a]     this device's coordinate along mesh axis a, in [0, p[a])
+ * The share of a tensor nests the splits in mesh-axis order: mesh axis 0
+ * cuts the full extent into p[0] balanced blocks (the 1-D rule above), mesh
+ * axis 1 cuts block c[0] into p[1] blocks, and so on; each tensor axis is cut
+ * only by the mesh axes that split it. Broadcast and Partial-sum axes do not
+ * cut. A 1-D layout (kind, axis, p, r) is the nd layout with d = 1,
+ * c[0] = r. */
+typedef struct {
+    int32_t ndim;
+    int32_t kind[SBP_MAX_MESH_DIMS];
+    int32_t axis[SBP_MAX_MESH_DIMS];
+    int32_t p[SBP_MAX_MESH_DIMS];
+    int32_t c[SBP_MAX_MESH_DIMS];
+} sbp_nd_layout_t;
+
+/* Mesh coordinate of a device (Sec. 4.2, "Strategies for heterogeneous
+ * interconnected networks"). Mesh axis a spans nodes[a] x gpus[a] devices:
+ * nodes[a] compute nodes times gpus[a] GPUs of each node. Device (node, gpu)
+ * -- node in [0, prod nodes), gpu in [0, prod gpus) -- has node-level digits
+ * n_a and GPU-level digits g_a, both mixed-radix with mesh axis 0 varying
+ * fastest (node = n_0 + nodes[0] (n_1 + nodes[1] (...)), likewise gpu), and
+ * coordinate c[a] = n_a * gpus[a] + g_a. The paper's example
+ * (S0:(1,2), B:(2,2)) on 2 nodes of 4 GPUs puts split 0 on GPUs (0,0),
+ * (0,2), (1,0), (1,2): mesh axis 0 varies fastest within a node. For a
+ * single-level mesh pass gpus = NULL (all 1) and the device rank as node.
+ * Pure host function. Errors: SBP_ERR_NULL (nodes or c), SBP_ERR_LAYOUT
+ * (ndim outside [1, SBP_MAX_MESH_DIMS], a factor < 1, or node / gpu outside
+ * its range). */
+int sbp_mesh_coords(int32_t ndim, const int32_t *nodes, const int32_t *gpus,
+                    int64_t node, int64_t gpu, int32_t *c);
+
+/* The device's share of a rows x cols tensor in nd state *l (nested splits,
+ * as described at sbp_nd_layout_t). Pure host function.
+ * Errors: SBP_ERR_NULL, SBP_ERR_LAYOUT (bad ndim, p, c, kind or axis),
+ * SBP_ERR_SHAPE (negative extent). */
+int sbp_nd_shard_index(const sbp_nd_layout_t *l, int64_t rows, int64_t cols,
+                       sbp_shard_t *out);
+
+/* Resolves the nd signature of Y = X W (Sec. 4.2: the 3-D rule factors
+ * into one 1-D signature per mesh axis) and writes the nd states of Y, dY,
+ * dX and dW (Sec. 4.3 gradient states, per axis). Each mesh axis must carry
+ * one of the 1-D factors of the table at the top of this file (DP, COL,
+ * KS), or Broadcast on both X and W (that axis does not divide the product:
+ * Y, dY, dX and dW are Broadcast on it). The layouts must agree on ndim, p
+ * and c. Any of y, dy, dx, dw may be NULL. Pure host function.
+ * Errors: SBP_ERR_NULL (x or w), SBP_ERR_LAYOUT, SBP_ERR_SIGNATURE. */
+int sbp_nd_signature(const sbp_nd_layout_t *x, const sbp_nd_layout_t *w,
+                     sbp_nd_layout_t *y, sbp_nd_layout_t *dy,
+                     sbp_nd_layout_t *dx, sbp_nd_layout_t *dw);
+
+/* nd forms of the four compute calls: the device's local products on its
+ * nd shares, on the same kernels. Views, dtypes, scopes, streams and errors
+ * are those of the 1-D calls, with nd layouts in place of 1-D ones (all
+ * layouts of one call agree on ndim, p and c, else SBP_ERR_LAYOUT).
+ * Local output shapes: X_r is the nd share of X, and so on; Y_r = X_r W_r,
+ * dX_r = dY_r W_r^T, dW_r = X_r^T dY_r. An output is Partial-sum -- and must
+ * be fp32 -- when any mesh axis leaves it Partial-sum: Y under a KS axis, dX
+ * under a COL axis, dW under a DP axis. */
+int sbp_nd_linear_fwd(const sbp_view_t *X, const sbp_nd_layout_t *lx,
+                      const sbp_view_t *W, const sbp_nd_layout_t *lw,
+                      sbp_view_t *Y, sbp_nd_layout_t *ly_out,
+                      hipStream_t stream);
+int sbp_nd_linear_bwd_data(const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
+                           const sbp_view_t *W, const sbp_nd_layout_t *lw,
+                           sbp_view_t *dX, sbp_nd_layout_t *ldx_out,
+                           hipStream_t stream);
+int sbp_nd_linear_bwd_weight(const sbp_view_t *X, const sbp_nd_layout_t *lx,
+                             const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
+                             sbp_view_t *dW, sbp_nd_layout_t *ldw_out,
+                             hipStream_t stream);
+int sbp_nd_linear_bwd(const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
+                      const sbp_view_t *X, const sbp_nd_layout_t *lx,
+                      const sbp_view_t *W, const sbp_nd_layout_t *lw,
+                      sbp_view_t *dX, sbp_nd_layout_t *ldx_out,
+                      sbp_view_t *dW, sbp_nd_layout_t *ldw_out,
+                      hipStream_t stream);
+
 /* --------------------------------------------------------- utilities --- */
 
 /* Static description of an error code (never NULL). */

@@ -3,7 +3,10 @@
 // Host-side SBP logic (AutoDDL Sec. 4.1 states, Sec. 4.2 SBP matmul rule,
 // Sec. 4.3 gradient states): layout checks, shard indexing, signature
 // resolution, argument validation, then one kernel launch on the caller's
-// stream. Every validation happens before the first HIP call.
+// stream. Every validation happens before the first HIP call. 1-D layouts
+// (one state on a mesh of p devices) and nd layouts (one state per mesh
+// axis) share the validation and launch code below; an nd signature is one
+// 1-D factor per mesh axis.
 #include <stdint.h>
 #include <string.h>
 
@@ -126,32 +129,6 @@ int check_view_common(const sbp_view_t *v) {
     return SBP_OK;
 }
 
-int local_input(const sbp_view_t *v, const sbp_layout_t *l, Local *out) {
-    int rc = check_view_common(v);
-    if (rc) return rc;
-    if (v->scope != SBP_GLOBAL && v->scope != SBP_LOCAL) return SBP_ERR_SHAPE;
-    out->dtype = v->dtype;
-    out->ld = v->ld;
-    out->grows = v->rows;
-    out->gcols = v->cols;
-    out->global = (v->scope == SBP_GLOBAL);
-    if (out->global) {
-        sbp_shard_t s;
-        rc = sbp_shard_index(l, v->rows, v->cols, &s);
-        if (rc) return rc;
-        out->rows = s.rows;
-        out->cols = s.cols;
-        out->ptr = static_cast<const char *>(v->data);
-        if (s.rows > 0 && s.cols > 0)
-            out->ptr += (s.row_off * v->ld + s.col_off) * (int64_t)elsize(v->dtype);
-    } else {
-        out->rows = v->rows;
-        out->cols = v->cols;
-        out->ptr = static_cast<const char *>(v->data);
-    }
-    return SBP_OK;
-}
-
 // [begin, end) bytes a view touches (empty when it has no elements).
 std::pair<uintptr_t, uintptr_t> extent(const void *p, int64_t rows, int64_t cols, int64_t ld,
                                        int32_t dtype) {
@@ -231,69 +208,200 @@ int run(const sbpi::Gemm &g, hipStream_t s) {
 }
 
 
-// Validation and operand mapping of the three products (no HIP calls).
-int prep_fwd(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *W,
-             const sbp_layout_t *lw, const sbp_view_t *Y, sbpi::Gemm *g, sbp_layout_t *st_out) {
-    if (!X || !W || !Y || !lx || !lw) return SBP_ERR_NULL;
-    int rc = check_pair(lx, lw);
+// ------------------------------------------------------------ nd layouts
+// The 1-D layout (kind, axis, p, r) of mesh axis a of an nd layout.
+sbp_layout_t axis_layout(const sbp_nd_layout_t *l, int a) {
+    sbp_layout_t o;
+    o.kind = l->kind[a];
+    o.axis = l->axis[a];
+    o.p = l->p[a];
+    o.r = l->c[a];
+    return o;
+}
+
+int check_nd(const sbp_nd_layout_t *l) {
+    if (!l) return SBP_ERR_NULL;
+    if (l->ndim < 1 || l->ndim > SBP_MAX_MESH_DIMS) return SBP_ERR_LAYOUT;
+    for (int a = 0; a < l->ndim; ++a) {
+        const sbp_layout_t o = axis_layout(l, a);
+        int rc = check_layout(&o);
+        if (rc) return rc;
+    }
+    return SBP_OK;
+}
+
+int check_pair(const sbp_nd_layout_t *a, const sbp_nd_layout_t *b) {
+    int rc = check_nd(a);
     if (rc) return rc;
-    Sig s = sig_from_xw(lx, lw);
+    if ((rc = check_nd(b))) return rc;
+    if (a->ndim != b->ndim) return SBP_ERR_LAYOUT;
+    for (int i = 0; i < a->ndim; ++i)
+        if (a->p[i] != b->p[i] || a->c[i] != b->c[i]) return SBP_ERR_LAYOUT;
+    return SBP_OK;
+}
+
+// Per-axis factor of an nd signature: a 1-D signature, or Broadcast on both
+// operands (the axis does not divide the product).
+constexpr int SIG_BB = 3;
+
+bool both_bcast(const sbp_layout_t &a, const sbp_layout_t &b) {
+    return is_bcast(&a) && is_bcast(&b);
+}
+
+// States of Y, dY, dX, dW on mesh axis a given its factor.
+void axis_states(int sig, const sbp_layout_t *like, sbp_layout_t out[4]) {
+    if (sig == SIG_BB) {
+        for (int t = 0; t < 4; ++t) out[t] = mk(SBP_BROADCAST, -1, like);
+        return;
+    }
+    states_of((Sig)sig, like, out);
+}
+
+void nd_set(sbp_nd_layout_t *l, int a, const sbp_layout_t &o) {
+    l->kind[a] = o.kind;
+    l->axis[a] = o.axis;
+}
+
+// Which pair of operands a product's signature is read from.
+enum Pair { PAIR_XW = 0, PAIR_DYW = 1, PAIR_XDY = 2 };
+
+int factor_of(Pair pr, const sbp_layout_t &a, const sbp_layout_t &b) {
+    Sig s = pr == PAIR_XW ? sig_from_xw(&a, &b)
+                          : (pr == PAIR_DYW ? sig_from_dyw(&a, &b) : sig_from_xdy(&a, &b));
+    if (s != SIG_NONE) return s;
+    return both_bcast(a, b) ? SIG_BB : -1;
+}
+
+// Signature of a product from its two input layouts: st[0..3] get the
+// states of Y, dY, dX, dW. 1-D form: the table at the top of sbp.h.
+int resolve(Pair pr, const sbp_layout_t *a, const sbp_layout_t *b, sbp_layout_t st[4]) {
+    int rc = check_pair(a, b);
+    if (rc) return rc;
+    Sig s = pr == PAIR_XW ? sig_from_xw(a, b)
+                          : (pr == PAIR_DYW ? sig_from_dyw(a, b) : sig_from_xdy(a, b));
     if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
+    states_of(s, a, st);
+    return SBP_OK;
+}
+
+// nd form: one factor per mesh axis (Sec. 4.2, the 3-D rule factors).
+int resolve(Pair pr, const sbp_nd_layout_t *a, const sbp_nd_layout_t *b, sbp_nd_layout_t st[4],
+            int *factors = nullptr) {
+    int rc = check_pair(a, b);
+    if (rc) return rc;
+    for (int t = 0; t < 4; ++t) st[t] = *a;
+    for (int i = 0; i < a->ndim; ++i) {
+        const sbp_layout_t la = axis_layout(a, i), lb = axis_layout(b, i);
+        const int f = factor_of(pr, la, lb);
+        if (f < 0) return SBP_ERR_SIGNATURE;
+        if (factors) factors[i] = f;
+        sbp_layout_t o[4];
+        axis_states(f, &la, o);
+        for (int t = 0; t < 4; ++t) nd_set(&st[t], i, o[t]);
+    }
+    return SBP_OK;
+}
+
+bool is_partial(const sbp_layout_t &l) { return l.kind == SBP_PARTIAL; }
+bool is_partial(const sbp_nd_layout_t &l) {
+    for (int a = 0; a < l.ndim; ++a)
+        if (l.kind[a] == SBP_PARTIAL) return true;
+    return false;
+}
+
+int shard_of(const sbp_layout_t *l, int64_t rows, int64_t cols, sbp_shard_t *s) {
+    return sbp_shard_index(l, rows, cols, s);
+}
+int shard_of(const sbp_nd_layout_t *l, int64_t rows, int64_t cols, sbp_shard_t *s) {
+    return sbp_nd_shard_index(l, rows, cols, s);
+}
+
+template <class L>
+int local_input(const sbp_view_t *v, const L *l, Local *out) {
+    int rc = check_view_common(v);
+    if (rc) return rc;
+    if (v->scope != SBP_GLOBAL && v->scope != SBP_LOCAL) return SBP_ERR_SHAPE;
+    out->dtype = v->dtype;
+    out->ld = v->ld;
+    out->grows = v->rows;
+    out->gcols = v->cols;
+    out->global = (v->scope == SBP_GLOBAL);
+    if (out->global) {
+        sbp_shard_t s;
+        rc = shard_of(l, v->rows, v->cols, &s);
+        if (rc) return rc;
+        out->rows = s.rows;
+        out->cols = s.cols;
+        out->ptr = static_cast<const char *>(v->data);
+        if (s.rows > 0 && s.cols > 0)
+            out->ptr += (s.row_off * v->ld + s.col_off) * (int64_t)elsize(v->dtype);
+    } else {
+        out->rows = v->rows;
+        out->cols = v->cols;
+        out->ptr = static_cast<const char *>(v->data);
+    }
+    return SBP_OK;
+}
+
+// Validation and operand mapping of the three products (no HIP calls), for
+// 1-D (L = sbp_layout_t) and nd (L = sbp_nd_layout_t) layouts.
+template <class L>
+int prep_fwd(const sbp_view_t *X, const L *lx, const sbp_view_t *W, const L *lw,
+             const sbp_view_t *Y, sbpi::Gemm *g, L *st_out) {
+    if (!X || !W || !Y || !lx || !lw) return SBP_ERR_NULL;
+    L st[4];
+    int rc = resolve(PAIR_XW, lx, lw, st);
+    if (rc) return rc;
     Local x, w;
     if ((rc = local_input(X, lx, &x))) return rc;
     if ((rc = local_input(W, lw, &w))) return rc;
     if (x.dtype != w.dtype) return SBP_ERR_DTYPE;
     if (x.global && w.global && x.gcols != w.grows) return SBP_ERR_SHAPE;
     if (x.cols != w.rows) return SBP_ERR_SHAPE;
-    sbp_layout_t st[4];
-    states_of(s, lx, st);
-    if ((rc = check_output(Y, x.rows, w.cols, x.dtype, st[0].kind, x, w))) return rc;
+    const int kind = is_partial(st[0]) ? SBP_PARTIAL : SBP_SPLIT;
+    if ((rc = check_output(Y, x.rows, w.cols, x.dtype, kind, x, w))) return rc;
     *g = sbpi::Gemm{sbpi::OR_FWD, x.dtype, Y->dtype, x.ptr, x.ld, w.ptr, w.ld,
                     Y->data, Y->ld, x.rows, w.cols, x.cols};
     *st_out = st[0];
     return SBP_OK;
 }
 
-int prep_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *W,
-                  const sbp_layout_t *lw, const sbp_view_t *dX, sbpi::Gemm *g,
-                  sbp_layout_t *st_out) {
+template <class L>
+int prep_bwd_data(const sbp_view_t *dY, const L *ldy, const sbp_view_t *W, const L *lw,
+                  const sbp_view_t *dX, sbpi::Gemm *g, L *st_out) {
     if (!dY || !W || !dX || !ldy || !lw) return SBP_ERR_NULL;
-    int rc = check_pair(ldy, lw);
+    L st[4];
+    int rc = resolve(PAIR_DYW, ldy, lw, st);
     if (rc) return rc;
-    Sig s = sig_from_dyw(ldy, lw);
-    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
     Local d, w;
     if ((rc = local_input(dY, ldy, &d))) return rc;
     if ((rc = local_input(W, lw, &w))) return rc;
     if (d.dtype != w.dtype) return SBP_ERR_DTYPE;
     if (d.global && w.global && d.gcols != w.gcols) return SBP_ERR_SHAPE;
     if (d.cols != w.cols) return SBP_ERR_SHAPE;
-    sbp_layout_t st[4];
-    states_of(s, ldy, st);
-    if ((rc = check_output(dX, d.rows, w.rows, d.dtype, st[2].kind, d, w))) return rc;
+    const int kind = is_partial(st[2]) ? SBP_PARTIAL : SBP_SPLIT;
+    if ((rc = check_output(dX, d.rows, w.rows, d.dtype, kind, d, w))) return rc;
     *g = sbpi::Gemm{sbpi::OR_BWD_DATA, d.dtype, dX->dtype, d.ptr, d.ld, w.ptr, w.ld,
                     dX->data, dX->ld, d.rows, w.rows, d.cols};
     *st_out = st[2];
     return SBP_OK;
 }
 
-int prep_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *dY,
-                    const sbp_layout_t *ldy, const sbp_view_t *dW, sbpi::Gemm *g,
-                    sbp_layout_t *st_out) {
+template <class L>
+int prep_bwd_weight(const sbp_view_t *X, const L *lx, const sbp_view_t *dY, const L *ldy,
+                    const sbp_view_t *dW, sbpi::Gemm *g, L *st_out) {
     if (!X || !dY || !dW || !lx || !ldy) return SBP_ERR_NULL;
-    int rc = check_pair(lx, ldy);
+    L st[4];
+    int rc = resolve(PAIR_XDY, lx, ldy, st);
     if (rc) return rc;
-    Sig s = sig_from_xdy(lx, ldy);
-    if (s == SIG_NONE) return SBP_ERR_SIGNATURE;
     Local x, d;
     if ((rc = local_input(X, lx, &x))) return rc;
     if ((rc = local_input(dY, ldy, &d))) return rc;
     if (x.dtype != d.dtype) return SBP_ERR_DTYPE;
     if (x.global && d.global && x.grows != d.grows) return SBP_ERR_SHAPE;
     if (x.rows != d.rows) return SBP_ERR_SHAPE;
-    sbp_layout_t st[4];
-    states_of(s, lx, st);
-    if ((rc = check_output(dW, x.cols, d.cols, x.dtype, st[3].kind, x, d))) return rc;
+    const int kind = is_partial(st[3]) ? SBP_PARTIAL : SBP_SPLIT;
+    if ((rc = check_output(dW, x.cols, d.cols, x.dtype, kind, x, d))) return rc;
     *g = sbpi::Gemm{sbpi::OR_BWD_WEIGHT, x.dtype, dW->dtype, x.ptr, x.ld, d.ptr, d.ld,
                     dW->data, dW->ld, x.cols, d.cols, x.rows};
     *st_out = st[3];
@@ -325,6 +433,87 @@ int run_pair(const sbpi::Gemm &gd, const sbpi::Gemm &gw, hipStream_t s) {
     int rc = run(gd, s);
     if (rc) return rc;
     return run(gw, s);
+}
+
+// The three input states of a backward call describe one signature: the
+// factor read from (X, W) equals those read from (dY, W) and (X, dY).
+bool one_signature(const sbp_layout_t *lx, const sbp_layout_t *lw, const sbp_layout_t *ldy) {
+    const Sig s = sig_from_xw(lx, lw);
+    return s != SIG_NONE && sig_from_dyw(ldy, lw) == s && sig_from_xdy(lx, ldy) == s;
+}
+bool one_signature(const sbp_nd_layout_t *lx, const sbp_nd_layout_t *lw,
+                   const sbp_nd_layout_t *ldy) {
+    for (int a = 0; a < lx->ndim; ++a) {
+        const sbp_layout_t x = axis_layout(lx, a), w = axis_layout(lw, a),
+                           d = axis_layout(ldy, a);
+        const int f = factor_of(PAIR_XW, x, w);
+        if (f < 0 || factor_of(PAIR_DYW, d, w) != f || factor_of(PAIR_XDY, x, d) != f)
+            return false;
+    }
+    return true;
+}
+
+template <class L>
+int linear_fwd(const sbp_view_t *X, const L *lx, const sbp_view_t *W, const L *lw,
+               sbp_view_t *Y, L *ly_out, hipStream_t stream) {
+    sbpi::Gemm g;
+    L st;
+    int rc = prep_fwd(X, lx, W, lw, Y, &g, &st);
+    if (rc) return rc;
+    if ((rc = run(g, stream))) return rc;
+    if (ly_out) *ly_out = st;
+    return SBP_OK;
+}
+
+template <class L>
+int linear_bwd_data(const sbp_view_t *dY, const L *ldy, const sbp_view_t *W, const L *lw,
+                    sbp_view_t *dX, L *ldx_out, hipStream_t stream) {
+    sbpi::Gemm g;
+    L st;
+    int rc = prep_bwd_data(dY, ldy, W, lw, dX, &g, &st);
+    if (rc) return rc;
+    if ((rc = run(g, stream))) return rc;
+    if (ldx_out) *ldx_out = st;
+    return SBP_OK;
+}
+
+template <class L>
+int linear_bwd_weight(const sbp_view_t *X, const L *lx, const sbp_view_t *dY, const L *ldy,
+                      sbp_view_t *dW, L *ldw_out, hipStream_t stream) {
+    sbpi::Gemm g;
+    L st;
+    int rc = prep_bwd_weight(X, lx, dY, ldy, dW, &g, &st);
+    if (rc) return rc;
+    if ((rc = run(g, stream))) return rc;
+    if (ldw_out) *ldw_out = st;
+    return SBP_OK;
+}
+
+template <class L>
+int linear_bwd(const sbp_view_t *dY, const L *ldy, const sbp_view_t *X, const L *lx,
+               const sbp_view_t *W, const L *lw, sbp_view_t *dX, L *ldx_out, sbp_view_t *dW,
+               L *ldw_out, hipStream_t stream) {
+    if (!dY || !X || !W || !dX || !dW || !ldy || !lx || !lw) return SBP_ERR_NULL;
+    int rc = check_pair(lx, lw);
+    if (rc) return rc;
+    if ((rc = check_pair(ldy, lw))) return rc;
+    // the three input states must describe one signature
+    if (!one_signature(lx, lw, ldy)) return SBP_ERR_SIGNATURE;
+    sbpi::Gemm gd, gw;
+    L sd, sw;
+    if ((rc = prep_bwd_data(dY, ldy, W, lw, dX, &gd, &sd))) return rc;
+    if ((rc = prep_bwd_weight(X, lx, dY, ldy, dW, &gw, &sw))) return rc;
+    // no output may overlap the other output or the input it is not checked
+    // against above (dX vs X, dW vs W)
+    const auto ex = extent(dX->data, dX->rows, dX->cols, dX->ld, dX->dtype);
+    const auto ew = extent(dW->data, dW->rows, dW->cols, dW->ld, dW->dtype);
+    const auto xr = extent(gw.A, gw.k, gw.m, gw.lda, gw.in_dtype);   // X_r: k x m view
+    const auto wr = extent(gd.B, gd.n, gd.k, gd.ldb, gd.in_dtype);   // W_r: n x k view
+    if (overlaps(ex, ew) || overlaps(ex, xr) || overlaps(ew, wr)) return SBP_ERR_ALIAS;
+    if ((rc = run_pair(gd, gw, stream))) return rc;
+    if (ldx_out) *ldx_out = sd;
+    if (ldw_out) *ldw_out = sw;
+    return SBP_OK;
 }
 
 }  // namespace
@@ -373,66 +562,114 @@ int sbp_signature(const sbp_layout_t *x, const sbp_layout_t *w, sbp_layout_t *y,
 int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *W,
                    const sbp_layout_t *lw, sbp_view_t *Y, sbp_layout_t *ly_out,
                    hipStream_t stream) {
-    sbpi::Gemm g;
-    sbp_layout_t st;
-    int rc = prep_fwd(X, lx, W, lw, Y, &g, &st);
-    if (rc) return rc;
-    if ((rc = run(g, stream))) return rc;
-    if (ly_out) *ly_out = st;
-    return SBP_OK;
+    return linear_fwd(X, lx, W, lw, Y, ly_out, stream);
 }
 
 int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *W,
                         const sbp_layout_t *lw, sbp_view_t *dX, sbp_layout_t *ldx_out,
                         hipStream_t stream) {
-    sbpi::Gemm g;
-    sbp_layout_t st;
-    int rc = prep_bwd_data(dY, ldy, W, lw, dX, &g, &st);
-    if (rc) return rc;
-    if ((rc = run(g, stream))) return rc;
-    if (ldx_out) *ldx_out = st;
-    return SBP_OK;
+    return linear_bwd_data(dY, ldy, W, lw, dX, ldx_out, stream);
 }
 
 int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *dY,
                           const sbp_layout_t *ldy, sbp_view_t *dW, sbp_layout_t *ldw_out,
                           hipStream_t stream) {
-    sbpi::Gemm g;
-    sbp_layout_t st;
-    int rc = prep_bwd_weight(X, lx, dY, ldy, dW, &g, &st);
-    if (rc) return rc;
-    if ((rc = run(g, stream))) return rc;
-    if (ldw_out) *ldw_out = st;
-    return SBP_OK;
+    return linear_bwd_weight(X, lx, dY, ldy, dW, ldw_out, stream);
 }
 
 int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *X,
                    const sbp_layout_t *lx, const sbp_view_t *W, const sbp_layout_t *lw,
                    sbp_view_t *dX, sbp_layout_t *ldx_out, sbp_view_t *dW,
                    sbp_layout_t *ldw_out, hipStream_t stream) {
-    if (!dY || !X || !W || !dX || !dW || !ldy || !lx || !lw) return SBP_ERR_NULL;
-    int rc = check_pair(lx, lw);
-    if (rc) return rc;
-    if ((rc = check_pair(ldy, lw))) return rc;
-    // the three input states must describe one signature
-    const Sig s = sig_from_xw(lx, lw);
-    if (s == SIG_NONE || sig_from_dyw(ldy, lw) != s || sig_from_xdy(lx, ldy) != s)
-        return SBP_ERR_SIGNATURE;
-    sbpi::Gemm gd, gw;
-    sbp_layout_t sd, sw;
-    if ((rc = prep_bwd_data(dY, ldy, W, lw, dX, &gd, &sd))) return rc;
-    if ((rc = prep_bwd_weight(X, lx, dY, ldy, dW, &gw, &sw))) return rc;
-    // no output may overlap the other output or the input it is not checked
-    // against above (dX vs X, dW vs W)
-    const auto ex = extent(dX->data, dX->rows, dX->cols, dX->ld, dX->dtype);
-    const auto ew = extent(dW->data, dW->rows, dW->cols, dW->ld, dW->dtype);
-    const auto xr = extent(gw.A, gw.k, gw.m, gw.lda, gw.in_dtype);   // X_r: k x m view
-    const auto wr = extent(gd.B, gd.n, gd.k, gd.ldb, gd.in_dtype);   // W_r: n x k view
-    if (overlaps(ex, ew) || overlaps(ex, xr) || overlaps(ew, wr)) return SBP_ERR_ALIAS;
-    if ((rc = run_pair(gd, gw, stream))) return rc;
-    if (ldx_out) *ldx_out = sd;
-    if (ldw_out) *ldw_out = sw;
+    return linear_bwd(dY, ldy, X, lx, W, lw, dX, ldx_out, dW, ldw_out, stream);
+}
+
+int sbp_mesh_coords(int32_t ndim, const int32_t *nodes, const int32_t *gpus, int64_t node,
+                    int64_t gpu, int32_t *c) {
+    if (!nodes || !c) return SBP_ERR_NULL;
+    if (ndim < 1 || ndim > SBP_MAX_MESH_DIMS) return SBP_ERR_LAYOUT;
+    int64_t n_total = 1, g_total = 1;
+    for (int a = 0; a < ndim; ++a) {
+        const int64_t g = gpus ? gpus[a] : 1;
+        if (nodes[a] < 1 || g < 1) return SBP_ERR_LAYOUT;
+        n_total *= nodes[a];
+        g_total *= g;
+        if (n_total * g_total > INT32_MAX) return SBP_ERR_LAYOUT;   // devices fit int32
+    }
+    if (node < 0 || node >= n_total || gpu < 0 || gpu >= g_total) return SBP_ERR_LAYOUT;
+    // mixed-radix digits, mesh axis 0 fastest, at both levels
+    for (int a = 0; a < ndim; ++a) {
+        const int64_t g = gpus ? gpus[a] : 1;
+        const int64_t nd = node % nodes[a], gd = gpu % g;
+        node /= nodes[a];
+        gpu /= g;
+        c[a] = (int32_t)(nd * g + gd);
+    }
     return SBP_OK;
+}
+
+int sbp_nd_shard_index(const sbp_nd_layout_t *l, int64_t rows, int64_t cols, sbp_shard_t *out) {
+    if (!l || !out) return SBP_ERR_NULL;
+    int rc = check_nd(l);
+    if (rc) return rc;
+    if (rows < 0 || cols < 0) return SBP_ERR_SHAPE;
+    sbp_shard_t s{0, 0, rows, cols};
+    // nested splits in mesh-axis order: each split axis cuts the current
+    // block of its tensor axis (the 1-D balanced rule on the block's extent)
+    for (int a = 0; a < l->ndim; ++a) {
+        if (l->kind[a] != SBP_SPLIT) continue;
+        const sbp_layout_t o = axis_layout(l, a);
+        const bool r0 = (l->axis[a] == 0);
+        sbp_shard_t sub;
+        if ((rc = sbp_shard_index(&o, r0 ? s.rows : 1, r0 ? 1 : s.cols, &sub))) return rc;
+        if (r0) {
+            s.row_off += sub.row_off;
+            s.rows = sub.rows;
+        } else {
+            s.col_off += sub.col_off;
+            s.cols = sub.cols;
+        }
+    }
+    *out = s;
+    return SBP_OK;
+}
+
+int sbp_nd_signature(const sbp_nd_layout_t *x, const sbp_nd_layout_t *w, sbp_nd_layout_t *y,
+                     sbp_nd_layout_t *dy, sbp_nd_layout_t *dx, sbp_nd_layout_t *dw) {
+    if (!x || !w) return SBP_ERR_NULL;
+    sbp_nd_layout_t st[4];
+    int rc = resolve(PAIR_XW, x, w, st);
+    if (rc) return rc;
+    if (y) *y = st[0];
+    if (dy) *dy = st[1];
+    if (dx) *dx = st[2];
+    if (dw) *dw = st[3];
+    return SBP_OK;
+}
+
+int sbp_nd_linear_fwd(const sbp_view_t *X, const sbp_nd_layout_t *lx, const sbp_view_t *W,
+                      const sbp_nd_layout_t *lw, sbp_view_t *Y, sbp_nd_layout_t *ly_out,
+                      hipStream_t stream) {
+    return linear_fwd(X, lx, W, lw, Y, ly_out, stream);
+}
+
+int sbp_nd_linear_bwd_data(const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
+                           const sbp_view_t *W, const sbp_nd_layout_t *lw, sbp_view_t *dX,
+                           sbp_nd_layout_t *ldx_out, hipStream_t stream) {
+    return linear_bwd_data(dY, ldy, W, lw, dX, ldx_out, stream);
+}
+
+int sbp_nd_linear_bwd_weight(const sbp_view_t *X, const sbp_nd_layout_t *lx,
+                             const sbp_view_t *dY, const sbp_nd_layout_t *ldy, sbp_view_t *dW,
+                             sbp_nd_layout_t *ldw_out, hipStream_t stream) {
+    return linear_bwd_weight(X, lx, dY, ldy, dW, ldw_out, stream);
+}
+
+int sbp_nd_linear_bwd(const sbp_view_t *dY, const sbp_nd_layout_t *ldy, const sbp_view_t *X,
+                      const sbp_nd_layout_t *lx, const sbp_view_t *W, const sbp_nd_layout_t *lw,
+                      sbp_view_t *dX, sbp_nd_layout_t *ldx_out, sbp_view_t *dW,
+                      sbp_nd_layout_t *ldw_out, hipStream_t stream) {
+    return linear_bwd(dY, ldy, X, lx, W, lw, dX, ldx_out, dW, ldw_out, stream);
 }
 
 const char *sbp_strerror(int code) {

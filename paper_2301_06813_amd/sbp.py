@@ -35,7 +35,11 @@ SBP_GLOBAL, SBP_LOCAL = 0, 1
 EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd_data",
            "sbp_linear_bwd_weight", "sbp_linear_bwd", "sbp_strerror", "sbp_last_hip_error", "sbp_plan",
            "sbp_plan_bwd", "sbp_set_plan_override", "sbp_set_bwd_override", "sbp_profile_begin",
-           "sbp_profile_end")
+           "sbp_profile_end", "sbp_mesh_coords", "sbp_nd_shard_index", "sbp_nd_signature",
+           "sbp_nd_linear_fwd", "sbp_nd_linear_bwd_data", "sbp_nd_linear_bwd_weight",
+           "sbp_nd_linear_bwd")
+
+SBP_MAX_MESH_DIMS = 4
 
 
 class sbp_layout_t(ctypes.Structure):
@@ -49,6 +53,30 @@ class sbp_layout_t(ctypes.Structure):
 
     def key(self):
         return (self.kind, self.axis, self.p, self.r)
+
+
+class sbp_nd_layout_t(ctypes.Structure):
+    _fields_ = [("ndim", ctypes.c_int32), ("kind", ctypes.c_int32 * 4),
+                ("axis", ctypes.c_int32 * 4), ("p", ctypes.c_int32 * 4),
+                ("c", ctypes.c_int32 * 4)]
+
+    def __repr__(self):
+        parts = []
+        for a in range(self.ndim):
+            k = self.kind[a]
+            name = {SBP_SPLIT: "S(%d)" % self.axis[a], SBP_BROADCAST: "B",
+                    SBP_PARTIAL: "P"}.get(k, "?%d" % k)
+            parts.append("%s:%d@%d" % (name, self.p[a], self.c[a]))
+        return "(" + ", ".join(parts) + ")"
+
+    def key(self):
+        n = self.ndim
+        return (n, tuple(self.kind[:n]), tuple(self.axis[:n]), tuple(self.p[:n]),
+                tuple(self.c[:n]))
+
+    def states(self):
+        """Per mesh axis (kind, axis)."""
+        return [(self.kind[a], self.axis[a]) for a in range(self.ndim)]
 
 
 class sbp_view_t(ctypes.Structure):
@@ -81,6 +109,22 @@ def broadcast(p: int, r: int) -> sbp_layout_t:
 
 def partial(p: int, r: int) -> sbp_layout_t:
     return sbp_layout_t(SBP_PARTIAL, -1, p, r)
+
+
+def nd_layout(states, mesh, coord) -> sbp_nd_layout_t:
+    """sbp_nd_layout_t from per-mesh-axis states ("S0", "S1", "B", "P" or
+    (kind, axis) pairs), mesh extents and this device's mesh coordinate."""
+    n = len(mesh)
+    if not (1 <= n <= SBP_MAX_MESH_DIMS) or len(states) != n or len(coord) != n:
+        raise ValueError("states, mesh and coord need one entry per mesh axis (1..4)")
+    names = {"S0": (SBP_SPLIT, 0), "S1": (SBP_SPLIT, 1), "B": (SBP_BROADCAST, -1),
+             "P": (SBP_PARTIAL, -1)}
+    l = sbp_nd_layout_t()
+    l.ndim = n
+    for a, st in enumerate(states):
+        k, ax = names[st] if isinstance(st, str) else st
+        l.kind[a], l.axis[a], l.p[a], l.c[a] = k, ax, mesh[a], coord[a]
+    return l
 
 
 _lib = None
@@ -117,6 +161,16 @@ def lib():
         L.sbp_profile_end.argtypes = [ctypes.c_void_p, ctypes.c_char_p, ctypes.c_int]
         L.sbp_plan_bwd.argtypes = ([ctypes.c_int64] * 3 + [ctypes.c_int32] + [ctypes.c_int64] * 3 +
                                    [ctypes.c_int32] + [P(ctypes.c_int32)] * 5)
+        ND = P(sbp_nd_layout_t)
+        L.sbp_mesh_coords.argtypes = [ctypes.c_int32, P(ctypes.c_int32), P(ctypes.c_int32),
+                                      ctypes.c_int64, ctypes.c_int64, P(ctypes.c_int32)]
+        L.sbp_nd_shard_index.argtypes = [ND, ctypes.c_int64, ctypes.c_int64, P(sbp_shard_t)]
+        L.sbp_nd_signature.argtypes = [ND] * 6
+        for fn in ("sbp_nd_linear_fwd", "sbp_nd_linear_bwd_data", "sbp_nd_linear_bwd_weight"):
+            getattr(L, fn).argtypes = [P(sbp_view_t), ND, P(sbp_view_t), ND, P(sbp_view_t), ND,
+                                       ctypes.c_void_p]
+        L.sbp_nd_linear_bwd.argtypes = [P(sbp_view_t), ND, P(sbp_view_t), ND, P(sbp_view_t), ND,
+                                        P(sbp_view_t), ND, P(sbp_view_t), ND, ctypes.c_void_p]
         for fn in EXPORTS:
             if fn != "sbp_strerror":
                 getattr(L, fn).restype = ctypes.c_int
@@ -173,7 +227,7 @@ def sbp_signature(x: sbp_layout_t, w: sbp_layout_t):
 
 
 def _compute(fn, a, la, b, lb, out, stream):
-    lo = sbp_layout_t()
+    lo = type(la)()
     s = current_stream() if stream is None else stream
     _check(getattr(lib(), fn)(ctypes.byref(a), ctypes.byref(la), ctypes.byref(b),
                               ctypes.byref(lb), ctypes.byref(out), ctypes.byref(lo),
@@ -209,6 +263,58 @@ def sbp_linear_bwd(dY: sbp_view_t, ldy: sbp_layout_t, X: sbp_view_t, lx: sbp_lay
                                 ctypes.byref(lx), ctypes.byref(W), ctypes.byref(lw),
                                 ctypes.byref(dX), ctypes.byref(sx), ctypes.byref(dW),
                                 ctypes.byref(sw), ctypes.c_void_p(s)))
+    return sx, sw
+
+
+# ------------------------------------------------------------------ nd-SBP
+def sbp_mesh_coords(nodes, gpus=None, node: int = 0, gpu: int = 0) -> list[int]:
+    """Mesh coordinate of device (node, gpu) on a mesh whose axis a spans
+    nodes[a] x gpus[a] devices (gpus None: a single-level mesh, node = rank)."""
+    n = len(nodes)
+    arr = ctypes.c_int32 * max(n, 1)
+    c = arr()
+    g = None if gpus is None else arr(*gpus)
+    _check(lib().sbp_mesh_coords(n, arr(*nodes), g, node, gpu, c))
+    return list(c[:n])
+
+
+def sbp_nd_shard_index(layout: sbp_nd_layout_t, rows: int, cols: int) -> sbp_shard_t:
+    out = sbp_shard_t()
+    _check(lib().sbp_nd_shard_index(ctypes.byref(layout), rows, cols, ctypes.byref(out)))
+    return out
+
+
+def sbp_nd_signature(x: sbp_nd_layout_t, w: sbp_nd_layout_t):
+    """(Y, dY, dX, dW) nd states for X in state x and W in state w."""
+    outs = [sbp_nd_layout_t() for _ in range(4)]
+    _check(lib().sbp_nd_signature(ctypes.byref(x), ctypes.byref(w),
+                                  *(ctypes.byref(o) for o in outs)))
+    return tuple(outs)
+
+
+def sbp_nd_linear_fwd(X, lx: sbp_nd_layout_t, W, lw: sbp_nd_layout_t, Y, stream=None):
+    """Y_r = X_r W_r on nd shares; returns Y's nd state."""
+    return _compute("sbp_nd_linear_fwd", X, lx, W, lw, Y, stream)
+
+
+def sbp_nd_linear_bwd_data(dY, ldy: sbp_nd_layout_t, W, lw: sbp_nd_layout_t, dX, stream=None):
+    """dX_r = dY_r W_r^T on nd shares; returns dX's nd state."""
+    return _compute("sbp_nd_linear_bwd_data", dY, ldy, W, lw, dX, stream)
+
+
+def sbp_nd_linear_bwd_weight(X, lx: sbp_nd_layout_t, dY, ldy: sbp_nd_layout_t, dW, stream=None):
+    """dW_r = X_r^T dY_r on nd shares; returns dW's nd state."""
+    return _compute("sbp_nd_linear_bwd_weight", X, lx, dY, ldy, dW, stream)
+
+
+def sbp_nd_linear_bwd(dY, ldy, X, lx, W, lw, dX, dW, stream=None):
+    """Both backward products on nd shares in one call; returns (dX state, dW state)."""
+    sx, sw = sbp_nd_layout_t(), sbp_nd_layout_t()
+    s = current_stream() if stream is None else stream
+    _check(lib().sbp_nd_linear_bwd(ctypes.byref(dY), ctypes.byref(ldy), ctypes.byref(X),
+                                   ctypes.byref(lx), ctypes.byref(W), ctypes.byref(lw),
+                                   ctypes.byref(dX), ctypes.byref(sx), ctypes.byref(dW),
+                                   ctypes.byref(sw), ctypes.c_void_p(s)))
     return sx, sw
 
 

@@ -45,32 +45,32 @@ def product_cases(wl_ids):
     import torch
     from . import linear, sbp, workloads
     wls = {2: workloads.ffn_shard, 3: workloads.attention_dp, 4: workloads.vgg_head,
-           5: workloads.transformer_step}
+           5: workloads.transformer_step, 6: workloads.transformer_3d}
     cases = {}
     for c in wl_ids:
         wl = wls[c]()
         for lin in wl.linears:
             for r in wl.ranks:
-                L = linear.layouts(lin.sig, wl.p, r)
+                L = linear.layouts_for(lin, wl, r)
                 for op in ("fwd", "bwd_data", "bwd_weight"):
                     rows, cols = linear.out_shape(op, L, lin.M, lin.K, lin.N)
-                    k = {"fwd": sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols,
-                         "bwd_data": sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols,
-                         "bwd_weight": sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows}[op]
+                    k = {"fwd": linear.shard(L["x"], lin.M, lin.K).cols,
+                         "bwd_data": linear.shard(L["dy"], lin.M, lin.N).cols,
+                         "bwd_weight": linear.shard(L["x"], lin.M, lin.K).rows}[op]
                     f32 = linear.out_dtype(op, L, wl.dtype) == torch.float32
-                    key = (ORIENT[op], int(f32), rows, cols, k, _eligible(op, L, lin, wl.p))
+                    key = (ORIENT[op], int(f32), rows, cols, k, _eligible(op, L, lin))
                     cases.setdefault(key, (wl, lin, op, r))
     return cases
 
 
-def _eligible(op, L, lin, p):
+def _eligible(op, L, lin):
     """Whether the pipelined kernel can read rank r's operand views: 16-byte
     aligned shard offsets, and leading dimensions and contiguous extents (the
     columns of a row-major share) that are multiples of 8 elements."""
-    from . import sbp
+    from . import linear
 
     def ok(layout, rows, cols):
-        s = sbp.sbp_shard_index(layout, rows, cols)
+        s = linear.shard(layout, rows, cols)
         return (s.row_off * cols + s.col_off) % 8 == 0 and cols % 8 == 0 and s.cols % 8 == 0
 
     M, K, N = lin.M, lin.K, lin.N
@@ -154,17 +154,17 @@ def bwd_pairs(wl_ids):
     pairs = {}
     for c in wl_ids:
         wl = {2: workloads.ffn_shard, 3: workloads.attention_dp, 4: workloads.vgg_head,
-              5: workloads.transformer_step}[c]()
+              5: workloads.transformer_step, 6: workloads.transformer_3d}[c]()
         for lin in wl.linears:
             for r in wl.ranks:
-                L = linear.layouts(lin.sig, wl.p, r)
+                L = linear.layouts_for(lin, wl, r)
                 keys = []
                 for op in ("bwd_data", "bwd_weight"):
                     rows, cols = linear.out_shape(op, L, lin.M, lin.K, lin.N)
-                    k = (sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols if op == "bwd_data"
-                         else sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows)
+                    k = (linear.shard(L["dy"], lin.M, lin.N).cols if op == "bwd_data"
+                         else linear.shard(L["x"], lin.M, lin.K).rows)
                     f32 = linear.out_dtype(op, L, wl.dtype) == torch.float32
-                    keys.append((ORIENT[op], int(f32), rows, cols, k, _eligible(op, L, lin, wl.p)))
+                    keys.append((ORIENT[op], int(f32), rows, cols, k, _eligible(op, L, lin)))
                 if keys[0][5] and keys[1][5]:
                     pairs.setdefault(tuple(keys), (wl, lin, r))
     return pairs
@@ -183,16 +183,16 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream, single_best=None):
         sets = []
         for i in range(nsets):
             X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
-            dX = linear.alloc_out("bwd_data", lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype, "cuda")
-            dW = linear.alloc_out("bwd_weight", lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype,
-                                  "cuda")
+            Lr = linear.layouts_for(lin, wl, r)
+            dX = linear.alloc_out_L("bwd_data", Lr, lin.M, lin.K, lin.N, wl.dtype, "cuda")
+            dW = linear.alloc_out_L("bwd_weight", Lr, lin.M, lin.K, lin.N, wl.dtype, "cuda")
             sets.append((X, W, dY, dX, dW))
         it = [0]
 
         def fn():
             X, W, dY, dX, dW = sets[it[0] % nsets]
             it[0] += 1
-            linear.run_bwd(lin.sig, wl.p, r, X, W, dY, dX, dW, stream.cuda_stream)
+            linear.run_bwd_L(Lr, X, W, dY, dX, dW, stream.cuda_stream)
 
         def timed(plan, mode, sw):
             sbp.sbp_set_plan_override(*plan)
@@ -267,7 +267,7 @@ def pick(timings, retime, top=5, rounds=3):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--out", default=None)
-    ap.add_argument("--workloads", default="2,3,4,5")
+    ap.add_argument("--workloads", default="2,3,4,5,6")
     ap.add_argument("--reps", type=int, default=10)
     ap.add_argument("--bwd", action="store_true", help="tune grouped backward pairs only")
     ap.add_argument("--all", action="store_true",
@@ -298,14 +298,15 @@ def main():
         sets = []
         for i in range(nsets):
             X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
-            out = linear.alloc_out(op, lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype, "cuda")
+            Lr = linear.layouts_for(lin, wl, r)
+            out = linear.alloc_out_L(op, Lr, lin.M, lin.K, lin.N, wl.dtype, "cuda")
             sets.append((X, W, dY, out))
         it = [0]
 
         def fn():
             X, W, dY, out = sets[it[0] % nsets]
             it[0] += 1
-            linear.run(op, lin.sig, wl.p, r, X, W, dY, out, stream.cuda_stream)
+            linear.run_L(op, Lr, X, W, dY, out, stream.cuda_stream)
 
         cands = valid_candidates(sbp, key, None)
         timings = []

@@ -1,4 +1,4 @@
-"""The five workloads: shapes, SBP signatures, seeds and value distributions.
+"""The workloads: shapes, SBP signatures, seeds and value distributions.
 
 Each workload is a list of linear layers ``Y = X W`` with global
 X (M x K), W (K x N) and upstream gradient dY (M x N), a device count p and
@@ -9,6 +9,10 @@ Signatures (1-D factors of the 3-D SBP matmul rule of Sec. 4.2):
     "DP"  (S(0), B)    -> S(0)   data parallel
     "COL" (B,    S(1)) -> S(1)   column split of W
     "KS"  (S(1), S(0)) -> P      split of the reduction dimension
+
+Workload 6 runs on a 2 x 2 x 2 device mesh: each linear carries one factor
+per mesh axis (nd-SBP, Sec. 4.1 Listing 1 and the 3-D rule of Sec. 4.2),
+and its "ranks" are mesh coordinates.
 
 Seeds: tensor t of linear l in workload c uses ``1000*c + 10*l + t`` with
 t = 1 (X), 2 (W), 3 (dY); workload 5 draws its signatures from seed 5000.
@@ -43,6 +47,7 @@ class Linear:
     x_relu: bool = False
     w_gain: float = 1.0   # W ~ N(0, w_gain / K)
     dy_std: float = 1.0
+    factors: tuple = ()   # nd workloads: one of "DP", "COL", "KS", "BB" per mesh axis
 
     @property
     def w_std(self) -> float:
@@ -60,7 +65,8 @@ class Workload:
     dtype: torch.dtype
     p: int
     linears: tuple
-    ranks: tuple          # ranks that parity covers
+    ranks: tuple          # ranks (nd workloads: mesh coordinates) that parity covers
+    mesh: tuple = ()      # nd workloads: devices per mesh axis (p = their product)
 
 
 def tiny_fp32() -> list[Workload]:
@@ -114,8 +120,26 @@ def transformer_step(layers: int = 24) -> Workload:
     return Workload(5, "transformer_24L_step_rank0_p8", torch.bfloat16, 8, tuple(lins), (0,))
 
 
+def transformer_3d() -> Workload:
+    """Workload 6: the four linears of one Transformer layer (8192 tokens,
+    hidden 1024, ffn 4096) on a 2 x 2 x 2 mesh of 8 devices, each under the
+    3-D rule of Sec. 4.2: X (S0, B, S1), W (B, S1, S0) -> Y (S0, S1, P), so
+    every device multiplies a (M/2) x (K/2) share of X by a (K/2) x (N/2)
+    share of W (the paper prefers a 3-D strategy for attention layers,
+    Sec. 4.5). Parity covers all eight devices; the benchmark reports device
+    (0, 0, 0)."""
+    mesh = (2, 2, 2)
+    f3 = ("DP", "COL", "KS")
+    dims = (("qkv", 1024, 3072), ("out", 1024, 1024), ("fc1", 1024, 4096), ("fc2", 4096, 1024))
+    lins = tuple(Linear(nm, 8192, k, n, "3D", 6000 + 10 * i, factors=f3)
+                 for i, (nm, k, n) in enumerate(dims))
+    coords = tuple((a, b, c) for a in range(2) for b in range(2) for c in range(2))
+    return Workload(6, "transformer_layer_3d_mesh2x2x2", torch.bfloat16, 8, lins, coords, mesh)
+
+
 def all_workloads() -> list[Workload]:
-    return tiny_fp32() + [ffn_shard(), attention_dp(), vgg_head(), transformer_step()]
+    return tiny_fp32() + [ffn_shard(), attention_dp(), vgg_head(), transformer_step(),
+                          transformer_3d()]
 
 
 def make_tensors(lin: Linear, dtype, device="cpu"):

@@ -1,0 +1,165 @@
+"""GPU parity of the nd-SBP entry points (device meshes, one SBP state per
+mesh axis) with the oracle's independent nd code.
+
+* bit-exact on integer inputs in [-3, 3] (every partial sum is an exact fp32
+  integer): several meshes and per-axis factor lists, every device of the
+  mesh, the three products and the two-product backward call, global and
+  local operand views;
+* the mesh reassembly invariant through the kernels: the eight devices'
+  outputs of the 3-D rule, placed at their shares and summed over the
+  Partial-sum axis, equal the exact global product;
+* workload 6 (a Transformer layer under the 3-D rule on a 2 x 2 x 2 mesh) at
+  full size, every device, on sampled outputs, normwise <= 2e-2 (bf16).
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2301_06813_amd import inputs, linear, sbp, workloads
+
+from helpers import decode, normwise_rel, out_bits, say
+
+pytestmark = pytest.mark.gpu
+OPS = ("fwd", "bwd_data", "bwd_weight")
+OP_ID = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
+S0, S1, B = (oracle.SPLIT, 0), (oracle.SPLIT, 1), (oracle.BCAST, -1)
+ORC_FACTOR = {"DP": (S0, B), "COL": (B, S1), "KS": (S1, S0), "BB": (B, B)}
+TO_ABI = {oracle.SPLIT: sbp.SBP_SPLIT, oracle.BCAST: sbp.SBP_BROADCAST,
+          oracle.PARTIAL: sbp.SBP_PARTIAL}
+TOL_BF16 = 2e-2
+
+
+def _orc_states(factors):
+    return [ORC_FACTOR[f][0] for f in factors], [ORC_FACTOR[f][1] for f in factors]
+
+
+def _coords(mesh):
+    return list(itertools.product(*(range(p) for p in mesh)))
+
+
+def _int_inputs(M, K, N, seed):
+    X = inputs.randint((M, K), -3, 3, seed + 1, torch.bfloat16, "cuda")
+    W = inputs.randint((K, N), -3, 3, seed + 2, torch.bfloat16, "cuda")
+    dY = inputs.randint((M, N), -3, 3, seed + 3, torch.bfloat16, "cuda")
+    return X, W, dY
+
+
+def _expect(op, factors, mesh, c, st, M, K, N):
+    xs, ws = _orc_states(factors)
+    _, _, want = oracle.nd_out_shape(OP_ID[op], M, K, N, xs, ws, mesh, c)
+    assert [(TO_ABI[k], a) for k, a in want] == st.states(), (op, factors, c, st)
+    assert list(st.p[:len(mesh)]) == list(mesh) and tuple(st.c[:len(mesh)]) == tuple(c)
+
+
+def _exact(out, want):
+    if out.dtype == torch.bfloat16:
+        return np.array_equal(out_bits(out), oracle.round_bf16(want))
+    return np.array_equal(decode(out), want)
+
+
+MESHES = [((2, 2, 2), ("DP", "COL", "KS")), ((3, 2), ("KS", "COL")), ((2, 3), ("DP", "DP")),
+          ((2, 2), ("KS", "KS")), ((2, 3), ("COL", "BB")), ((2, 1, 3), ("BB", "DP", "COL"))]
+
+
+@pytest.mark.parametrize("mesh,factors", MESHES,
+                         ids=["%s-%s" % ("x".join(map(str, m)), "+".join(f)) for m, f in MESHES])
+def test_nd_exact_every_device(mesh, factors):
+    # ragged sizes: no share is a multiple of a tile
+    M, K, N = 304, 1112, 280
+    X, W, dY = _int_inputs(M, K, N, 700)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    xs, ws = _orc_states(factors)
+    for c in _coords(mesh):
+        for op in OPS:
+            say("nd exact", mesh, factors, c, op)
+            out, st = linear.call_nd(op, factors, mesh, c, X, W, dY)
+            torch.cuda.synchronize()
+            _expect(op, factors, mesh, c, st, M, K, N)
+            want = oracle.nd_linear(OP_ID[op], Xh, Wh, dYh, xs, ws, mesh, c)
+            assert out.shape == want.shape, (op, c, out.shape, want.shape)
+            assert _exact(out, want), (mesh, factors, c, op)
+        say("nd exact bwd pair", mesh, factors, c)
+        dX, dW, (sx, sw) = linear.call_bwd_nd(factors, mesh, c, X, W, dY)
+        torch.cuda.synchronize()
+        _expect("bwd_data", factors, mesh, c, sx, M, K, N)
+        _expect("bwd_weight", factors, mesh, c, sw, M, K, N)
+        assert _exact(dX, oracle.nd_linear(oracle.BWD_DATA, Xh, Wh, dYh, xs, ws, mesh, c))
+        assert _exact(dW, oracle.nd_linear(oracle.BWD_WEIGHT, Xh, Wh, dYh, xs, ws, mesh, c))
+
+
+def test_nd_reassembly_through_kernels():
+    M, K, N = 200, 328, 136
+    mesh, factors = (2, 2, 2), ("DP", "COL", "KS")
+    X, W, dY = _int_inputs(M, K, N, 800)
+    Xi, Wi, dYi = (oracle.bf16_to_f64(inputs.host_bits(t)) for t in (X, W, dY))
+    glob = {"fwd": Xi @ Wi, "bwd_data": dYi @ Wi.T, "bwd_weight": Xi.T @ dYi}
+    for op in OPS:
+        grow, gcol = glob[op].shape
+        total = np.zeros((grow, gcol))
+        for c in _coords(mesh):
+            say("nd reassembly", op, c)
+            out, st = linear.call_nd(op, factors, mesh, c, X, W, dY)
+            torch.cuda.synchronize()
+            s = sbp.sbp_nd_shard_index(st, grow, gcol)
+            total[s.row_off:s.row_off + s.rows, s.col_off:s.col_off + s.cols] += decode(out)
+        # every output of the 3-D rule is Partial-sum on exactly one mesh axis
+        assert np.array_equal(total, glob[op]), op
+
+
+def test_nd_local_views_equal_global():
+    M, K, N = 264, 520, 200
+    mesh, factors, c = (2, 2, 2), ("DP", "COL", "KS"), (1, 0, 1)
+    X, W, dY = _int_inputs(M, K, N, 900)
+    L = linear.nd_layouts(factors, mesh, c)
+
+    def local(t, l, pad):
+        s = sbp.sbp_nd_shard_index(l, *t.shape)
+        buf = torch.zeros((s.rows, s.cols + pad), dtype=t.dtype, device="cuda")
+        buf[:, :s.cols] = t[s.row_off:s.row_off + s.rows, s.col_off:s.col_off + s.cols]
+        return buf[:, :s.cols]
+
+    Xl, Wl, dYl = local(X, L["x"], 24), local(W, L["w"], 8), local(dY, L["dy"], 40)
+    for op in OPS:
+        say("nd local views", op)
+        ref, _ = linear.call_nd(op, factors, mesh, c, X, W, dY)
+        out = torch.empty_like(ref)
+        v = lambda t: sbp.view(t, sbp.SBP_LOCAL)
+        o = sbp.view(out, sbp.SBP_LOCAL)
+        if op == "fwd":
+            sbp.sbp_nd_linear_fwd(v(Xl), L["x"], v(Wl), L["w"], o)
+        elif op == "bwd_data":
+            sbp.sbp_nd_linear_bwd_data(v(dYl), L["dy"], v(Wl), L["w"], o)
+        else:
+            sbp.sbp_nd_linear_bwd_weight(v(Xl), L["x"], v(dYl), L["dy"], o)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), op
+
+
+def test_workload6_full_size_sampled():
+    wl = workloads.transformer_3d()
+    rng = np.random.default_rng(6)
+    for lin in wl.linears:
+        X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
+        Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+        xs, ws = _orc_states(lin.factors)
+        for c in wl.ranks:
+            for op in OPS:
+                say(wl.name, lin.name, op, c)
+                out, st = linear.call_nd(op, lin.factors, wl.mesh, c, X, W, dY)
+                torch.cuda.synchronize()
+                _expect(op, lin.factors, wl.mesh, c, st, lin.M, lin.K, lin.N)
+                rows, cols = out.shape
+                ii = rng.integers(0, rows, 600)
+                jj = rng.integers(0, cols, 600)
+                ii[:4] = [0, 0, rows - 1, rows - 1]
+                jj[:4] = [0, cols - 1, 0, cols - 1]
+                got = decode(out[torch.as_tensor(ii, device="cuda"),
+                                 torch.as_tensor(jj, device="cuda")])
+                want = oracle.nd_linear_samples(OP_ID[op], Xh, Wh, dYh, xs, ws, wl.mesh, c, ii, jj)
+                rel = normwise_rel(got, want)
+                assert rel <= TOL_BF16, (lin.name, op, c, rel)
+                del out
+        del X, W, dY
