@@ -6,8 +6,9 @@
 // 0, 1, ..., S-1 -- the same order whatever the schedule, so results are
 // deterministic -- and writes the output as fp32, or as bf16 rounded to
 // nearest even. Each thread owns 4 consecutive columns of one row: 16-byte
-// loads of every slice when n is a multiple of 4, and stores that are
-// contiguous across the threads of a wave.
+// loads of every slice when n is a multiple of 4, and one vector store (or
+// element stores at a ragged edge or an unaligned output) that is contiguous
+// across the threads of a wave.
 #include "gemm.h"
 #include "profile.h"
 
@@ -17,28 +18,53 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 // Sums the S slices of one product's 4-column group gidx (row gidx /
 // groups_per_row) in split order and stores it; out-of-range ids do nothing.
+// The slices' loads are issued four at a time before they are added (still
+// in split order), so a thread waits for one memory latency per four slices
+// rather than per slice. vec: C's base and ldc allow one 16-byte (fp32) or
+// 8-byte (bf16) store per group.
 template <bool OUT_F32>
 __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int S, void *C,
-                                             int64_t ldc, int64_t gidx) {
+                                             int64_t ldc, bool vec, int64_t gidx) {
     const int groups_per_row = (n + 3) / 4;
     if (gidx >= (int64_t)m * groups_per_row) return;
     const int row = (int)(gidx / groups_per_row);
     const int col = (int)(gidx % groups_per_row) * 4;
     const size_t slice = (size_t)m * (size_t)n;
     const float *p = ws + (size_t)row * n + col;
-    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    f32x4v v = {0.f, 0.f, 0.f, 0.f};
     if ((n & 3) == 0) {
-        for (int s = 0; s < S; ++s) {
-            const f32x4v x = __builtin_nontemporal_load(reinterpret_cast<const f32x4v *>(p + s * slice));
-            v[0] += x[0];
-            v[1] += x[1];
-            v[2] += x[2];
-            v[3] += x[3];
+        auto ld = [&](int s) {
+            return __builtin_nontemporal_load(reinterpret_cast<const f32x4v *>(p + s * slice));
+        };
+        int s = 0;
+        for (; s + 4 <= S; s += 4) {
+            const f32x4v x0 = ld(s), x1 = ld(s + 1), x2 = ld(s + 2), x3 = ld(s + 3);
+            v += x0;
+            v += x1;
+            v += x2;
+            v += x3;
         }
+        for (; s < S; ++s) v += ld(s);
     } else {
         for (int s = 0; s < S; ++s)
             for (int e = 0; e < 4; ++e)
                 if (col + e < n) v[e] += p[s * slice + e];
+    }
+    if (vec && col + 4 <= n) {
+        if constexpr (OUT_F32) {
+            *reinterpret_cast<f32x4v *>(reinterpret_cast<float *>(C) + (int64_t)row * ldc + col) =
+                v;
+        } else {
+            typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+            u32x2v w;
+            w[0] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[0]) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[1]) << 16);
+            w[1] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2]) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[3]) << 16);
+            *reinterpret_cast<u32x2v *>(reinterpret_cast<uint16_t *>(C) + (int64_t)row * ldc +
+                                        col) = w;
+        }
+        return;
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -55,8 +81,9 @@ __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int 
 
 template <bool OUT_F32>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float *ws, int m, int n, int S,
-                                                           void *C, int64_t ldc) {
-    reduce_group<OUT_F32>(ws, m, n, S, C, ldc, (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+                                                           void *C, int64_t ldc, int vec) {
+    reduce_group<OUT_F32>(ws, m, n, S, C, ldc, vec != 0,
+                          (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
 }
 
 // The split reductions of the two backward products of one linear in one
@@ -67,6 +94,7 @@ struct ReduceJob {
     int m, n, S;
     void *C;
     int64_t ldc;
+    int vec;
 };
 
 template <bool OD, bool OW>
@@ -74,9 +102,10 @@ __global__ __launch_bounds__(256) void split_reduce_pair_kernel(ReduceJob d, Red
                                                                 int blocks_d) {
     const int b = blockIdx.x;
     if (b < blocks_d)
-        reduce_group<OD>(d.ws, d.m, d.n, d.S, d.C, d.ldc, (int64_t)b * blockDim.x + threadIdx.x);
+        reduce_group<OD>(d.ws, d.m, d.n, d.S, d.C, d.ldc, d.vec != 0,
+                         (int64_t)b * blockDim.x + threadIdx.x);
     else
-        reduce_group<OW>(w.ws, w.m, w.n, w.S, w.C, w.ldc,
+        reduce_group<OW>(w.ws, w.m, w.n, w.S, w.C, w.ldc, w.vec != 0,
                          (int64_t)(b - blocks_d) * blockDim.x + threadIdx.x);
 }
 
@@ -84,15 +113,25 @@ __global__ __launch_bounds__(256) void split_reduce_pair_kernel(ReduceJob d, Red
 
 namespace sbpi {
 
+// Whether every 4-column group of C can be stored with one aligned vector
+// store: 16 bytes for fp32, 8 for bf16.
+static int reduce_vec(const Gemm &g) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(g.C);
+    const uintptr_t align = g.out_dtype == DT_F32 ? 16 : 8;
+    return (a % align == 0 && g.ldc % 4 == 0) ? 1 : 0;
+}
+
 hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipStream_t s) {
     const int64_t groups = g.m * ((g.n + 3) / 4);
     const unsigned blocks = (unsigned)((groups + 255) / 256);
+    const int vec = reduce_vec(g);
     if (g.out_dtype == DT_F32)
         return launch_kernel(sbpk::split_reduce_kernel<true>, "split_reduce_kernel<true>",
                              dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C,
-                             g.ldc);
+                             g.ldc, vec);
     return launch_kernel(sbpk::split_reduce_kernel<false>, "split_reduce_kernel<false>",
-                         dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C, g.ldc);
+                         dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C, g.ldc,
+                         vec);
 }
 
 static unsigned reduce_blocks(const Gemm &g) {
@@ -102,8 +141,8 @@ static unsigned reduce_blocks(const Gemm &g) {
 
 hipError_t launch_split_reduce_pair(const Gemm &gd, int sd, const float *wsd, const Gemm &gw,
                                     int sw, const float *wsw, hipStream_t s) {
-    const sbpk::ReduceJob d{wsd, (int)gd.m, (int)gd.n, sd, gd.C, gd.ldc};
-    const sbpk::ReduceJob w{wsw, (int)gw.m, (int)gw.n, sw, gw.C, gw.ldc};
+    const sbpk::ReduceJob d{wsd, (int)gd.m, (int)gd.n, sd, gd.C, gd.ldc, reduce_vec(gd)};
+    const sbpk::ReduceJob w{wsw, (int)gw.m, (int)gw.n, sw, gw.C, gw.ldc, reduce_vec(gw)};
     const unsigned bd = reduce_blocks(gd), bw = reduce_blocks(gw);
     const bool od = gd.out_dtype == DT_F32, ow = gw.out_dtype == DT_F32;
 #define SBP_PAIR(OD_, OW_, NAME)                                                             \
