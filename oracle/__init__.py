@@ -31,8 +31,8 @@ SRC = os.path.join(HERE, "oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
 # signature ids (the oracle's own numbering)
-DP, COL, KS = 0, 1, 2
-SIGNATURES = {"DP": DP, "COL": COL, "KS": KS}
+DP, COL, KS, PB, BP, BB = 0, 1, 2, 3, 4, 5
+SIGNATURES = {"DP": DP, "COL": COL, "KS": KS, "PB": PB, "BP": BP, "BB": BB}
 # operation ids
 FWD, BWD_DATA, BWD_WEIGHT = 0, 1, 2
 OPS = {"fwd": FWD, "bwd_data": BWD_DATA, "bwd_weight": BWD_WEIGHT}

@@ -22,6 +22,12 @@
  *       column          (B,    S(1)) -> S(1)      [p0 = p2 = 1 case]
  *       K-split         (S(1), S(0)) -> P         [p0 = p1 = 1 case]
  *   and each device multiplies its local shares ("local matmul").
+ *   By linearity three more signatures need no split at all:
+ *       partial input   (P, B) -> P    and    (B, P) -> P
+ *       replicated      (B, B) -> B
+ *   (a product is linear in each operand, so partial sums of one operand
+ *   give partial sums of the product; two replicated operands give a
+ *   replicated product).
  *
  *   Backward: dX = dY W^T and dW = X^T dY on the same local shares. A
  *   broadcast operand's gradient is a partial sum (Sec. 4.3: a replicated
@@ -49,7 +55,7 @@
 
 /* ----------------------------------------------------------------- ids --- */
 /* signatures */
-enum { ORC_DP = 0, ORC_COL = 1, ORC_KS = 2 };
+enum { ORC_DP = 0, ORC_COL = 1, ORC_KS = 2, ORC_PB = 3, ORC_BP = 4, ORC_BB = 5 };
 /* operations */
 enum { ORC_FWD = 0, ORC_BWD_DATA = 1, ORC_BWD_WEIGHT = 2 };
 /* tensor state kinds */
@@ -76,22 +82,30 @@ void orc_split(int64_t D, int64_t p, int64_t r, int64_t *off, int64_t *len)
 /*
  * For signature sig, writes the (kind, axis) state of the six tensors in the
  * order X, W, Y, dY, dX, dW. Axis is -1 for Broadcast and Partial-sum.
+ * The gradient of a Split(i) tensor is Split(i), of a Broadcast tensor a
+ * Partial-sum (Sec. 4.3), of a Partial-sum tensor a Broadcast.
  * Returns 0, or -1 for an unknown signature.
  */
 int orc_tags(int sig, int32_t kinds[6], int32_t axes[6])
 {
-    /*                 X          W          Y            dY         dX           dW        */
-    static const int32_t K[3][6] = {
-        {ORC_SPLIT, ORC_BCAST, ORC_SPLIT,   ORC_SPLIT, ORC_SPLIT,   ORC_PARTIAL}, /* DP  */
-        {ORC_BCAST, ORC_SPLIT, ORC_SPLIT,   ORC_SPLIT, ORC_PARTIAL, ORC_SPLIT  }, /* COL */
-        {ORC_SPLIT, ORC_SPLIT, ORC_PARTIAL, ORC_BCAST, ORC_SPLIT,   ORC_SPLIT  }, /* KS  */
+    /*                 X            W            Y            dY           dX           dW        */
+    static const int32_t K[6][6] = {
+        {ORC_SPLIT,   ORC_BCAST,   ORC_SPLIT,   ORC_SPLIT,   ORC_SPLIT,   ORC_PARTIAL}, /* DP  */
+        {ORC_BCAST,   ORC_SPLIT,   ORC_SPLIT,   ORC_SPLIT,   ORC_PARTIAL, ORC_SPLIT  }, /* COL */
+        {ORC_SPLIT,   ORC_SPLIT,   ORC_PARTIAL, ORC_BCAST,   ORC_SPLIT,   ORC_SPLIT  }, /* KS  */
+        {ORC_PARTIAL, ORC_BCAST,   ORC_PARTIAL, ORC_BCAST,   ORC_BCAST,   ORC_PARTIAL}, /* PB  */
+        {ORC_BCAST,   ORC_PARTIAL, ORC_PARTIAL, ORC_BCAST,   ORC_PARTIAL, ORC_BCAST  }, /* BP  */
+        {ORC_BCAST,   ORC_BCAST,   ORC_BCAST,   ORC_PARTIAL, ORC_PARTIAL, ORC_PARTIAL}, /* BB  */
     };
-    static const int32_t A[3][6] = {
+    static const int32_t A[6][6] = {
         { 0, -1,  0,  0,  0, -1},
         {-1,  1,  1,  1, -1,  1},
         { 1,  0, -1, -1,  1,  0},
+        {-1, -1, -1, -1, -1, -1},
+        {-1, -1, -1, -1, -1, -1},
+        {-1, -1, -1, -1, -1, -1},
     };
-    if (sig < 0 || sig > 2) return -1;
+    if (sig < 0 || sig > 5) return -1;
     for (int t = 0; t < 6; ++t) { kinds[t] = K[sig][t]; axes[t] = A[sig][t]; }
     return 0;
 }
@@ -284,10 +298,9 @@ int orc_linear_samples(int sig, int op, int enc, int64_t M, int64_t K,
  * p1*p2; the nesting order makes (S1:p1, S1:p2) the split over p1*p2 with
  * block c1*p2 + c2 whenever p1*p2 divides the extent.)
  *
- * Signature. Each mesh axis carries one 1-D factor of the table above (the
- * 3-D rule of Sec. 4.2 is DP on mesh axis 0, COL on axis 1, KS on axis 2),
- * or Broadcast for both X and W: such an axis replicates the whole product
- * and all six tensors are Broadcast on it.
+ * Signature. Each mesh axis carries one 1-D signature of the table above
+ * (the 3-D rule of Sec. 4.2 is DP on mesh axis 0, COL on axis 1, KS on
+ * axis 2); an axis with X and W both Broadcast replicates the product.
  *
  * Mesh coordinate of a device (Sec. 4.2, heterogeneous networks). Mesh axis
  * a spans nodes[a] nodes x gpus[a] GPUs per node. The node index and the
@@ -298,7 +311,6 @@ int orc_linear_samples(int sig, int op, int enc, int64_t M, int64_t K,
  * the node digit above the GPU digit within one mesh axis is a reading.
  */
 #define ORC_MAXD 4
-#define ORC_BB 3   /* replicated mesh axis: X and W both Broadcast */
 
 int orc_mesh_coord(int d, const int32_t *nodes, const int32_t *gpus,
                    int64_t node, int64_t gpu, int32_t *c)
@@ -321,11 +333,10 @@ int orc_mesh_coord(int d, const int32_t *nodes, const int32_t *gpus,
 static int axis_factor(int32_t xk, int32_t xa, int32_t wk, int32_t wa)
 {
     int32_t kd[6], ax[6];
-    for (int sig = 0; sig < 3; ++sig) {
+    for (int sig = 0; sig < 6; ++sig) {
         orc_tags(sig, kd, ax);
         if (kd[0] == xk && ax[0] == xa && kd[1] == wk && ax[1] == wa) return sig;
     }
-    if (xk == ORC_BCAST && xa == -1 && wk == ORC_BCAST && wa == -1) return ORC_BB;
     return -1;
 }
 
@@ -343,11 +354,7 @@ int orc_nd_tags(int d, const int32_t *xk, const int32_t *xa, const int32_t *wk,
         int f = axis_factor(xk[a], xa[a], wk[a], wa[a]);
         int32_t kd[6], ax[6];
         if (f < 0) return -1;
-        if (f == ORC_BB) {
-            for (int t = 0; t < 6; ++t) { kd[t] = ORC_BCAST; ax[t] = -1; }
-        } else {
-            orc_tags(f, kd, ax);
-        }
+        orc_tags(f, kd, ax);
         for (int t = 0; t < 6; ++t) {
             kinds[t * d + a] = kd[t];
             axes[t * d + a] = ax[t];

@@ -28,9 +28,9 @@ import oracle
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 S0, S1, B, P = (oracle.SPLIT, 0), (oracle.SPLIT, 1), (oracle.BCAST, -1), (oracle.PARTIAL, -1)
 NAMES = {"S0": S0, "S1": S1, "B": B, "P": P}
-# per-axis states of X and W for each factor (the oracle's 1-D table, plus a
-# replicated axis)
-FACTOR = {"DP": (S0, B), "COL": (B, S1), "KS": (S1, S0), "BB": (B, B)}
+# per-axis states of X and W for each factor (the oracle's 1-D table)
+FACTOR = {"DP": (S0, B), "COL": (B, S1), "KS": (S1, S0), "PB": (P, B), "BP": (B, P),
+          "BB": (B, B)}
 OPS = (oracle.FWD, oracle.BWD_DATA, oracle.BWD_WEIGHT)
 
 
@@ -46,17 +46,35 @@ def coords(mesh):
     return list(itertools.product(*(range(p) for p in mesh)))
 
 
-def nd_reassemble(orc, op, factors, mesh, Xe, We, dYe, M, K, N):
+def partial_inputs(rng, T, states, mesh):
+    """Per device coordinate, the tensor a device holds of the integer tensor
+    T in per-axis states `states`: on the Partial-sum axes, integer parts
+    that sum to T over those axes' coordinates (the full T elsewhere)."""
+    pax = [a for a, st in enumerate(states) if st == P]
+    combos = list(itertools.product(*(range(mesh[a]) for a in pax)))
+    parts = [rng.integers(-3, 4, T.shape) for _ in combos[:-1]]
+    parts.append(T - sum(parts, np.zeros_like(T)))
+    by = dict(zip(combos, parts))
+    return lambda c: by[tuple(c[a] for a in pax)].astype(np.float32)
+
+
+def nd_reassemble(orc, op, factors, mesh, Xi, Wi, dYi, M, K, N, rng=None):
     """All devices' outputs of op combined by the output's per-axis states.
-    Raises AssertionError when Broadcast copies differ or blocks do not tile."""
+    Inputs in a Partial-sum state get per-device integer parts of the given
+    integer tensors. Raises AssertionError when Broadcast copies differ or
+    blocks do not tile."""
+    rng = np.random.default_rng(1) if rng is None else rng
     xs = [FACTOR[f][0] for f in factors]
     ws = [FACTOR[f][1] for f in factors]
+    t = orc.nd_tags(xs, ws)
+    xin, win, dyin = (partial_inputs(rng, T, st, mesh) for T, st in
+                      ((Xi, t[0]), (Wi, t[1]), (dYi, t[3])))
     grow, gcol = {oracle.FWD: (M, N), oracle.BWD_DATA: (M, K), oracle.BWD_WEIGHT: (K, N)}[op]
     total = np.zeros((grow, gcol))
     cover = np.zeros((grow, gcol), dtype=np.int64)
     first = {}
     for c in coords(mesh):
-        part = orc.nd_linear(op, Xe, We, dYe, xs, ws, mesh, c)
+        part = orc.nd_linear(op, xin(c), win(c), dyin(c), xs, ws, mesh, c)
         rows, cols, st = orc.nd_out_shape(op, M, K, N, xs, ws, mesh, c)
         assert part.shape == (rows, cols)
         r0, c0, nr, nc = orc.nd_share(st, mesh, c, grow, gcol)
@@ -85,6 +103,9 @@ CASES = [
     ((2, 3), ("COL", "BB")),
     ((1, 3, 2), ("BB", "DP", "KS")),
     ((2, 1, 2, 2), ("DP", "BB", "COL", "KS")),
+    ((2, 3), ("PB", "COL")),
+    ((3, 2), ("DP", "BP")),
+    ((2, 2, 2), ("PB", "BP", "BB")),
 ]
 SHAPES = [(13, 11, 7), (8, 12, 6)]
 
@@ -94,11 +115,10 @@ def nd_invariant_failures(orc, cases=CASES):
     rng = np.random.default_rng(17)
     for (M, K, N) in SHAPES:
         Xi, Wi, dYi = (rng.integers(-3, 4, s) for s in ((M, K), (K, N), (M, N)))
-        Xe, We, dYe = (a.astype(np.float32) for a in (Xi, Wi, dYi))
         for mesh, factors in cases:
             for op in OPS:
                 try:
-                    got = nd_reassemble(orc, op, factors, mesh, Xe, We, dYe, M, K, N)
+                    got = nd_reassemble(orc, op, factors, mesh, Xi, Wi, dYi, M, K, N, rng)
                     ok = np.array_equal(got, _global(op, Xi, Wi, dYi))
                 except (AssertionError, ValueError):
                     ok = False
@@ -228,7 +248,7 @@ def test_nd_samples_match_blocks(orc):
 def test_bad_nd_arguments_raise(orc):
     X = np.ones((4, 4), np.float32)
     with pytest.raises(ValueError):
-        orc.nd_tags([S0, P], [B, B])                       # Partial-sum input
+        orc.nd_tags([S0, P], [B, P])                       # two Partial-sum operands
     with pytest.raises(ValueError):
         orc.nd_tags([S1], [S1])                            # no factor
     with pytest.raises(ValueError):
@@ -244,9 +264,8 @@ ND_MUTATIONS = [
     ("last mesh axis varies fastest",
      "int64_t node_stride = 1, gpu_stride = 1;\n    for (int a = 0; a < d; ++a) {",
      "int64_t node_stride = 1, gpu_stride = 1;\n    for (int a = d - 1; a >= 0; --a) {"),
-    ("replicated axis tagged Partial-sum",
-     "for (int t = 0; t < 6; ++t) { kd[t] = ORC_BCAST; ax[t] = -1; }",
-     "for (int t = 0; t < 6; ++t) { kd[t] = t == 2 ? ORC_PARTIAL : ORC_BCAST; ax[t] = -1; }"),
+    ("factor search skips the partial-input signatures", "for (int sig = 0; sig < 6; ++sig) {",
+     "for (int sig = 0; sig < 3; ++sig) {"),
     ("dY share taken from W's states", "pl->dy = nd_share_of(d, kinds + 3 * d, axes + 3 * d",
      "pl->dy = nd_share_of(d, kinds + 1 * d, axes + 1 * d"),
 ]

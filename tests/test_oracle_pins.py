@@ -27,6 +27,9 @@ import oracle
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 SIGS = (oracle.DP, oracle.COL, oracle.KS)
+# signatures with a Partial-sum or replicated operand and no split
+LINEAR_SIGS = (oracle.PB, oracle.BP, oracle.BB)
+ALL_SIGS = SIGS + LINEAR_SIGS
 OPS = (oracle.FWD, oracle.BWD_DATA, oracle.BWD_WEIGHT)
 
 
@@ -151,13 +154,62 @@ def test_gradient_state_duality(orc):
     # grad of Split(i) is Split(i); grad of Broadcast is Partial-sum and vice
     # versa (Sec. 4.3 states the Broadcast-weight case).
     dual = {oracle.SPLIT: oracle.SPLIT, oracle.BCAST: oracle.PARTIAL, oracle.PARTIAL: oracle.BCAST}
-    for sig in SIGS:
+    for sig in ALL_SIGS:
         t = orc.tags(sig)
         X, W, Y, dY, dX, dW = t
         for fwd, grad in ((X, dX), (W, dW), (Y, dY)):
             assert grad[0] == dual[fwd[0]]
             if fwd[0] == oracle.SPLIT:
                 assert grad[1] == fwd[1]
+
+
+def partial_parts(rng, T, p):
+    """p integer tensors that sum to the integer tensor T (a Partial-sum
+    state of T over p devices)."""
+    parts = [rng.integers(-3, 4, T.shape) for _ in range(p - 1)]
+    return parts + [T - sum(parts, np.zeros_like(T))]
+
+
+def linear_sig_failures(orc):
+    """(signature, op, p, shape) where the per-rank outputs of a signature with
+    a Partial-sum or replicated operand, given per-rank partial inputs whose
+    sum is the true tensor, do not reassemble into the exact global product
+    (Partial-sum outputs summed, Broadcast outputs equal on every rank)."""
+    bad = []
+    rng = np.random.default_rng(9)
+    for (M, K, N) in SHAPES:
+        Xi, Wi, dYi = (rng.integers(-3, 4, s) for s in ((M, K), (K, N), (M, N)))
+        for sig in LINEAR_SIGS:
+            t = orc.tags(sig)
+            for op in OPS:
+                want = _global_product(op, Xi, Wi, dYi)
+                for p in (1, 2, 3):
+                    # inputs in Partial-sum state get per-rank partials
+                    ins = []
+                    for T, st in ((Xi, t[0]), (Wi, t[1]), (dYi, t[3])):
+                        ins.append(partial_parts(rng, T, p) if st[0] == oracle.PARTIAL
+                                   else [T] * p)
+                    try:
+                        outs = [orc.linear(sig, op, *(a[r].astype(np.float32) for a in ins), p, r)
+                                for r in range(p)]
+                        kind = orc.out_shape(sig, op, M, K, N, p, 0)[2]
+                        if kind == oracle.PARTIAL:
+                            got = np.sum(np.stack(outs), axis=0)
+                        else:
+                            assert all(np.array_equal(o, outs[0]) for o in outs)
+                            got = outs[0]
+                        ok = np.array_equal(got, want)
+                    except (AssertionError, ValueError):
+                        ok = False
+                    if not ok:
+                        bad.append((sig, op, p, (M, K, N)))
+    return bad
+
+
+def test_partial_and_replicated_signatures_reassemble(orc):
+    # By linearity: (P, B) -> P and (B, P) -> P, (B, B) -> B; their backward
+    # states follow the duality (a Broadcast tensor's gradient is Partial-sum)
+    assert linear_sig_failures(orc) == []
 
 
 def test_forward_rule_is_a_factor_of_the_3d_rule(orc):
@@ -229,7 +281,7 @@ def test_samples_match_blocks(orc):
 def test_bad_arguments_raise(orc):
     X = np.ones((4, 4), np.float32)
     with pytest.raises(ValueError):
-        orc.linear(3, 0, X, X, X, 2, 0)       # unknown signature
+        orc.linear(6, 0, X, X, X, 2, 0)       # unknown signature
     with pytest.raises(ValueError):
         orc.linear(0, 0, X, X, X, 2, 2)       # rank out of range
     with pytest.raises(ValueError):
@@ -260,11 +312,17 @@ MUTATIONS = [
     ("forward reads a fixed column of X", "decode(X, enc, (pl->x.r0 + i) * K + (pl->x.c0 + k))",
      "decode(X, enc, (pl->x.r0 + i) * K + (pl->x.c0))"),
     ("data-parallel weight gradient tagged Broadcast",
-     "{ORC_SPLIT, ORC_BCAST, ORC_SPLIT,   ORC_SPLIT, ORC_SPLIT,   ORC_PARTIAL}",
-     "{ORC_SPLIT, ORC_BCAST, ORC_SPLIT,   ORC_SPLIT, ORC_SPLIT,   ORC_BCAST  }"),
+     "{ORC_SPLIT,   ORC_BCAST,   ORC_SPLIT,   ORC_SPLIT,   ORC_SPLIT,   ORC_PARTIAL}",
+     "{ORC_SPLIT,   ORC_BCAST,   ORC_SPLIT,   ORC_SPLIT,   ORC_SPLIT,   ORC_BCAST  }"),
     ("K-split output tagged Broadcast",
-     "{ORC_SPLIT, ORC_SPLIT, ORC_PARTIAL, ORC_BCAST, ORC_SPLIT,   ORC_SPLIT  }",
-     "{ORC_SPLIT, ORC_SPLIT, ORC_BCAST,   ORC_BCAST, ORC_SPLIT,   ORC_SPLIT  }"),
+     "{ORC_SPLIT,   ORC_SPLIT,   ORC_PARTIAL, ORC_BCAST,   ORC_SPLIT,   ORC_SPLIT  }",
+     "{ORC_SPLIT,   ORC_SPLIT,   ORC_BCAST,   ORC_BCAST,   ORC_SPLIT,   ORC_SPLIT  }"),
+    ("replicated product's gradients tagged Broadcast",
+     "{ORC_BCAST,   ORC_BCAST,   ORC_BCAST,   ORC_PARTIAL, ORC_PARTIAL, ORC_PARTIAL}",
+     "{ORC_BCAST,   ORC_BCAST,   ORC_BCAST,   ORC_BCAST,   ORC_BCAST,   ORC_BCAST  }"),
+    ("partial-input output tagged Broadcast",
+     "{ORC_PARTIAL, ORC_BCAST,   ORC_PARTIAL, ORC_BCAST,   ORC_BCAST,   ORC_PARTIAL}",
+     "{ORC_PARTIAL, ORC_BCAST,   ORC_BCAST,   ORC_BCAST,   ORC_BCAST,   ORC_PARTIAL}"),
 ]
 
 
@@ -276,7 +334,7 @@ def test_planted_mistakes_are_caught(tmp_path, name, old, new):
     mut.write_text(src.replace(old, new))
     lib = oracle.build(force=True, src=str(mut), out=str(tmp_path / "liboracle_mut.so"))
     bad = oracle.Oracle(lib)
-    caught = bool(invariant_failures(bad, encs=("f32",)))
+    caught = bool(invariant_failures(bad, encs=("f32",))) or bool(linear_sig_failures(bad))
     if not caught:
         # a mistake in the state table shows up in the duality check instead
         try:
