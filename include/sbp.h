@@ -8,13 +8,21 @@
  * This library runs rank r's local forward and backward products on one GPU
  * and tags each output with its SBP state.
  *
- * Supported signatures (the 1-D factors of the Sec. 4.2 rule; a broadcast
- * operand's gradient is a partial sum, Sec. 4.3 "Sources of Communication"):
+ * Supported signatures (the 1-D factors of the Sec. 4.2 rule, and three
+ * that follow from linearity; a broadcast tensor's gradient is a partial
+ * sum, Sec. 4.3 "Sources of Communication", and a partial sum's gradient is
+ * broadcast):
  *
  *   name  X      W      -> Y     | dY     dX     dW
  *   DP    S(0)   B      -> S(0)  | S(0)   S(0)   P
  *   COL   B      S(1)   -> S(1)  | S(1)   P      S(1)
  *   KS    S(1)   S(0)   -> P     | B      S(1)   S(0)
+ *   PB    P      B      -> P     | B      B      P
+ *   BP    B      P      -> P     | B      P      B
+ *   BB    B      B      -> B     | P      P      P
+ *
+ * PB, BP and BB divide no dimension: every device multiplies full-size
+ * operands (its own partial of a P operand).
  *
  * Conventions (all functions):
  *   - Matrices are row-major with a leading dimension ld (elements between
@@ -126,7 +134,8 @@ int sbp_signature(const sbp_layout_t *x, const sbp_layout_t *w,
 /* Forward local matmul Y_r = X_r W_r (Sec. 4.2, "local matmul").
  * X: M x K (or rank r's share), state *lx; W: K x N (or share), state *lw.
  * Y: rank r's local output, state written to *ly_out (may be NULL):
- *    DP m_r x N, COL M x n_r, KS M x N (Partial-sum, must be fp32).
+ *    DP m_r x N, COL M x n_r, KS M x N (Partial-sum, must be fp32);
+ *    PB and BP M x N (Partial-sum, fp32), BB M x N (Broadcast).
  * Inputs bf16 or fp32 (same dtype); Y is fp32, or bf16 for bf16 inputs and
  * a Split/Broadcast output (rounded to nearest even from the fp32
  * accumulator). */
@@ -136,9 +145,11 @@ int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx,
 
 /* Backward-data local matmul dX_r = dY_r W_r^T (Sec. 4.2: the redistributions
  * of the forward path have backward counterparts; Sec. 4.3).
- * dY: state *ldy (S(0) for DP, S(1) for COL, B for KS); W: state *lw.
+ * dY: state *ldy (S(0) for DP, S(1) for COL, B for KS, PB and BP, P for
+ *     BB); W: state *lw.
  * dX: rank r's local output, state to *ldx_out: DP m_r x K (S(0)),
- *     COL M x K (Partial-sum, fp32), KS M x k_r (S(1)). */
+ *     COL M x K (Partial-sum, fp32), KS M x k_r (S(1)); PB M x K (B), BP
+ *     and BB M x K (Partial-sum, fp32). */
 int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy,
                         const sbp_view_t *W, const sbp_layout_t *lw,
                         sbp_view_t *dX, sbp_layout_t *ldx_out,
@@ -148,7 +159,8 @@ int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy,
  * weight receives partial-sum gradients).
  * X: state *lx; dY: state *ldy.
  * dW: rank r's local output, state to *ldw_out: DP K x N (Partial-sum,
- *     fp32), COL K x n_r (S(1)), KS k_r x N (S(0)). */
+ *     fp32), COL K x n_r (S(1)), KS k_r x N (S(0)); PB and BB K x N
+ *     (Partial-sum, fp32), BP K x N (B). */
 int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx,
                           const sbp_view_t *dY, const sbp_layout_t *ldy,
                           sbp_view_t *dW, sbp_layout_t *ldw_out,
@@ -226,10 +238,10 @@ int sbp_nd_shard_index(const sbp_nd_layout_t *l, int64_t rows, int64_t cols,
 /* Resolves the nd signature of Y = X W (Sec. 4.2: the 3-D rule factors
  * into one 1-D signature per mesh axis) and writes the nd states of Y, dY,
  * dX and dW (Sec. 4.3 gradient states, per axis). Each mesh axis must carry
- * one of the 1-D factors of the table at the top of this file (DP, COL,
- * KS), or Broadcast on both X and W (that axis does not divide the product:
- * Y, dY, dX and dW are Broadcast on it). The layouts must agree on ndim, p
- * and c. Any of y, dy, dx, dw may be NULL. Pure host function.
+ * one of the 1-D signatures of the table at the top of this file; an axis
+ * with X and W both Broadcast (BB) replicates the product, and the
+ * gradients are partial sums on it. The layouts must agree on ndim, p and
+ * c. Any of y, dy, dx, dw may be NULL. Pure host function.
  * Errors: SBP_ERR_NULL (x or w), SBP_ERR_LAYOUT, SBP_ERR_SIGNATURE. */
 int sbp_nd_signature(const sbp_nd_layout_t *x, const sbp_nd_layout_t *w,
                      sbp_nd_layout_t *y, sbp_nd_layout_t *dy,
@@ -241,8 +253,8 @@ int sbp_nd_signature(const sbp_nd_layout_t *x, const sbp_nd_layout_t *w,
  * layouts of one call agree on ndim, p and c, else SBP_ERR_LAYOUT).
  * Local output shapes: X_r is the nd share of X, and so on; Y_r = X_r W_r,
  * dX_r = dY_r W_r^T, dW_r = X_r^T dY_r. An output is Partial-sum -- and must
- * be fp32 -- when any mesh axis leaves it Partial-sum: Y under a KS axis, dX
- * under a COL axis, dW under a DP axis. */
+ * be fp32 -- when any mesh axis leaves it Partial-sum (Y under a KS, PB or
+ * BP axis, dX under a COL, BP or BB axis, dW under a DP, PB or BB axis). */
 int sbp_nd_linear_fwd(const sbp_view_t *X, const sbp_nd_layout_t *lx,
                       const sbp_view_t *W, const sbp_nd_layout_t *lw,
                       sbp_view_t *Y, sbp_nd_layout_t *ly_out,

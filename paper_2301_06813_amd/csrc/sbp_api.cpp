@@ -21,12 +21,13 @@ namespace {
 
 thread_local int g_last_hip = 0;
 
-enum Sig { SIG_DP = 0, SIG_COL = 1, SIG_KS = 2, SIG_NONE = -1 };
+enum Sig { SIG_DP = 0, SIG_COL = 1, SIG_KS = 2, SIG_PB = 3, SIG_BP = 4, SIG_BB = 5, SIG_NONE = -1 };
 
 bool is_split(const sbp_layout_t *l, int axis) {
     return l->kind == SBP_SPLIT && l->axis == axis;
 }
 bool is_bcast(const sbp_layout_t *l) { return l->kind == SBP_BROADCAST; }
+bool is_partial(const sbp_layout_t *l) { return l->kind == SBP_PARTIAL; }
 
 int check_layout(const sbp_layout_t *l) {
     if (!l) return SBP_ERR_NULL;
@@ -50,24 +51,36 @@ int check_pair(const sbp_layout_t *a, const sbp_layout_t *b) {
     return SBP_OK;
 }
 
-// Forward rule (Sec. 4.2, 1-D factors): (S0,B)->S0, (B,S1)->S1, (S1,S0)->P.
+// Forward rule (Sec. 4.2, 1-D factors): (S0,B)->S0, (B,S1)->S1, (S1,S0)->P;
+// and, by linearity of the product in each operand, (P,B)->P, (B,P)->P and
+// (B,B)->B.
 Sig sig_from_xw(const sbp_layout_t *x, const sbp_layout_t *w) {
     if (is_split(x, 0) && is_bcast(w)) return SIG_DP;
     if (is_bcast(x) && is_split(w, 1)) return SIG_COL;
     if (is_split(x, 1) && is_split(w, 0)) return SIG_KS;
+    if (is_partial(x) && is_bcast(w)) return SIG_PB;
+    if (is_bcast(x) && is_partial(w)) return SIG_BP;
+    if (is_bcast(x) && is_bcast(w)) return SIG_BB;
     return SIG_NONE;
 }
-// Backward-data inputs: dY takes Y's dual state (S stays S, P becomes B).
+// Backward-data inputs: dY takes Y's dual state (S stays S, P becomes B, B
+// becomes P).
 Sig sig_from_dyw(const sbp_layout_t *dy, const sbp_layout_t *w) {
     if (is_split(dy, 0) && is_bcast(w)) return SIG_DP;
     if (is_split(dy, 1) && is_split(w, 1)) return SIG_COL;
     if (is_bcast(dy) && is_split(w, 0)) return SIG_KS;
+    if (is_bcast(dy) && is_bcast(w)) return SIG_PB;
+    if (is_bcast(dy) && is_partial(w)) return SIG_BP;
+    if (is_partial(dy) && is_bcast(w)) return SIG_BB;
     return SIG_NONE;
 }
 Sig sig_from_xdy(const sbp_layout_t *x, const sbp_layout_t *dy) {
     if (is_split(x, 0) && is_split(dy, 0)) return SIG_DP;
     if (is_bcast(x) && is_split(dy, 1)) return SIG_COL;
     if (is_split(x, 1) && is_bcast(dy)) return SIG_KS;
+    if (is_partial(x) && is_bcast(dy)) return SIG_PB;
+    if (is_bcast(x) && is_bcast(dy)) return SIG_BP;
+    if (is_bcast(x) && is_partial(dy)) return SIG_BB;
     return SIG_NONE;
 }
 
@@ -95,6 +108,24 @@ void states_of(Sig s, const sbp_layout_t *like, sbp_layout_t out[4]) {
             out[1] = mk(SBP_SPLIT, 1, like);
             out[2] = mk(SBP_PARTIAL, -1, like);
             out[3] = mk(SBP_SPLIT, 1, like);
+            break;
+        case SIG_PB:   // X P, W B: Y P, dY B, dX B, dW P
+            out[0] = mk(SBP_PARTIAL, -1, like);
+            out[1] = mk(SBP_BROADCAST, -1, like);
+            out[2] = mk(SBP_BROADCAST, -1, like);
+            out[3] = mk(SBP_PARTIAL, -1, like);
+            break;
+        case SIG_BP:   // X B, W P: Y P, dY B, dX P, dW B
+            out[0] = mk(SBP_PARTIAL, -1, like);
+            out[1] = mk(SBP_BROADCAST, -1, like);
+            out[2] = mk(SBP_PARTIAL, -1, like);
+            out[3] = mk(SBP_BROADCAST, -1, like);
+            break;
+        case SIG_BB:   // X B, W B: Y B, dY P, dX P, dW P
+            out[0] = mk(SBP_BROADCAST, -1, like);
+            out[1] = mk(SBP_PARTIAL, -1, like);
+            out[2] = mk(SBP_PARTIAL, -1, like);
+            out[3] = mk(SBP_PARTIAL, -1, like);
             break;
         default:
             out[0] = mk(SBP_PARTIAL, -1, like);
@@ -240,22 +271,6 @@ int check_pair(const sbp_nd_layout_t *a, const sbp_nd_layout_t *b) {
     return SBP_OK;
 }
 
-// Per-axis factor of an nd signature: a 1-D signature, or Broadcast on both
-// operands (the axis does not divide the product).
-constexpr int SIG_BB = 3;
-
-bool both_bcast(const sbp_layout_t &a, const sbp_layout_t &b) {
-    return is_bcast(&a) && is_bcast(&b);
-}
-
-// States of Y, dY, dX, dW on mesh axis a given its factor.
-void axis_states(int sig, const sbp_layout_t *like, sbp_layout_t out[4]) {
-    if (sig == SIG_BB) {
-        for (int t = 0; t < 4; ++t) out[t] = mk(SBP_BROADCAST, -1, like);
-        return;
-    }
-    states_of((Sig)sig, like, out);
-}
 
 void nd_set(sbp_nd_layout_t *l, int a, const sbp_layout_t &o) {
     l->kind[a] = o.kind;
@@ -265,11 +280,11 @@ void nd_set(sbp_nd_layout_t *l, int a, const sbp_layout_t &o) {
 // Which pair of operands a product's signature is read from.
 enum Pair { PAIR_XW = 0, PAIR_DYW = 1, PAIR_XDY = 2 };
 
+// Per-axis factor of an nd signature: the 1-D signature of that axis's states.
 int factor_of(Pair pr, const sbp_layout_t &a, const sbp_layout_t &b) {
     Sig s = pr == PAIR_XW ? sig_from_xw(&a, &b)
                           : (pr == PAIR_DYW ? sig_from_dyw(&a, &b) : sig_from_xdy(&a, &b));
-    if (s != SIG_NONE) return s;
-    return both_bcast(a, b) ? SIG_BB : -1;
+    return s == SIG_NONE ? -1 : s;
 }
 
 // Signature of a product from its two input layouts: st[0..3] get the
@@ -296,7 +311,7 @@ int resolve(Pair pr, const sbp_nd_layout_t *a, const sbp_nd_layout_t *b, sbp_nd_
         if (f < 0) return SBP_ERR_SIGNATURE;
         if (factors) factors[i] = f;
         sbp_layout_t o[4];
-        axis_states(f, &la, o);
+        states_of((Sig)f, &la, o);
         for (int t = 0; t < 4; ++t) nd_set(&st[t], i, o[t]);
     }
     return SBP_OK;

@@ -6,10 +6,10 @@ shape (``sbp_shard_index``), allocates the output and calls the entry point.
 All computation happens in libsbp.so.
 
 Signatures are the 1-D factors of AutoDDL's SBP matmul (Sec. 4.2):
-DP (S(0),B)->S(0), COL (B,S(1))->S(1), KS (S(1),S(0))->P. On a device mesh
-an nd signature is one factor per mesh axis (the 3-D rule of Sec. 4.2 is
-("DP", "COL", "KS")), or "BB" for an axis over which both operands are
-replicated; the ``*_nd`` functions take (factors, mesh, coord).
+DP (S(0),B)->S(0), COL (B,S(1))->S(1), KS (S(1),S(0))->P, and by linearity
+PB (P,B)->P, BP (B,P)->P, BB (B,B)->B. On a device mesh an nd signature is
+one of them per mesh axis (the 3-D rule of Sec. 4.2 is ("DP", "COL", "KS"));
+the ``*_nd`` functions take (factors, mesh, coord).
 """
 from __future__ import annotations
 
@@ -28,6 +28,12 @@ def input_layouts(sig: str, p: int, r: int):
         return sbp.broadcast(p, r), sbp.split(1, p, r)
     if sig == "KS":
         return sbp.split(1, p, r), sbp.split(0, p, r)
+    if sig == "PB":
+        return sbp.partial(p, r), sbp.broadcast(p, r)
+    if sig == "BP":
+        return sbp.broadcast(p, r), sbp.partial(p, r)
+    if sig == "BB":
+        return sbp.broadcast(p, r), sbp.broadcast(p, r)
     raise ValueError("unknown signature %r" % sig)
 
 
@@ -46,7 +52,8 @@ def layouts_for(lin, wl, r) -> dict:
 
 
 # states of X and W on one mesh axis, per factor
-FACTOR_STATES = {"DP": ("S0", "B"), "COL": ("B", "S1"), "KS": ("S1", "S0"), "BB": ("B", "B")}
+FACTOR_STATES = {"DP": ("S0", "B"), "COL": ("B", "S1"), "KS": ("S1", "S0"), "PB": ("P", "B"),
+                 "BP": ("B", "P"), "BB": ("B", "B")}
 
 
 def nd_input_layouts(factors, mesh, coord):

@@ -47,7 +47,7 @@ class Linear:
     x_relu: bool = False
     w_gain: float = 1.0   # W ~ N(0, w_gain / K)
     dy_std: float = 1.0
-    factors: tuple = ()   # nd workloads: one of "DP", "COL", "KS", "BB" per mesh axis
+    factors: tuple = ()   # nd workloads: one signature name per mesh axis
 
     @property
     def w_std(self) -> float:

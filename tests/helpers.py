@@ -8,7 +8,8 @@ import torch
 import oracle
 from paper_2301_06813_amd import inputs, linear, sbp
 
-SIG_ID = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS}
+SIG_ID = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS, "PB": oracle.PB,
+          "BP": oracle.BP, "BB": oracle.BB}
 OP_ID = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
 TILES = [(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
 KERNELS = (1, 2)   # pipelined direct-to-LDS, generic

@@ -90,7 +90,7 @@ ORC_KIND = {sbp.SBP_SPLIT: oracle.SPLIT, sbp.SBP_BROADCAST: oracle.BCAST,
 
 def test_signature_table_matches_oracle(L, orc):
     expected = {}
-    for sig in (oracle.DP, oracle.COL, oracle.KS):
+    for sig in (oracle.DP, oracle.COL, oracle.KS, oracle.PB, oracle.BP, oracle.BB):
         t = orc.tags(sig)
         expected[(t[0], t[1])] = t[2:]
     for xs in ALL_STATES:
@@ -154,9 +154,15 @@ ERR_CASES = [
     ("r >= p", dict(lx=sbp.split(0, 4, 4)), sbp.SBP_ERR_LAYOUT),
     ("p mismatch", dict(lw=sbp.broadcast(8, 1)), sbp.SBP_ERR_LAYOUT),
     ("r mismatch", dict(lw=sbp.broadcast(4, 2)), sbp.SBP_ERR_LAYOUT),
-    ("bad signature (B,B)", dict(lx=sbp.broadcast(4, 1)), sbp.SBP_ERR_SIGNATURE),
+    ("bad signature (P,S0)", dict(lx=sbp.partial(4, 1), lw=sbp.split(0, 4, 1)),
+     sbp.SBP_ERR_SIGNATURE),
     ("bad signature (S0,S0)", dict(lw=sbp.split(0, 4, 1)), sbp.SBP_ERR_SIGNATURE),
-    ("partial input", dict(lx=sbp.partial(4, 1)), sbp.SBP_ERR_SIGNATURE),
+    ("partial input, split weight", dict(lx=sbp.partial(4, 1), lw=sbp.split(1, 4, 1)),
+     sbp.SBP_ERR_SIGNATURE),
+    # (P, B) -> P resolves, so a bf16 output of the right shape is refused
+    ("partial input, bf16 output", dict(lx=sbp.partial(4, 1),
+                                        y=sbp.raw_view(YA, 64, 48, 48, BF, sbp.SBP_LOCAL)),
+     sbp.SBP_ERR_DTYPE),
     ("inner dims", dict(w=sbp.raw_view(WA, 33, 48, 48, BF)), sbp.SBP_ERR_SHAPE),
     ("ld < cols", dict(x=sbp.raw_view(XA, 64, 32, 31, BF)), sbp.SBP_ERR_SHAPE),
     ("negative rows", dict(x=sbp.raw_view(XA, -1, 32, 32, BF)), sbp.SBP_ERR_SHAPE),
@@ -205,9 +211,9 @@ def test_backward_signature_errors(L):
     dy = sbp.raw_view(XA, 64, 48, 48, BF)
     w = sbp.raw_view(WA, 32, 48, 48, BF)
     dx = sbp.raw_view(YA, 16, 32, 32, BF, sbp.SBP_LOCAL)
-    # bwd_data: dY P is never an input state
+    # bwd_data: (dY P, W S(0)) is no signature (dY is P only under BB, with W B)
     rc = sbp.lib().sbp_linear_bwd_data(ctypes.byref(dy), ctypes.byref(sbp.partial(4, 1)),
-                                       ctypes.byref(w), ctypes.byref(sbp.broadcast(4, 1)),
+                                       ctypes.byref(w), ctypes.byref(sbp.split(0, 4, 1)),
                                        ctypes.byref(dx), ctypes.byref(lo), None)
     assert rc == sbp.SBP_ERR_SIGNATURE
     # bwd_weight: (X S(0), dY B) is no signature

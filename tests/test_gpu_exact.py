@@ -53,6 +53,22 @@ def test_exact_all_signatures_default_plan(shape):
                     _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
 
 
+@pytest.mark.parametrize("shape", [(300, 1000, 270), (1, 70, 9)])
+def test_exact_partial_and_replicated_signatures(shape):
+    # (P,B)->P, (B,P)->P, (B,B)->B: full-size local operands on every rank
+    M, K, N = shape
+    X, W, dY = _int_inputs(M, K, N, 150)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    for p in (1, 4):
+        for r in sorted({0, p - 1}):
+            for sig in ("PB", "BP", "BB"):
+                for op in OPS:
+                    say("exact", shape, p, r, sig, op)
+                    _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh)
+                say("exact bwd pair", shape, p, r, sig)
+                _check_exact_bwd(sig, p, r, X, W, dY, Xh, Wh, dYh)
+
+
 TILE_KERNELS = [(t, k) for k in KERNELS for t in TILES] + EXTRA_TILE_KERNELS
 TK_IDS = ["%dx%d-k%d" % (t[0], t[1], k) for t, k in TILE_KERNELS]
 

@@ -25,8 +25,9 @@ from helpers import decode, normwise_rel, out_bits, say
 pytestmark = pytest.mark.gpu
 OPS = ("fwd", "bwd_data", "bwd_weight")
 OP_ID = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
-S0, S1, B = (oracle.SPLIT, 0), (oracle.SPLIT, 1), (oracle.BCAST, -1)
-ORC_FACTOR = {"DP": (S0, B), "COL": (B, S1), "KS": (S1, S0), "BB": (B, B)}
+S0, S1, B, P = (oracle.SPLIT, 0), (oracle.SPLIT, 1), (oracle.BCAST, -1), (oracle.PARTIAL, -1)
+ORC_FACTOR = {"DP": (S0, B), "COL": (B, S1), "KS": (S1, S0), "PB": (P, B), "BP": (B, P),
+              "BB": (B, B)}
 TO_ABI = {oracle.SPLIT: sbp.SBP_SPLIT, oracle.BCAST: sbp.SBP_BROADCAST,
           oracle.PARTIAL: sbp.SBP_PARTIAL}
 TOL_BF16 = 2e-2
@@ -61,7 +62,8 @@ def _exact(out, want):
 
 
 MESHES = [((2, 2, 2), ("DP", "COL", "KS")), ((3, 2), ("KS", "COL")), ((2, 3), ("DP", "DP")),
-          ((2, 2), ("KS", "KS")), ((2, 3), ("COL", "BB")), ((2, 1, 3), ("BB", "DP", "COL"))]
+          ((2, 2), ("KS", "KS")), ((2, 3), ("COL", "BB")), ((2, 1, 3), ("BB", "DP", "COL")),
+          ((2, 2, 2), ("PB", "COL", "BP"))]
 
 
 @pytest.mark.parametrize("mesh,factors", MESHES,

@@ -98,7 +98,7 @@ def test_nd_signature_matches_oracle(L):
             for t, g in enumerate(got):
                 assert g.states() == want[2 + t]
                 assert list(g.p[:2]) == mesh and list(g.c[:2]) == c
-    assert accepted == 16   # four factors (DP, COL, KS, replicated) per axis
+    assert accepted == 36   # six 1-D signatures per axis
 
 
 def test_nd_layout_errors(L):
@@ -158,7 +158,7 @@ def test_nd_call_validation(L):
     # layouts disagree on the coordinate
     other = sbp.nd_layout(["B", "S1", "S0"], mesh, (0, 0, 1))
     assert call(sbp.raw_view(YA, 32, 24, 24, F32, sbp.SBP_LOCAL), llw=other) == sbp.SBP_ERR_LAYOUT
-    # no factor on mesh axis 1: (B, B) is allowed, (S1, S1) is not
+    # no signature on mesh axis 2: (S1, S1)
     bad_w = sbp.nd_layout(["B", "S1", "S1"], mesh, c)
     assert call(sbp.raw_view(YA, 32, 24, 24, F32, sbp.SBP_LOCAL), llw=bad_w) == \
         sbp.SBP_ERR_SIGNATURE
