@@ -90,8 +90,14 @@ typedef enum { SBP_BF16 = 0, SBP_F32 = 1 } sbp_dtype_t;
 
 /* SBP_GLOBAL: the view spans the whole global tensor and the library selects
  * rank r's share inside it (a strided sub-view, never a copy).
- * SBP_LOCAL: the view is exactly rank r's share. */
-typedef enum { SBP_GLOBAL = 0, SBP_LOCAL = 1 } sbp_scope_t;
+ * SBP_LOCAL: the view is exactly rank r's share.
+ * SBP_ACCUMULATE (outputs only): the call adds its product to the output's
+ * current contents instead of overwriting them -- gradient accumulation
+ * over micro-batches (Sec. 5 splits each mini-batch into micro-batches and
+ * accumulates their gradients). The output must be fp32 (else
+ * SBP_ERR_DTYPE); each element becomes old + product with one fp32
+ * rounding (the product itself summed in fp32 first). */
+typedef enum { SBP_GLOBAL = 0, SBP_LOCAL = 1, SBP_ACCUMULATE = 2 } sbp_scope_t;
 
 /* A strided 2-D view: element (i, j) is at data + i*ld + j (elements). */
 typedef struct {
@@ -100,7 +106,8 @@ typedef struct {
     int64_t cols;
     int64_t ld;
     int32_t dtype; /* sbp_dtype_t */
-    int32_t scope; /* sbp_scope_t; ignored for outputs, which are always local */
+    int32_t scope; /* sbp_scope_t; outputs are always local: SBP_ACCUMULATE
+                      adds to them, any other value overwrites them */
 } sbp_view_t;
 
 /* Rank r's share of a tensor: rows [row_off, row_off+rows) x cols

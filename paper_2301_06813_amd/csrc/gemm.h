@@ -27,6 +27,7 @@ struct Gemm {
     void *C;
     int64_t ldc;
     int64_t m, n, k;
+    int accumulate = 0;    // fp32 output only: C += product instead of C = product
 };
 
 struct Plan {
@@ -66,6 +67,8 @@ int kernel_code(const Plan &p);   // kernel code of a plan, as sbp_plan reports 
 // GEMM of plan p; with p.splits > 1 it writes partials to ws and then runs
 // the split reduction into g.C.
 hipError_t launch_bf16(const Gemm &g, const Plan &p, float *ws, hipStream_t s);
+// Adds the splits' partials (in split order) and stores them into g.C, or
+// adds the sum to g.C's contents when g.accumulate.
 hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipStream_t s);
 // Both split reductions of a grouped backward launch, in one launch.
 hipError_t launch_split_reduce_pair(const Gemm &gd, int sd, const float *wsd, const Gemm &gw,

@@ -224,9 +224,10 @@ struct StageRow {
 // wave writes whole contiguous row segments. `vec`: C's base and ldc allow
 // aligned 16-byte stores; otherwise (and at the right edge) elements are
 // stored one by one.
-template <int BM, int BN, int LD, int NT_, bool F32>
+template <int BM, int BN, int LD, int NT_, bool F32, bool ACC = false>
 __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t ldc, int m,
                                              int n, int m0, int n0, bool vec, int tid) {
+    static_assert(F32 || !ACC, "accumulation needs an fp32 output");
     constexpr int EPC = F32 ? 4 : 8;             // output elements per 16-byte chunk
     constexpr int CPR = BN / EPC;                // chunks per tile row
     constexpr int ITER = BM * CPR / NT_;
@@ -239,14 +240,15 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
         if (row >= m || col >= n) continue;
         const float *src = tile + r * LD + c;
         if constexpr (F32) {
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(src);
+            f32x4 v = *reinterpret_cast<const f32x4 *>(src);
             float *dst = reinterpret_cast<float *>(C) + (int64_t)row * ldc + col;
             if (vec && col + 4 <= n) {
+                if constexpr (ACC) v += *reinterpret_cast<const f32x4 *>(dst);
                 *reinterpret_cast<f32x4 *>(dst) = v;
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    if (col + e < n) dst[e] = v[e];
+                    if (col + e < n) dst[e] = ACC ? dst[e] + v[e] : v[e];
             }
         } else {
             const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
@@ -428,8 +430,9 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     if constexpr (EPI == EPI_ROWQ) {
         // lane owns row r = lane % 32 of each 32 x 32 block and, for register
         // quad q, columns 8 q + 4 (lane / 32) + 0..3
-        auto store_all = [&](auto f32_tag, void *out, int64_t ldo, bool vec) {
+        auto store_all = [&](auto f32_tag, auto acc_tag, void *out, int64_t ldo, bool vec) {
             constexpr bool F32 = decltype(f32_tag)::value;
+            constexpr bool ACC = decltype(acc_tag)::value;
 #pragma unroll
             for (int i = 0; i < MI; ++i) {
                 const int row = m0 + wm * WM + i * 32 + (lane & 31);
@@ -445,11 +448,14 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                             if (vec && col + 4 <= g.n) {
                                 f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1],
                                            acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                                if constexpr (ACC) v += *reinterpret_cast<const f32x4 *>(dst);
                                 *reinterpret_cast<f32x4 *>(dst) = v;
                             } else {
 #pragma unroll
                                 for (int e = 0; e < 4; ++e)
-                                    if (col + e < g.n) dst[e] = acc[i][j][4 * q + e];
+                                    if (col + e < g.n)
+                                        dst[e] = ACC ? dst[e] + acc[i][j][4 * q + e]
+                                                     : acc[i][j][4 * q + e];
                             }
                         } else {
                             uint16_t *dst =
@@ -473,9 +479,13 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
             }
         };
         if (partial)
-            store_all(std::true_type{}, ws_out, (int64_t)g.n, g.n % 4 == 0);
+            store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n, g.n % 4 == 0);
+        else if (OUT_F32 && g.accumulate)
+            store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
+                      g.C, g.ldc, (bool)g.vec_c4);
         else
-            store_all(std::integral_constant<bool, OUT_F32>{}, g.C, g.ldc, (bool)g.vec_c4);
+            store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, g.C, g.ldc,
+                      (bool)g.vec_c4);
         return;
     }
 
@@ -515,6 +525,9 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         if (partial)
             store_staged<BM, BN, LD, 64 * NW, true>(tile, ws_out, g.n, g.m, g.n, m0, n0,
                                                     g.n % 4 == 0, tid);
+        else if (OUT_F32 && g.accumulate)
+            store_staged<BM, BN, LD, 64 * NW, OUT_F32, OUT_F32>(tile, g.C, g.ldc, g.m, g.n, m0,
+                                                                n0, g.vec_c4, tid);
         else
             store_staged<BM, BN, LD, 64 * NW, OUT_F32>(tile, g.C, g.ldc, g.m, g.n, m0, n0,
                                                        OUT_F32 ? g.vec_c4 : g.vec_c8, tid);
@@ -522,8 +535,9 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         return;
     }
 
-    auto store_all = [&](auto f32_tag, void *out, int64_t ldo) {
+    auto store_all = [&](auto f32_tag, auto acc_tag, void *out, int64_t ldo) {
         constexpr bool F32 = decltype(f32_tag)::value;
+        constexpr bool ACC = decltype(acc_tag)::value;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
 #pragma unroll
@@ -535,7 +549,10 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                     for (int r = 0; r < 16; ++r) {
                         const int row = rbase + 8 * (r >> 2) + (r & 3);
                         if (row < g.m) {
-                            if constexpr (F32)
+                            if constexpr (F32 && ACC) {
+                                float *d = reinterpret_cast<float *>(out) + (int64_t)row * ldo + col;
+                                *d = *d + acc[i][j][r];
+                            } else if constexpr (F32)
                                 reinterpret_cast<float *>(out)[(int64_t)row * ldo + col] =
                                     acc[i][j][r];
                             else
@@ -548,9 +565,12 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         }
     };
     if (partial)
-        store_all(std::true_type{}, ws_out, (int64_t)g.n);
+        store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n);
+    else if (OUT_F32 && g.accumulate)
+        store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
+                  g.C, g.ldc);
     else
-        store_all(std::integral_constant<bool, OUT_F32>{}, g.C, g.ldc);
+        store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, g.C, g.ldc);
 }
 
 

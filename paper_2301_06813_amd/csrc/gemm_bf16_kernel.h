@@ -70,6 +70,7 @@ struct GemmArgs {
     int32_t vec_a, vec_b;       // operand base and ld allow aligned 16-byte loads
     int32_t vec_c4, vec_c8;     // C's base and ldc allow aligned 16-byte stores of
                                 // 4 fp32 / 8 bf16 elements
+    int32_t accumulate;         // fp32 C: add the product to C's contents
 };
 
 // Byte offset of 16-byte chunk c (0..7) of LDS row `row`.
@@ -366,8 +367,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
                     const int row = rbase + 8 * (r >> 2) + (r & 3);
                     if (row < g.m) {
                         if constexpr (OUT_F32) {
-                            float *C = reinterpret_cast<float *>(g.C);
-                            C[(int64_t)row * g.ldc + col] = acc[i][j][r];
+                            float *C = reinterpret_cast<float *>(g.C) + (int64_t)row * g.ldc + col;
+                            *C = g.accumulate ? *C + acc[i][j][r] : acc[i][j][r];
                         } else {
                             uint16_t *C = reinterpret_cast<uint16_t *>(g.C);
                             C[(int64_t)row * g.ldc + col] = f32_to_bf16_bits(acc[i][j][r]);

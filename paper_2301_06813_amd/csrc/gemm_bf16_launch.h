@@ -129,6 +129,7 @@ static inline sbpk::GemmArgs make_args(const Gemm &g, const Plan &p, float *ws) 
     const bool c16 = (reinterpret_cast<uintptr_t>(g.C) & 15) == 0;
     a.vec_c4 = c16 && (g.ldc % 4 == 0);
     a.vec_c8 = c16 && (g.ldc % 8 == 0);
+    a.accumulate = g.accumulate;
     return a;
 }
 

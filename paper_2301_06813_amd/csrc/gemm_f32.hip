@@ -21,6 +21,7 @@ struct F32Args {
     int64_t lda, ldb, ldc;
     int32_t m, n, k;
     int32_t tiles_n;
+    int32_t accumulate;   // add the product to C's contents
 };
 
 template <bool A_KMAJ, bool B_KMAJ>
@@ -82,7 +83,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(F32Args g) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int col = n0 + tx + 16 * j;
-            if (col < g.n) g.C[(int64_t)row * g.ldc + col] = acc[i][j];
+            if (col >= g.n) continue;
+            float *c = g.C + (int64_t)row * g.ldc + col;
+            *c = g.accumulate ? *c + acc[i][j] : acc[i][j];
         }
     }
 }
@@ -115,6 +118,7 @@ hipError_t launch_f32(const Gemm &g, hipStream_t s) {
     a.m = (int32_t)g.m;
     a.n = (int32_t)g.n;
     a.k = (int32_t)g.k;
+    a.accumulate = g.accumulate;
     const int tiles_m = (int)((g.m + sbpk::F_BM - 1) / sbpk::F_BM);
     a.tiles_n = (int)((g.n + sbpk::F_BN - 1) / sbpk::F_BN);
     const int grid = tiles_m * a.tiles_n;

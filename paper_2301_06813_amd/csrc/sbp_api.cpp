@@ -182,6 +182,7 @@ int check_output(const sbp_view_t *o, int64_t rows, int64_t cols, int32_t in_dty
     if (o->rows != rows || o->cols != cols) return SBP_ERR_SHAPE;
     if (in_dtype == SBP_F32 && o->dtype != SBP_F32) return SBP_ERR_DTYPE;
     if (out_kind == SBP_PARTIAL && o->dtype != SBP_F32) return SBP_ERR_DTYPE;
+    if (o->scope == SBP_ACCUMULATE && o->dtype != SBP_F32) return SBP_ERR_DTYPE;
     auto oe = extent(o->data, o->rows, o->cols, o->ld, o->dtype);
     if (overlaps(oe, extent(a.ptr, a.rows, a.cols, a.ld, a.dtype)) ||
         overlaps(oe, extent(b.ptr, b.rows, b.cols, b.ld, b.dtype)))
@@ -377,6 +378,7 @@ int prep_fwd(const sbp_view_t *X, const L *lx, const sbp_view_t *W, const L *lw,
     if ((rc = check_output(Y, x.rows, w.cols, x.dtype, kind, x, w))) return rc;
     *g = sbpi::Gemm{sbpi::OR_FWD, x.dtype, Y->dtype, x.ptr, x.ld, w.ptr, w.ld,
                     Y->data, Y->ld, x.rows, w.cols, x.cols};
+    g->accumulate = Y->scope == SBP_ACCUMULATE;
     *st_out = st[0];
     return SBP_OK;
 }
@@ -398,6 +400,7 @@ int prep_bwd_data(const sbp_view_t *dY, const L *ldy, const sbp_view_t *W, const
     if ((rc = check_output(dX, d.rows, w.rows, d.dtype, kind, d, w))) return rc;
     *g = sbpi::Gemm{sbpi::OR_BWD_DATA, d.dtype, dX->dtype, d.ptr, d.ld, w.ptr, w.ld,
                     dX->data, dX->ld, d.rows, w.rows, d.cols};
+    g->accumulate = dX->scope == SBP_ACCUMULATE;
     *st_out = st[2];
     return SBP_OK;
 }
@@ -419,6 +422,7 @@ int prep_bwd_weight(const sbp_view_t *X, const L *lx, const sbp_view_t *dY, cons
     if ((rc = check_output(dW, x.cols, d.cols, x.dtype, kind, x, d))) return rc;
     *g = sbpi::Gemm{sbpi::OR_BWD_WEIGHT, x.dtype, dW->dtype, x.ptr, x.ld, d.ptr, d.ld,
                     dW->data, dW->ld, x.cols, d.cols, x.rows};
+    g->accumulate = dW->scope == SBP_ACCUMULATE;
     *st_out = st[3];
     return SBP_OK;
 }

@@ -4,8 +4,8 @@
 // products in a workspace, slice s holding the m x n output of split s
 // (row-major, ld n). This kernel adds the slices in split order
 // 0, 1, ..., S-1 -- the same order whatever the schedule, so results are
-// deterministic -- and writes the output as fp32, or as bf16 rounded to
-// nearest even. Each thread owns 4 consecutive columns of one row: 16-byte
+// deterministic -- and writes the output as fp32 (or adds the sum to the
+// fp32 output's contents), or as bf16 rounded to nearest even. Each thread owns 4 consecutive columns of one row: 16-byte
 // loads of every slice when n is a multiple of 4, and one vector store (or
 // element stores at a ragged edge or an unaligned output) that is contiguous
 // across the threads of a wave.
@@ -24,7 +24,7 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 // 8-byte (bf16) store per group.
 template <bool OUT_F32>
 __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int S, void *C,
-                                             int64_t ldc, bool vec, int64_t gidx) {
+                                             int64_t ldc, bool vec, bool acc, int64_t gidx) {
     const int groups_per_row = (n + 3) / 4;
     if (gidx >= (int64_t)m * groups_per_row) return;
     const int row = (int)(gidx / groups_per_row);
@@ -52,8 +52,10 @@ __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int 
     }
     if (vec && col + 4 <= n) {
         if constexpr (OUT_F32) {
-            *reinterpret_cast<f32x4v *>(reinterpret_cast<float *>(C) + (int64_t)row * ldc + col) =
-                v;
+            f32x4v *dst =
+                reinterpret_cast<f32x4v *>(reinterpret_cast<float *>(C) + (int64_t)row * ldc + col);
+            if (acc) v = *dst + v;
+            *dst = v;
         } else {
             typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
             u32x2v w;
@@ -70,7 +72,8 @@ __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int 
     for (int e = 0; e < 4; ++e) {
         if (col + e >= n) break;
         if constexpr (OUT_F32) {
-            reinterpret_cast<float *>(C)[(int64_t)row * ldc + col + e] = v[e];
+            float *dst = reinterpret_cast<float *>(C) + (int64_t)row * ldc + col + e;
+            *dst = acc ? *dst + v[e] : v[e];
         } else {
             __bf16 h = (__bf16)v[e];
             reinterpret_cast<uint16_t *>(C)[(int64_t)row * ldc + col + e] =
@@ -81,8 +84,9 @@ __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int 
 
 template <bool OUT_F32>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float *ws, int m, int n, int S,
-                                                           void *C, int64_t ldc, int vec) {
-    reduce_group<OUT_F32>(ws, m, n, S, C, ldc, vec != 0,
+                                                           void *C, int64_t ldc, int vec,
+                                                           int acc) {
+    reduce_group<OUT_F32>(ws, m, n, S, C, ldc, vec != 0, OUT_F32 && acc != 0,
                           (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
 }
 
@@ -95,6 +99,7 @@ struct ReduceJob {
     void *C;
     int64_t ldc;
     int vec;
+    int acc;   // fp32 output: add to C's contents
 };
 
 template <bool OD, bool OW>
@@ -102,10 +107,10 @@ __global__ __launch_bounds__(256) void split_reduce_pair_kernel(ReduceJob d, Red
                                                                 int blocks_d) {
     const int b = blockIdx.x;
     if (b < blocks_d)
-        reduce_group<OD>(d.ws, d.m, d.n, d.S, d.C, d.ldc, d.vec != 0,
+        reduce_group<OD>(d.ws, d.m, d.n, d.S, d.C, d.ldc, d.vec != 0, OD && d.acc != 0,
                          (int64_t)b * blockDim.x + threadIdx.x);
     else
-        reduce_group<OW>(w.ws, w.m, w.n, w.S, w.C, w.ldc, w.vec != 0,
+        reduce_group<OW>(w.ws, w.m, w.n, w.S, w.C, w.ldc, w.vec != 0, OW && w.acc != 0,
                          (int64_t)(b - blocks_d) * blockDim.x + threadIdx.x);
 }
 
@@ -128,10 +133,10 @@ hipError_t launch_split_reduce(const Gemm &g, int splits, const float *ws, hipSt
     if (g.out_dtype == DT_F32)
         return launch_kernel(sbpk::split_reduce_kernel<true>, "split_reduce_kernel<true>",
                              dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C,
-                             g.ldc, vec);
+                             g.ldc, vec, g.accumulate);
     return launch_kernel(sbpk::split_reduce_kernel<false>, "split_reduce_kernel<false>",
                          dim3(blocks), dim3(256), s, ws, (int)g.m, (int)g.n, splits, g.C, g.ldc,
-                         vec);
+                         vec, 0);
 }
 
 static unsigned reduce_blocks(const Gemm &g) {
@@ -141,8 +146,10 @@ static unsigned reduce_blocks(const Gemm &g) {
 
 hipError_t launch_split_reduce_pair(const Gemm &gd, int sd, const float *wsd, const Gemm &gw,
                                     int sw, const float *wsw, hipStream_t s) {
-    const sbpk::ReduceJob d{wsd, (int)gd.m, (int)gd.n, sd, gd.C, gd.ldc, reduce_vec(gd)};
-    const sbpk::ReduceJob w{wsw, (int)gw.m, (int)gw.n, sw, gw.C, gw.ldc, reduce_vec(gw)};
+    const sbpk::ReduceJob d{wsd, (int)gd.m, (int)gd.n, sd, gd.C, gd.ldc, reduce_vec(gd),
+                            gd.accumulate};
+    const sbpk::ReduceJob w{wsw, (int)gw.m, (int)gw.n, sw, gw.C, gw.ldc, reduce_vec(gw),
+                            gw.accumulate};
     const unsigned bd = reduce_blocks(gd), bw = reduce_blocks(gw);
     const bool od = gd.out_dtype == DT_F32, ow = gw.out_dtype == DT_F32;
 #define SBP_PAIR(OD_, OW_, NAME)                                                             \

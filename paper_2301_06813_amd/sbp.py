@@ -30,7 +30,7 @@ SBP_ERR_HIP = -8
 
 SBP_SPLIT, SBP_BROADCAST, SBP_PARTIAL = 0, 1, 2
 SBP_BF16, SBP_F32 = 0, 1
-SBP_GLOBAL, SBP_LOCAL = 0, 1
+SBP_GLOBAL, SBP_LOCAL, SBP_ACCUMULATE = 0, 1, 2
 
 EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd_data",
            "sbp_linear_bwd_weight", "sbp_linear_bwd", "sbp_strerror", "sbp_last_hip_error", "sbp_plan",

@@ -157,6 +157,8 @@ ERR_CASES = [
     ("bad signature (P,S0)", dict(lx=sbp.partial(4, 1), lw=sbp.split(0, 4, 1)),
      sbp.SBP_ERR_SIGNATURE),
     ("bad signature (S0,S0)", dict(lw=sbp.split(0, 4, 1)), sbp.SBP_ERR_SIGNATURE),
+    ("accumulate into bf16", dict(y=sbp.raw_view(YA, 16, 48, 48, BF, sbp.SBP_ACCUMULATE)),
+     sbp.SBP_ERR_DTYPE),
     ("partial input, split weight", dict(lx=sbp.partial(4, 1), lw=sbp.split(1, 4, 1)),
      sbp.SBP_ERR_SIGNATURE),
     # (P, B) -> P resolves, so a bf16 output of the right shape is refused

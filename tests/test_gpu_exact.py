@@ -69,6 +69,90 @@ def test_exact_partial_and_replicated_signatures(shape):
                 _check_exact_bwd(sig, p, r, X, W, dY, Xh, Wh, dYh)
 
 
+def _accumulate_case(op, sig, p, r, X, W, dY, Xh, Wh, dYh, seed):
+    """An fp32 output holding integers gets the product added (SBP_ACCUMULATE);
+    the result must equal old + the oracle's product exactly."""
+    L = linear.layouts(sig, p, r)
+    M, K = X.shape
+    N = W.shape[1]
+    rows, cols = linear.out_shape(op, L, M, K, N)
+    old = inputs.randint((rows, cols), -8, 8, seed, torch.float32, "cuda")
+    out = old.clone()
+    linear.run_L(op, L, X, W, dY, out, accumulate=True)
+    torch.cuda.synchronize()
+    want = old.double().cpu().numpy() + oracle_full(op, sig, p, r, Xh, Wh, dYh)
+    assert np.array_equal(decode(out), want), (op, sig, p, r)
+
+
+# (tile, kernel, splits) plans that reach every epilogue: direct, staged,
+# row-quad, the generic kernel, and the split reduction
+ACC_PLANS = [None, ((128, 128), 1, 1), ((128, 128), 1, 3), ((128, 128), 5, 1), ((64, 64), 7, 1),
+             ((256, 256), 6, 1), ((128, 128), 2, 1), ((64, 64), 2, 2)]
+
+
+@pytest.mark.parametrize("plan", ACC_PLANS, ids=[str(p_) for p_ in ACC_PLANS])
+def test_exact_accumulate(plan):
+    M, K, N = 304, 1104, 272
+    X, W, dY = _int_inputs(M, K, N, 300)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    try:
+        if plan is not None:
+            (bm, bn), code, splits = plan
+            sbp.sbp_set_plan_override(bm, bn, splits, code)
+        for p, r in ((2, 1), (3, 0)):
+            for sig in ("DP", "COL", "KS", "PB"):
+                for op in OPS:
+                    say("accumulate", plan, p, r, sig, op)
+                    _accumulate_case(op, sig, p, r, X, W, dY, Xh, Wh, dYh, 310 + r)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
+
+
+def test_exact_accumulate_grouped_backward():
+    # gradient accumulation over two micro-batches through the two-product
+    # call: dW = X1^T dY1 + X2^T dY2 (dX overwritten each time)
+    M, K, N = 256, 384, 320
+    X1, W, dY1 = _int_inputs(M, K, N, 400)
+    X2, _, dY2 = _int_inputs(M, K, N, 410)
+    for grouped in (1, 2):
+        for sig, p, r in (("DP", 4, 1), ("KS", 2, 0), ("COL", 4, 3)):
+            say("accumulate grouped", grouped, sig, p, r)
+            L = linear.layouts(sig, p, r)
+            dX = linear.alloc_out("bwd_data", sig, p, r, M, K, N, X1.dtype, "cuda")
+            dW = linear.alloc_out("bwd_weight", sig, p, r, M, K, N, X1.dtype, "cuda").float()
+            dW.zero_()
+            try:
+                sbp.sbp_set_plan_override(128, 128, 2, 1)
+                sbp.sbp_set_bwd_override(grouped, 3)
+                for X, dY in ((X1, dY1), (X2, dY2)):
+                    linear.run_bwd_L(L, X, W, dY, dX, dW, accumulate_dw=True)
+                torch.cuda.synchronize()
+            finally:
+                sbp.sbp_set_plan_override(0, 0, 1)
+            want = sum(oracle_full("bwd_weight", sig, p, r, *(inputs.host_bits(t) for t in
+                                                              (X, W, dY)))
+                       for X, dY in ((X1, dY1), (X2, dY2)))
+            assert np.array_equal(decode(dW), want), (grouped, sig)
+            want_dx = oracle_full("bwd_data", sig, p, r, *(inputs.host_bits(t) for t in
+                                                          (X2, W, dY2)))
+            got_dx = decode(dX)
+            if dX.dtype == torch.bfloat16:
+                assert np.array_equal(out_bits(dX), oracle.round_bf16(want_dx))
+            else:
+                assert np.array_equal(got_dx, want_dx)
+
+
+def test_exact_accumulate_fp32_inputs():
+    g = torch.Generator().manual_seed(5)
+    X, W, dY = (torch.randint(-3, 4, s, generator=g).float().cuda() for s in
+                ((64, 128), (128, 256), (64, 256)))
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    for sig in ("DP", "COL", "KS"):
+        for op in OPS:
+            say("accumulate fp32", sig, op)
+            _accumulate_case(op, sig, 4, 2, X, W, dY, Xh, Wh, dYh, 500)
+
+
 TILE_KERNELS = [(t, k) for k in KERNELS for t in TILES] + EXTRA_TILE_KERNELS
 TK_IDS = ["%dx%d-k%d" % (t[0], t[1], k) for t, k in TILE_KERNELS]
 
