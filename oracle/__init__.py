@@ -38,6 +38,8 @@ FWD, BWD_DATA, BWD_WEIGHT = 0, 1, 2
 OPS = {"fwd": FWD, "bwd_data": BWD_DATA, "bwd_weight": BWD_WEIGHT}
 # state kinds
 SPLIT, BCAST, PARTIAL = 0, 1, 2
+# attention-core products (see oracle.c)
+ATT_S, ATT_O, ATT_DQ, ATT_DK, ATT_DP, ATT_DV = 0, 1, 2, 3, 4, 5
 # input encodings
 IN_BF16, IN_F32 = 0, 1
 
@@ -98,6 +100,8 @@ class Oracle:
         lib.orc_nd_linear_samples.argtypes = [ci, ci, i64, i64, i64, ci, p32, p32, p32, p32, p32,
                                               p32, vp, vp, vp, i64, vp, vp, vp]
         lib.orc_nd_linear_samples.restype = ci
+        lib.orc_attn.argtypes = [ci, ci, i64, i64, i64, i64, i64, i64, i64, vp, vp, vp]
+        lib.orc_attn.restype = ci
         self.lib = lib
 
     def split(self, D: int, p: int, r: int) -> tuple[int, int]:
@@ -245,6 +249,27 @@ class Oracle:
             raise ValueError("bad nd oracle arguments")
         return out
 
+    # ------------------------------------------------ attention core
+    def attn(self, which, T1, T2, p, r, sq, sk, d) -> np.ndarray:
+        """Device r's output of attention product `which` (ATT_*) under a head
+        split over p devices, as fp64 [batch][local heads][rows][cols]. T1 and
+        T2 are the operands in the order of the product's definition,
+        contiguous [batch][heads][rows][cols], bf16 bits (uint16) or fp32."""
+        (T1, T2, _), enc = _prep(T1, T2, None)
+        nb, nh = T1.shape[:2]
+        _, hr = self.split(nh, p, r)
+        shapes = {ATT_S: (sq, sk), ATT_O: (sq, d), ATT_DQ: (sq, d), ATT_DK: (sk, d),
+                  ATT_DP: (sq, sk), ATT_DV: (sk, d)}
+        if which not in shapes:
+            raise ValueError("unknown attention product %r" % which)
+        rows, cols = shapes[which]
+        out = np.empty((nb, hr, rows, cols), dtype=np.float64)
+        rc = self.lib.orc_attn(which, enc, nb, nh, sq, sk, d, p, r, _ptr(T1), _ptr(T2),
+                               out.ctypes.data)
+        if rc != 0:
+            raise ValueError("bad attention oracle arguments")
+        return out
+
     def round_bf16(self, x) -> np.ndarray:
         """Round fp64 values to bf16 (nearest, ties to even); returns uint16 bit patterns."""
         x = np.ascontiguousarray(x, dtype=np.float64)
@@ -331,6 +356,10 @@ def linear_samples(sig, op, X, W, dY, p, r, ii, jj, M=None, K=None, N=None):
 
 def round_bf16(x) -> np.ndarray:
     return default().round_bf16(x)
+
+
+def attn(which, T1, T2, p, r, sq, sk, d):
+    return default().attn(which, T1, T2, p, r, sq, sk, d)
 
 
 def mesh_coord(nodes, gpus=None, node=0, gpu=0):

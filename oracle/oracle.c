@@ -477,6 +477,86 @@ int orc_nd_linear_samples(int op, int enc, int64_t M, int64_t K, int64_t N, int 
     return run_samples(&pl, op, enc, K, N, X, W, dY, n, ii, jj, out);
 }
 
+/* ------------------------------ attention core under a head split ----- */
+/*
+ * Multi-head attention reduces to batched matrix products (Sec. 2). Tensors
+ * are contiguous [batch][heads][rows][cols]; with the head dimension split
+ * over p devices (the balanced split above) device r holds heads
+ * [h0, h0 + hr) of every operand and computes, per batch b and local head
+ * h (global head h0 + h), the products below. Outputs are [batch][hr][.][.].
+ *
+ *   ORC_ATT_S   S[i][j]  = sum_d Q[i][d]  K[j][d]     (scores)
+ *   ORC_ATT_O   O[i][d]  = sum_j P[i][j]  V[j][d]     (context)
+ *   ORC_ATT_DQ  dQ[i][d] = sum_j dS[i][j] K[j][d]
+ *   ORC_ATT_DK  dK[j][d] = sum_i dS[i][j] Q[i][d]
+ *   ORC_ATT_DP  dP[i][j] = sum_d dO[i][d] V[j][d]
+ *   ORC_ATT_DV  dV[j][d] = sum_i P[i][j]  dO[i][d]
+ *
+ * Arguments: the two operands in the order written (e.g. dS then K), with
+ * sq, sk and d the query length, key length and head dimension.
+ */
+enum { ORC_ATT_S = 0, ORC_ATT_O = 1, ORC_ATT_DQ = 2, ORC_ATT_DK = 3, ORC_ATT_DP = 4,
+       ORC_ATT_DV = 5 };
+
+/* Rows and columns of one output matrix, and the shapes of the operands. */
+static int att_shapes(int which, int64_t sq, int64_t sk, int64_t d, int64_t *orow,
+                      int64_t *ocol, int64_t *r1, int64_t *c1, int64_t *r2, int64_t *c2)
+{
+    switch (which) {
+    case ORC_ATT_S:  *orow = sq; *ocol = sk; *r1 = sq; *c1 = d;  *r2 = sk; *c2 = d;  return 0;
+    case ORC_ATT_O:  *orow = sq; *ocol = d;  *r1 = sq; *c1 = sk; *r2 = sk; *c2 = d;  return 0;
+    case ORC_ATT_DQ: *orow = sq; *ocol = d;  *r1 = sq; *c1 = sk; *r2 = sk; *c2 = d;  return 0;
+    case ORC_ATT_DK: *orow = sk; *ocol = d;  *r1 = sq; *c1 = sk; *r2 = sq; *c2 = d;  return 0;
+    case ORC_ATT_DP: *orow = sq; *ocol = sk; *r1 = sq; *c1 = d;  *r2 = sk; *c2 = d;  return 0;
+    case ORC_ATT_DV: *orow = sk; *ocol = d;  *r1 = sq; *c1 = sk; *r2 = sq; *c2 = d;  return 0;
+    }
+    return -1;
+}
+
+int orc_attn(int which, int enc, int64_t nb, int64_t nh, int64_t sq, int64_t sk,
+             int64_t d, int64_t p, int64_t r, const void *T1, const void *T2,
+             double *out)
+{
+    int64_t orow, ocol, r1, c1, r2, c2, h0, hr;
+    if (att_shapes(which, sq, sk, d, &orow, &ocol, &r1, &c1, &r2, &c2) != 0) return -1;
+    if (enc != ORC_IN_BF16 && enc != ORC_IN_F32) return -1;
+    if (p < 1 || r < 0 || r >= p || nb < 0 || nh < 0) return -1;
+    orc_split(nh, p, r, &h0, &hr);
+    const int64_t s1 = r1 * c1, s2 = r2 * c2;   /* elements per (batch, head) matrix */
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t b = 0; b < nb; ++b)
+        for (int64_t h = 0; h < hr; ++h) {
+            const int64_t m1 = (b * nh + h0 + h) * s1, m2 = (b * nh + h0 + h) * s2;
+            double *o = out + (b * hr + h) * orow * ocol;
+            for (int64_t i = 0; i < orow; ++i)
+                for (int64_t j = 0; j < ocol; ++j) {
+                    double acc = 0.0;
+                    switch (which) {
+                    case ORC_ATT_S:   /* Q[i][t] K[j][t] */
+                        for (int64_t t = 0; t < d; ++t)
+                            acc += decode(T1, enc, m1 + i * c1 + t) * decode(T2, enc, m2 + j * c2 + t);
+                        break;
+                    case ORC_ATT_O:   /* P[i][t] V[t][j] */
+                    case ORC_ATT_DQ:  /* dS[i][t] K[t][j] */
+                        for (int64_t t = 0; t < sk; ++t)
+                            acc += decode(T1, enc, m1 + i * c1 + t) * decode(T2, enc, m2 + t * c2 + j);
+                        break;
+                    case ORC_ATT_DK:  /* dS[t][i] Q[t][j] */
+                    case ORC_ATT_DV:  /* P[t][i] dO[t][j] */
+                        for (int64_t t = 0; t < sq; ++t)
+                            acc += decode(T1, enc, m1 + t * c1 + i) * decode(T2, enc, m2 + t * c2 + j);
+                        break;
+                    case ORC_ATT_DP:  /* dO[i][t] V[j][t] */
+                        for (int64_t t = 0; t < d; ++t)
+                            acc += decode(T1, enc, m1 + i * c1 + t) * decode(T2, enc, m2 + j * c2 + t);
+                        break;
+                    }
+                    o[i * ocol + j] = acc;
+                }
+        }
+    return 0;
+}
+
 /*
  * Round fp64 values to bfloat16 (8 significant bits, round to nearest, ties
  * to even) and return the 16-bit patterns. Used where a bf16 output of the
