@@ -289,6 +289,97 @@ def report_workload(cid, ranks, reps):
             "calls": rows}
 
 
+def report_attention(r, reps):
+    """Per-call throughput of workload 7 (the attention core under a head
+    split) on device r: the four attention calls, each replayed from a HIP
+    graph over three rotating input sets. Returns one dict for the JSON line."""
+    import torch
+    from paper_2301_06813_amd import inputs, sbp, workloads
+    wc = workloads.attention_core()
+    B, H, S, D, p = wc.batch, wc.heads, wc.seq, wc.head_dim, wc.p
+    h0, hr = sbp_split(H, p, r)
+    stream = torch.cuda.Stream()
+    sets = []
+    for i in range(3):
+        sd = wc.seed_base + 10 * i
+        act = inputs.randn((B, S, 3, H, D), 1.0, sd + 1, torch.bfloat16, "cuda")
+        logits = inputs.randn((B, hr, S, S), 1.0, sd + 2, torch.float32, "cuda")
+        t = dict(Q=act[:, :, 0].permute(0, 2, 1, 3), K=act[:, :, 1].permute(0, 2, 1, 3),
+                 V=act[:, :, 2].permute(0, 2, 1, 3), act=act,
+                 P=torch.softmax(logits, -1).to(torch.bfloat16),
+                 dS=inputs.randn((B, hr, S, S), 1.0, sd + 3, torch.bfloat16, "cuda"),
+                 dO=inputs.randn((B, hr, S, D), 1.0, sd + 4, torch.bfloat16, "cuda"))
+        del logits
+        for k, shp in (("S", (B, hr, S, S)), ("O", (B, hr, S, D)), ("dQ", (B, hr, S, D)),
+                       ("dK", (B, hr, S, D)), ("dP", (B, hr, S, S)), ("dV", (B, hr, S, D))):
+            t["o_" + k] = torch.empty(shp, dtype=torch.bfloat16, device="cuda")
+        sets.append(t)
+    G = lambda x: sbp.view4(x, sbp.SBP_GLOBAL)
+    L = lambda x: sbp.view4(x, sbp.SBP_LOCAL)
+    calls = {
+        "scores": (lambda t, s: sbp.sbp_attn_scores(G(t["Q"]), G(t["K"]), L(t["o_S"]), p, r, s),
+                   [("S = Q K^T", S, S, D)]),
+        "context": (lambda t, s: sbp.sbp_attn_context(L(t["P"]), G(t["V"]), L(t["o_O"]), p, r, s),
+                    [("O = P V", S, D, S)]),
+        "scores_bwd": (lambda t, s: sbp.sbp_attn_scores_bwd(L(t["dS"]), G(t["Q"]), G(t["K"]),
+                                                            L(t["o_dQ"]), L(t["o_dK"]), p, r, s),
+                       [("dQ = dS K", S, D, S), ("dK = dS^T Q", S, D, S)]),
+        "context_bwd": (lambda t, s: sbp.sbp_attn_context_bwd(L(t["dO"]), L(t["P"]), G(t["V"]),
+                                                              L(t["o_dP"]), L(t["o_dV"]), p, r, s),
+                        [("dP = dO V^T", S, S, D), ("dV = P^T dO", S, D, S)]),
+    }
+    rows = []
+    for name, (fn, prods) in calls.items():
+        it = [0]
+
+        def call():
+            t = sets[it[0] % len(sets)]
+            it[0] += 1
+            fn(t, stream.cuda_stream)
+        with torch.cuda.stream(stream):
+            call()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                for _ in range(reps):
+                    call()
+        g.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(3):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        us = t0.elapsed_time(t1) * 1e3 / (3 * reps)
+        fl = sum(2.0 * B * hr * m * n * k for _, m, n, k in prods)
+        by = sum(2.0 * B * hr * (m * k + k * n + m * n) for _, m, n, k in prods)
+        rows.append({"call": name, "products": ["%s %dx%dx%d x%d" % (d, m, n, k, B * hr)
+                                                for d, m, n, k in prods],
+                     "us": us, "tflops": fl / us / 1e6,
+                     "pct_of_bf16_peak": 100.0 * fl / us / 1e6 / BF16_PEAK_TFLOPS,
+                     "algorithmic_gbs": by / us / 1e3,
+                     "roofline_min_us": max(fl / BF16_PEAK_TFLOPS / 1e6, by / HBM_PEAK_GBS / 1e3)})
+        log("%-12s %7.1f us %6.0f TFLOP/s %6.0f GB/s %s" % (name, us, fl / us / 1e6, by / us / 1e3,
+                                                           ", ".join(rows[-1]["products"])))
+    tot_us = sum(x["us"] for x in rows)
+    tot_fl = sum(x["tflops"] * x["us"] * 1e6 for x in rows)
+    return {"metric": "local-shard GEMM TFLOP/s (fwd+bwd) per SBP signature; % of bf16 MFMA peak",
+            "value": tot_fl / tot_us / 1e6, "unit": "TFLOP/s", "n_gpus": 1,
+            "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": wc.name, "batch": B, "heads": H, "seq": S, "head_dim": D,
+                       "p": p, "rank": r, "local_heads": hr,
+                       "mode": "per-call hip_graph replay"},
+            "calls": rows}
+
+
+def sbp_split(D, p, r):
+    """(offset, length) of rank r's balanced block of D over p (the library's rule)."""
+    from paper_2301_06813_amd import sbp
+    s = sbp.sbp_shard_index(sbp.split(0, p, r), D, 1)
+    return s.row_off, s.rows
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -300,9 +391,9 @@ def main():
     ap.add_argument("--dump", default=None, help="write per-launch shapes and durations (JSON)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (scale for HBM counters)")
-    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 4, 5, 6),
-                    help="5 (default): the 24-layer step; 2-4: per-call report of that "
-                         "workload's local products")
+    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 4, 5, 6, 7),
+                    help="5 (default): the 24-layer step; 2-4, 6: per-call report of that "
+                         "workload's local products; 7: the attention core")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build measures rank r's local products on a "
@@ -323,6 +414,9 @@ def main():
                           "copies": 5}))
         return
     sbp.lib()
+    if args.workload == 7:
+        print(json.dumps(report_attention(0, reps=10)))
+        return
     if args.workload != 5:
         ranks = {4: (0, 1), 6: ((0, 0, 0),)}.get(args.workload, (0,))
         print(json.dumps(report_workload(args.workload, ranks, reps=10)))

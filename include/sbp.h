@@ -281,6 +281,58 @@ int sbp_nd_linear_bwd(const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
                       sbp_view_t *dW, sbp_nd_layout_t *ldw_out,
                       hipStream_t stream);
 
+/* ------------------------------ attention core under a head split --- */
+
+/* A strided 4-D view [batch][heads][rows][cols]: element (b, h, i, j) is at
+ * data + b*stride_b + h*stride_h + i*ld + j (elements). Views into a fused
+ * activation -- e.g. the Q, K or V part of a QKV projection output laid out
+ * [batch][seq][3][heads][head_dim] -- have stride_h = head_dim and ld =
+ * 3*heads*head_dim. scope: SBP_GLOBAL (inputs) -- heads counts all H heads
+ * and the call takes rank r's heads; SBP_LOCAL -- heads counts rank r's
+ * heads only; outputs always hold rank r's heads (SBP_ACCUMULATE adds to an
+ * fp32 output, as for the 2-D calls). */
+typedef struct {
+    void *data;
+    int64_t batch, heads, rows, cols;
+    int64_t stride_b, stride_h, ld;
+    int32_t dtype; /* sbp_dtype_t */
+    int32_t scope; /* sbp_scope_t */
+} sbp_view4_t;
+
+/* Multi-head attention reduces to batched matrix products (Sec. 2). Under a
+ * split of the head dimension over p devices (heads split(H, p, r), the
+ * balanced rule), every operand and output is Split on heads and each
+ * device multiplies its own heads: one product per (batch, local head), no
+ * partial sums. Inputs are bf16 (SBP_ERR_DTYPE otherwise); outputs bf16
+ * (rounded to nearest even) or fp32. Softmax, its scale and masking are not
+ * part of these calls.
+ *
+ *   sbp_attn_scores       S  = Q K^T    Q: [B][H][Sq][D], K: [B][H][Sk][D]
+ *                                       -> S: [B][H_r][Sq][Sk]
+ *   sbp_attn_context      O  = P V      P: [B][H][Sq][Sk], V: [B][H][Sk][D]
+ *                                       -> O: [B][H_r][Sq][D]
+ *   sbp_attn_scores_bwd   dQ = dS K, dK = dS^T Q (dS like S; dQ like Q, dK
+ *                         like K, each over rank r's heads)
+ *   sbp_attn_context_bwd  dP = dO V^T, dV = P^T dO (dO like O; dP like P, dV
+ *                         like V)
+ *
+ * Errors: SBP_ERR_NULL, SBP_ERR_LAYOUT (p < 1 or r outside [0, p)),
+ * SBP_ERR_SHAPE (extents that disagree, ld < cols, a negative or too large
+ * extent or stride, an output whose elements overlap one another, or an
+ * output of the wrong shape), SBP_ERR_DTYPE, SBP_ERR_ALIGN, SBP_ERR_ALIAS
+ * (an output's span overlaps an input's or the other output's span),
+ * SBP_ERR_HIP. */
+int sbp_attn_scores(const sbp_view4_t *Q, const sbp_view4_t *K, sbp_view4_t *S,
+                    int32_t p, int32_t r, hipStream_t stream);
+int sbp_attn_context(const sbp_view4_t *P, const sbp_view4_t *V, sbp_view4_t *O,
+                     int32_t p, int32_t r, hipStream_t stream);
+int sbp_attn_scores_bwd(const sbp_view4_t *dS, const sbp_view4_t *Q,
+                        const sbp_view4_t *K, sbp_view4_t *dQ, sbp_view4_t *dK,
+                        int32_t p, int32_t r, hipStream_t stream);
+int sbp_attn_context_bwd(const sbp_view4_t *dO, const sbp_view4_t *P,
+                         const sbp_view4_t *V, sbp_view4_t *dP, sbp_view4_t *dV,
+                         int32_t p, int32_t r, hipStream_t stream);
+
 /* --------------------------------------------------------- utilities --- */
 
 /* Static description of an error code (never NULL). */
@@ -365,6 +417,14 @@ int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits,
  * Clearing the plan override (tile_m = 0) also resets this to mode 0.
  * Errors: SBP_ERR_SHAPE for a mode outside [0, 2] or splits_w < 1. */
 int sbp_set_bwd_override(int32_t mode, int32_t splits_w);
+
+/* Restricts the plan override of sbp_set_plan_override to the products of
+ * the orientations in mask (bit 0 forward / Y = X W, bit 1 backward-data /
+ * A B^T, bit 2 backward-weight / A^T B); the others keep their own plans
+ * (tuning one product of a two-product call). Clearing the plan override
+ * (tile_m = 0) resets the mask to 7. Errors: SBP_ERR_SHAPE for a mask
+ * outside [1, 7]. */
+int sbp_set_override_orients(int32_t mask);
 
 #ifdef __cplusplus
 }

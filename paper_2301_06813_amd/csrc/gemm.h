@@ -28,6 +28,11 @@ struct Gemm {
     int64_t ldc;
     int64_t m, n, k;
     int accumulate = 0;    // fp32 output only: C += product instead of C = product
+    // batched products (attention core): batches x heads independent
+    // products; element strides between consecutive batches / heads of A, B, C
+    int64_t batches = 1, heads = 1;
+    int64_t sa_b = 0, sa_h = 0, sb_b = 0, sb_h = 0, sc_b = 0, sc_h = 0;
+    int64_t nbatch() const { return batches * heads; }
 };
 
 struct Plan {
@@ -60,6 +65,7 @@ Plan plan_bf16(const Gemm &g);
 bool tile_supported(int bm, int bn, bool dma);
 void set_override(int bm, int bn, int splits, int kernel);   // bm = 0 clears
 void set_override_occ(int occ);                              // 0: one workgroup per item
+void set_override_orients(int mask);   // bit o: the override applies to orientation o
 void set_bwd_override(int mode, int splits_w);   // 0 default, 1 separate, 2 grouped
 bool override_supported(int bm, int bn, int kernel);
 int kernel_code(const Plan &p);   // kernel code of a plan, as sbp_plan reports it

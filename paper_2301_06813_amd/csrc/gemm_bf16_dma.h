@@ -320,8 +320,14 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     const int wm = sw / WGN, wn = sw % WGN;
 
     const int tiles = g.tiles_m * g.tiles_n;
-    const int split = L / tiles;
-    const int t = L % tiles;
+    // batch item (the attention core's batched products; 0 otherwise)
+    const int per_b = tiles * g.splits;
+    const uint16_t *Ab, *Bb;
+    void *Cb;
+    batch_bases<OUT_F32>(g, L / per_b, &Ab, &Bb, &Cb);
+    const int Lb = L % per_b;
+    const int split = Lb / tiles;
+    const int t = Lb % tiles;
     constexpr int GROUP = SBP_TILE_GROUP;
     const int grp = t / (GROUP * g.tiles_n);
     const int first_m = grp * GROUP;
@@ -341,8 +347,8 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     auto issue = [&](int kb, int stage) {
         char *base = smem + stage * STAGE;
         const int k0 = k_begin + kb * BKD;
-        TA::issue(g.A, g.lda, m0, g.m, k0, k_lim, base, wave, lane);
-        TB::issue(g.B, g.ldb, n0, g.n, k0, k_lim, base + A_BYTES, wave, lane);
+        TA::issue(Ab, g.lda, m0, g.m, k0, k_lim, base, wave, lane);
+        TB::issue(Bb, g.ldb, n0, g.n, k0, k_lim, base + A_BYTES, wave, lane);
     };
 
     f32x16 acc[MI][NI];
@@ -482,9 +488,9 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
             store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n, g.n % 4 == 0);
         else if (OUT_F32 && g.accumulate)
             store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
-                      g.C, g.ldc, (bool)g.vec_c4);
+                      Cb, g.ldc, (bool)g.vec_c4);
         else
-            store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, g.C, g.ldc,
+            store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, Cb, g.ldc,
                       (bool)g.vec_c4);
         return;
     }
@@ -526,10 +532,10 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
             store_staged<BM, BN, LD, 64 * NW, true>(tile, ws_out, g.n, g.m, g.n, m0, n0,
                                                     g.n % 4 == 0, tid);
         else if (OUT_F32 && g.accumulate)
-            store_staged<BM, BN, LD, 64 * NW, OUT_F32, OUT_F32>(tile, g.C, g.ldc, g.m, g.n, m0,
+            store_staged<BM, BN, LD, 64 * NW, OUT_F32, OUT_F32>(tile, Cb, g.ldc, g.m, g.n, m0,
                                                                 n0, g.vec_c4, tid);
         else
-            store_staged<BM, BN, LD, 64 * NW, OUT_F32>(tile, g.C, g.ldc, g.m, g.n, m0, n0,
+            store_staged<BM, BN, LD, 64 * NW, OUT_F32>(tile, Cb, g.ldc, g.m, g.n, m0, n0,
                                                        OUT_F32 ? g.vec_c4 : g.vec_c8, tid);
         __syncthreads();   // the staged tile is free again
         return;
@@ -568,9 +574,9 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n);
     else if (OUT_F32 && g.accumulate)
         store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
-                  g.C, g.ldc);
+                  Cb, g.ldc);
     else
-        store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, g.C, g.ldc);
+        store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, Cb, g.ldc);
 }
 
 
@@ -586,7 +592,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG,
                              (Occupancy<BM, BN, BKD, NS, WGM * WGN * KG, KG>::VALUE))
 void gemm_bf16_dma_kernel(GemmArgs g) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
-    const int total = g.tiles_m * g.tiles_n * g.splits;
+    const int total = g.tiles_m * g.tiles_n * g.splits * g.nbatch;
     for (int v = blockIdx.x; v < total; v += gridDim.x) {
         // a later item refills the pipeline's LDS: every wave must be done
         // reading it (the direct epilogue does not end with a barrier)
@@ -608,8 +614,8 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG,
                              (Occupancy<BM, BN, BKD, NS, WGM * WGN * KG, KG>::VALUE))
 void gemm_bf16_dma_bwd_kernel(GemmArgs gd, GemmArgs gw, int data_first) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
-    const int wd = gd.tiles_m * gd.tiles_n * gd.splits;
-    const int ww = gw.tiles_m * gw.tiles_n * gw.splits;
+    const int wd = gd.tiles_m * gd.tiles_n * gd.splits * gd.nbatch;
+    const int ww = gw.tiles_m * gw.tiles_n * gw.splits * gw.nbatch;
     const int b = blockIdx.x;
     const bool is_data = data_first ? (b < wd) : (b >= ww);
     if (is_data) {

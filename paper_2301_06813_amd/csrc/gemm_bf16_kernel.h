@@ -71,7 +71,29 @@ struct GemmArgs {
     int32_t vec_c4, vec_c8;     // C's base and ldc allow aligned 16-byte stores of
                                 // 4 fp32 / 8 bf16 elements
     int32_t accumulate;         // fp32 C: add the product to C's contents
+    // Batched products (the attention core): nbatch = batches x heads
+    // independent m x n x k products; product z = b * heads + h reads A at
+    // A + b sa_b + h sa_h (elements), likewise B, and writes C at
+    // C + b sc_b + h sc_h. nbatch = 1 for a single product. Batched launches
+    // never split the reduction.
+    int32_t nbatch, heads;
+    int64_t sa_b, sa_h, sb_b, sb_h, sc_b, sc_h;
 };
+
+// Operand and output bases of batch item z (uniform per work item).
+template <bool OUT_F32>
+__device__ __forceinline__ void batch_bases(const GemmArgs &g, int z, const uint16_t **A,
+                                            const uint16_t **B, void **C) {
+    *A = g.A;
+    *B = g.B;
+    *C = g.C;
+    if (g.nbatch > 1) {
+        const int64_t zb = z / g.heads, zh = z % g.heads;
+        *A += zb * g.sa_b + zh * g.sa_h;
+        *B += zb * g.sb_b + zh * g.sb_h;
+        *C = static_cast<char *>(g.C) + (zb * g.sc_b + zh * g.sc_h) * (OUT_F32 ? 4 : 2);
+    }
+}
 
 // Byte offset of 16-byte chunk c (0..7) of LDS row `row`.
 __device__ __forceinline__ uint32_t lds_off(int row, int c) {
@@ -248,9 +270,14 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     const int wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // ---- which tile and which reduction range
+    // ---- which batch item, tile and reduction range
     const int tiles = g.tiles_m * g.tiles_n;
-    const int L = remap_xcd(blockIdx.x, tiles * g.splits);
+    const int per_b = tiles * g.splits;
+    const int Lz = remap_xcd(blockIdx.x, per_b * g.nbatch);
+    const int L = Lz % per_b;
+    const uint16_t *Ab, *Bb;
+    void *Cb;
+    batch_bases<OUT_F32>(g, Lz / per_b, &Ab, &Bb, &Cb);
     const int split = L / tiles;
     const int t = L % tiles;
     // grouped order: runs of GROUP tile-rows, column-major inside a run
@@ -275,10 +302,10 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     const bool b_in = vb && (n0 + BN <= g.n);
     auto load_tiles = [&](int k0) {
         const bool k_in = (k0 + BK <= k_lim);
-        if (a_in && k_in) ta.load_full(g.A, g.lda, m0, k0, tid);
-        else ta.load_edge(g.A, g.lda, m0, g.m, k0, k_lim, tid, va);
-        if (b_in && k_in) tb.load_full(g.B, g.ldb, n0, k0, tid);
-        else tb.load_edge(g.B, g.ldb, n0, g.n, k0, k_lim, tid, vb);
+        if (a_in && k_in) ta.load_full(Ab, g.lda, m0, k0, tid);
+        else ta.load_edge(Ab, g.lda, m0, g.m, k0, k_lim, tid, va);
+        if (b_in && k_in) tb.load_full(Bb, g.ldb, n0, k0, tid);
+        else tb.load_edge(Bb, g.ldb, n0, g.n, k0, k_lim, tid, vb);
     };
 
     f32x16 acc[MI][NI];
@@ -367,10 +394,10 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
                     const int row = rbase + 8 * (r >> 2) + (r & 3);
                     if (row < g.m) {
                         if constexpr (OUT_F32) {
-                            float *C = reinterpret_cast<float *>(g.C) + (int64_t)row * g.ldc + col;
+                            float *C = reinterpret_cast<float *>(Cb) + (int64_t)row * g.ldc + col;
                             *C = g.accumulate ? *C + acc[i][j][r] : acc[i][j][r];
                         } else {
-                            uint16_t *C = reinterpret_cast<uint16_t *>(g.C);
+                            uint16_t *C = reinterpret_cast<uint16_t *>(Cb);
                             C[(int64_t)row * g.ldc + col] = f32_to_bf16_bits(acc[i][j][r]);
                         }
                     }

@@ -124,19 +124,32 @@ static inline sbpk::GemmArgs make_args(const Gemm &g, const Plan &p, float *ws) 
     a.splits = p.splits;
     a.kchunk = p.kblk_per_split * 64;
     a.ws = ws;
-    a.vec_a = ((reinterpret_cast<uintptr_t>(g.A) & 15) == 0) && (g.lda % 8 == 0);
-    a.vec_b = ((reinterpret_cast<uintptr_t>(g.B) & 15) == 0) && (g.ldb % 8 == 0);
-    const bool c16 = (reinterpret_cast<uintptr_t>(g.C) & 15) == 0;
+    const bool batch_a = g.nbatch() == 1 || (g.sa_b % 8 == 0 && g.sa_h % 8 == 0);
+    const bool batch_b = g.nbatch() == 1 || (g.sb_b % 8 == 0 && g.sb_h % 8 == 0);
+    a.vec_a = ((reinterpret_cast<uintptr_t>(g.A) & 15) == 0) && (g.lda % 8 == 0) && batch_a;
+    a.vec_b = ((reinterpret_cast<uintptr_t>(g.B) & 15) == 0) && (g.ldb % 8 == 0) && batch_b;
+    // every batch item's output base must keep the 16-byte alignment
+    const int64_t es = g.out_dtype == DT_F32 ? 4 : 2;
+    const bool c16 = (reinterpret_cast<uintptr_t>(g.C) & 15) == 0 &&
+                     (g.nbatch() == 1 || ((g.sc_b * es) % 16 == 0 && (g.sc_h * es) % 16 == 0));
     a.vec_c4 = c16 && (g.ldc % 4 == 0);
     a.vec_c8 = c16 && (g.ldc % 8 == 0);
     a.accumulate = g.accumulate;
+    a.nbatch = (int32_t)g.nbatch();
+    a.heads = (int32_t)g.heads;
+    a.sa_b = g.sa_b;
+    a.sa_h = g.sa_h;
+    a.sb_b = g.sb_b;
+    a.sb_h = g.sb_h;
+    a.sc_b = g.sc_b;
+    a.sc_h = g.sc_h;
     return a;
 }
 
 template <bool AK, bool BK_>
 static hipError_t launch_orient(const Gemm &g, const Plan &p, float *ws, hipStream_t s) {
     const sbpk::GemmArgs a = make_args(g, p, ws);
-    const int items = a.tiles_m * a.tiles_n * a.splits;
+    const int items = a.tiles_m * a.tiles_n * a.splits * a.nbatch;
     // with splits the GEMM writes fp32 partials, whatever the output dtype
     hipError_t e = (g.out_dtype == DT_F32 || p.splits > 1)
                        ? launch_tile<AK, BK_, true>(p, a, items, s)

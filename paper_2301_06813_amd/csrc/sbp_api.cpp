@@ -15,6 +15,7 @@
 #include <utility>
 
 #include "../../include/sbp.h"
+#include "api_internal.h"
 #include "gemm.h"
 
 namespace {
@@ -537,6 +538,10 @@ int linear_bwd(const sbp_view_t *dY, const L *ldy, const sbp_view_t *X, const L 
 
 }  // namespace
 
+namespace sbpa {
+int run_gemm(const sbpi::Gemm &g, hipStream_t s) { return run(g, s); }
+}  // namespace sbpa
+
 extern "C" {
 
 int sbp_shard_index(const sbp_layout_t *l, int64_t rows, int64_t cols, sbp_shard_t *out) {
@@ -765,12 +770,19 @@ int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits, int32_
         sbpi::set_override(0, 0, 1, 0);
         sbpi::set_override_occ(0);
         sbpi::set_bwd_override(0, 1);
+        sbpi::set_override_orients(7);
         return SBP_OK;
     }
     if (splits < 1 || wgs_per_cu < 0 || wgs_per_cu > 8) return SBP_ERR_SHAPE;
     if (!sbpi::override_supported(tile_m, tile_n, kernel)) return SBP_ERR_SHAPE;
     sbpi::set_override(tile_m, tile_n, splits, kernel);
     sbpi::set_override_occ(wgs_per_cu);
+    return SBP_OK;
+}
+
+int sbp_set_override_orients(int32_t mask) {
+    if (mask < 1 || mask > 7) return SBP_ERR_SHAPE;
+    sbpi::set_override_orients(mask);
     return SBP_OK;
 }
 

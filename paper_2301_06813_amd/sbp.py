@@ -37,7 +37,8 @@ EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd
            "sbp_plan_bwd", "sbp_set_plan_override", "sbp_set_bwd_override", "sbp_profile_begin",
            "sbp_profile_end", "sbp_mesh_coords", "sbp_nd_shard_index", "sbp_nd_signature",
            "sbp_nd_linear_fwd", "sbp_nd_linear_bwd_data", "sbp_nd_linear_bwd_weight",
-           "sbp_nd_linear_bwd")
+           "sbp_nd_linear_bwd", "sbp_attn_scores", "sbp_attn_context", "sbp_attn_scores_bwd",
+           "sbp_attn_context_bwd", "sbp_set_override_orients")
 
 SBP_MAX_MESH_DIMS = 4
 
@@ -81,6 +82,13 @@ class sbp_nd_layout_t(ctypes.Structure):
 
 class sbp_view_t(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("ld", ctypes.c_int64), ("dtype", ctypes.c_int32), ("scope", ctypes.c_int32)]
+
+
+class sbp_view4_t(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("batch", ctypes.c_int64), ("heads", ctypes.c_int64),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
                 ("ld", ctypes.c_int64), ("dtype", ctypes.c_int32), ("scope", ctypes.c_int32)]
 
 
@@ -157,6 +165,7 @@ def lib():
                                P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_int32)]
         L.sbp_set_plan_override.argtypes = [ctypes.c_int32] * 5
         L.sbp_set_bwd_override.argtypes = [ctypes.c_int32] * 2
+        L.sbp_set_override_orients.argtypes = [ctypes.c_int32]
         L.sbp_profile_begin.argtypes = [ctypes.c_int]
         L.sbp_profile_end.argtypes = [ctypes.c_void_p, ctypes.c_char_p, ctypes.c_int]
         L.sbp_plan_bwd.argtypes = ([ctypes.c_int64] * 3 + [ctypes.c_int32] + [ctypes.c_int64] * 3 +
@@ -171,6 +180,12 @@ def lib():
                                        ctypes.c_void_p]
         L.sbp_nd_linear_bwd.argtypes = [P(sbp_view_t), ND, P(sbp_view_t), ND, P(sbp_view_t), ND,
                                         P(sbp_view_t), ND, P(sbp_view_t), ND, ctypes.c_void_p]
+        V4 = P(sbp_view4_t)
+        for fn in ("sbp_attn_scores", "sbp_attn_context"):
+            getattr(L, fn).argtypes = [V4, V4, V4, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+        for fn in ("sbp_attn_scores_bwd", "sbp_attn_context_bwd"):
+            getattr(L, fn).argtypes = [V4, V4, V4, V4, V4, ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_void_p]
         for fn in EXPORTS:
             if fn != "sbp_strerror":
                 getattr(L, fn).restype = ctypes.c_int
@@ -196,6 +211,23 @@ def view(t, scope=SBP_GLOBAL) -> sbp_view_t:
         raise TypeError("unsupported dtype %s" % t.dtype)
     ld = max(t.stride(0), t.shape[1], 1)
     return sbp_view_t(t.data_ptr(), t.shape[0], t.shape[1], ld, dt, scope)
+
+
+def view4(t, scope=SBP_GLOBAL) -> sbp_view4_t:
+    """sbp_view4_t of a 4-D torch tensor [batch][heads][rows][cols] (any
+    strides with unit column stride; e.g. a permuted view into a fused QKV
+    activation)."""
+    import torch
+    if t.dim() != 4:
+        raise ValueError("view4 needs a 4-D tensor")
+    if t.stride(3) != 1 and t.shape[3] > 1:
+        raise ValueError("views need unit column stride")
+    dt = {torch.bfloat16: SBP_BF16, torch.float32: SBP_F32}.get(t.dtype)
+    if dt is None:
+        raise TypeError("unsupported dtype %s" % t.dtype)
+    ld = max(t.stride(2), t.shape[3], 1)
+    return sbp_view4_t(t.data_ptr(), t.shape[0], t.shape[1], t.shape[2], t.shape[3],
+                       t.stride(0), t.stride(1), ld, dt, scope)
 
 
 def raw_view(ptr, rows, cols, ld, dtype, scope=SBP_GLOBAL) -> sbp_view_t:
@@ -318,6 +350,35 @@ def sbp_nd_linear_bwd(dY, ldy, X, lx, W, lw, dX, dW, stream=None):
     return sx, sw
 
 
+# ------------------------------------------------------- attention core
+def _stream(stream):
+    return ctypes.c_void_p(current_stream() if stream is None else stream)
+
+
+def sbp_attn_scores(Q, K, S, p: int, r: int, stream=None):
+    """S = Q K^T per (batch, local head) under a head split over p devices."""
+    _check(lib().sbp_attn_scores(ctypes.byref(Q), ctypes.byref(K), ctypes.byref(S), p, r,
+                                 _stream(stream)))
+
+
+def sbp_attn_context(P_, V, O, p: int, r: int, stream=None):
+    """O = P V per (batch, local head)."""
+    _check(lib().sbp_attn_context(ctypes.byref(P_), ctypes.byref(V), ctypes.byref(O), p, r,
+                                  _stream(stream)))
+
+
+def sbp_attn_scores_bwd(dS, Q, K, dQ, dK, p: int, r: int, stream=None):
+    """dQ = dS K and dK = dS^T Q per (batch, local head)."""
+    _check(lib().sbp_attn_scores_bwd(ctypes.byref(dS), ctypes.byref(Q), ctypes.byref(K),
+                                     ctypes.byref(dQ), ctypes.byref(dK), p, r, _stream(stream)))
+
+
+def sbp_attn_context_bwd(dO, P_, V, dP, dV, p: int, r: int, stream=None):
+    """dP = dO V^T and dV = P^T dO per (batch, local head)."""
+    _check(lib().sbp_attn_context_bwd(ctypes.byref(dO), ctypes.byref(P_), ctypes.byref(V),
+                                      ctypes.byref(dP), ctypes.byref(dV), p, r, _stream(stream)))
+
+
 def sbp_last_hip_error() -> int:
     return lib().sbp_last_hip_error()
 
@@ -359,6 +420,12 @@ def sbp_profile_end(capacity: int):
         _check(n)
     raw = names.raw
     return [(raw[i * nl:(i + 1) * nl].split(b"\0", 1)[0].decode(), us[i]) for i in range(n)]
+
+
+def sbp_set_override_orients(mask: int) -> None:
+    """Apply the plan override only to orientations in mask (bit 0 forward,
+    1 backward-data, 2 backward-weight); cleared with the plan override."""
+    _check(lib().sbp_set_override_orients(mask))
 
 
 def sbp_set_bwd_override(mode: int, splits_w: int = 1) -> None:

@@ -81,7 +81,7 @@ def _eligible(op, L, lin):
     return int(ok(L["x"], M, K) and ok(L["dy"], M, N))
 
 
-def valid_candidates(sbp, key, tiles_n_items):
+def valid_candidates(sbp, key, tiles_n_items, max_splits=None, nbatch=1):
     """(tile_m, tile_n, splits, kernel, wgs_per_cu) plans to time for key (the
     argument order of sbp_set_plan_override)."""
     orient, f32, m, n, k, dma = key
@@ -97,13 +97,15 @@ def valid_candidates(sbp, key, tiles_n_items):
                 continue
             last = 0
             for s in SPLITS:
+                if max_splits is not None and s > max_splits:
+                    continue
                 per = -(-kblocks // min(s, kblocks))
                 eff = -(-kblocks // per)
                 if eff == last or (eff > 1 and per < 2):
                     continue
                 last = eff
-                items = tiles * eff
-                if items > 8192 or (eff > 1 and items > 4096):
+                items = tiles * eff * nbatch
+                if (items > 8192 and nbatch == 1) or (eff > 1 and items > 4096):
                     continue
                 occs = (0,) if (code == 2 or items <= 256) else (0, 1, 2)
                 for occ in occs:
@@ -174,7 +176,7 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream, single_best=None):
     """Grouped launch of each backward pair against its two products run
     separately: the sum of their tuned times (single_best, from the same run),
     else a measured pair of launches of the compiled-in plans."""
-    pairs = bwd_pairs([int(c) for c in args.workloads.split(",")])
+    pairs = bwd_pairs([int(c) for c in args.workloads.split(",") if int(c) != 7])
     log("%d distinct backward pairs" % len(pairs))
     rows = []
     for (kd, kw), (wl, lin, r) in sorted(pairs.items()):
@@ -253,6 +255,74 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream, single_best=None):
     log("wrote %s" % args.out)
 
 
+def tune_attention(args, torch, sbp, stream):
+    """Plans of the attention core's batched products (workload 7): one row per
+    distinct product, keyed with its batch count. Each product is tuned through
+    the call that holds it, with the plan override restricted to its
+    orientation (the call's other product keeps its own plan)."""
+    from . import inputs, workloads
+    wc = workloads.attention_core()
+    B, H, S, D, p = wc.batch, wc.heads, wc.seq, wc.head_dim, wc.p
+    hr = -(-H // p) if H % p else H // p      # rank 0's heads (balanced split)
+    nb = B * hr
+    sets = []
+    for i in range(3):
+        sd = wc.seed_base + 10 * i
+        act = inputs.randn((B, S, 3, H, D), 1.0, sd + 1, torch.bfloat16, "cuda")
+        t = dict(act=act, Q=act[:, :, 0].permute(0, 2, 1, 3), K=act[:, :, 1].permute(0, 2, 1, 3),
+                 V=act[:, :, 2].permute(0, 2, 1, 3),
+                 P=inputs.randn((B, hr, S, S), 1.0, sd + 2, torch.bfloat16, "cuda"),
+                 dS=inputs.randn((B, hr, S, S), 1.0, sd + 3, torch.bfloat16, "cuda"))
+        for k_, shp in (("S", (B, hr, S, S)), ("O", (B, hr, S, D)), ("dQ", (B, hr, S, D)),
+                        ("dK", (B, hr, S, D))):
+            t[k_] = torch.empty(shp, dtype=torch.bfloat16, device="cuda")
+        sets.append(t)
+    G = lambda x: sbp.view4(x, sbp.SBP_GLOBAL)
+    L = lambda x: sbp.view4(x, sbp.SBP_LOCAL)
+    calls = [  # (call, orientation mask, product key)
+        (lambda t, s: sbp.sbp_attn_scores(G(t["Q"]), G(t["K"]), L(t["S"]), p, 0, s), 2,
+         (ORIENT["bwd_data"], 0, S, S, D, 1)),
+        (lambda t, s: sbp.sbp_attn_context(L(t["P"]), G(t["V"]), L(t["O"]), p, 0, s), 1,
+         (ORIENT["fwd"], 0, S, D, S, 1)),
+        (lambda t, s: sbp.sbp_attn_scores_bwd(L(t["dS"]), G(t["Q"]), G(t["K"]), L(t["dQ"]),
+                                              L(t["dK"]), p, 0, s), 4,
+         (ORIENT["bwd_weight"], 0, S, D, S, 1)),
+    ]
+    rows = []
+    for call, mask, key in calls:
+        it = [0]
+
+        def fn():
+            t = sets[it[0] % len(sets)]
+            it[0] += 1
+            call(t, stream.cuda_stream)
+
+        def timed(plan, reps):
+            sbp.sbp_set_plan_override(*plan)
+            sbp.sbp_set_override_orients(mask)
+            try:
+                return time_plan(torch, sbp, fn, plan, reps, stream, keep=True)
+            finally:
+                sbp.sbp_set_plan_override(0, 0, 1)
+
+        cands = valid_candidates(sbp, key, None, max_splits=1, nbatch=nb)
+        timings = []
+        for plan in cands:
+            try:
+                timings.append((timed(plan, args.reps), plan))
+            except sbp.SbpError as e:
+                log("  plan %s failed: %s" % (plan, e))
+        best = pick(timings, lambda pl: timed(pl, 3 * args.reps))
+        auto = time_plan(torch, sbp, fn, (0, 0, 1, 0, 0), 3 * args.reps, stream)
+        log("attention %s m %d n %d k %d x%d: best %6.1f us %s (model plan %6.1f us), %d candidates"
+            % (list(ORIENT)[key[0]], key[2], key[3], key[4], nb, best[0], best[1], auto,
+               len(cands)))
+        rows.append((key, best[1], best[0], auto, nb))
+    del sets
+    torch.cuda.empty_cache()
+    return rows
+
+
 def pick(timings, retime, top=5, rounds=3):
     """Best plan of [(us, plan)]: the `top` fastest of the sweep are timed again
     `rounds` times at higher repetition and ranked by their median."""
@@ -267,7 +337,7 @@ def pick(timings, retime, top=5, rounds=3):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--out", default=None)
-    ap.add_argument("--workloads", default="2,3,4,5,6")
+    ap.add_argument("--workloads", default="2,3,4,5,6,7")
     ap.add_argument("--reps", type=int, default=10)
     ap.add_argument("--bwd", action="store_true", help="tune grouped backward pairs only")
     ap.add_argument("--all", action="store_true",
@@ -286,7 +356,7 @@ def main():
     if args.bwd:
         tune_bwd(args, torch, sbp, linear, workloads, stream)
         return
-    cases = product_cases([int(c) for c in args.workloads.split(",")])
+    cases = product_cases([int(c) for c in args.workloads.split(",") if int(c) != 7])
     log("%d distinct local products" % len(cases))
     single_best = {}
     rows = []
@@ -324,6 +394,10 @@ def main():
         rows.append((key, best[1], best[0], auto))
         del sets
         torch.cuda.empty_cache()
+    wl_ids = [int(c) for c in args.workloads.split(",")]
+    if 7 in wl_ids:
+        rows += [(key, plan, us, auto) + (nb,) for key, plan, us, auto, nb in
+                 tune_attention(args, torch, sbp, stream)]
     log("tuned in %.0f s" % (time.time() - t_start))
     dev = torch.cuda.get_device_properties(0)
     with open(args.out, "w") as f:
@@ -331,9 +405,12 @@ def main():
                 % (dev.name, dev.multi_processor_count))
         f.write("// orient, out_f32, m, n, k, pipelined-eligible -> tile_m, tile_n, kernel, "
                 "splits, persistent workgroups per CU; fastest measured, us (model's plan, us)\n")
-        for (orient, f32, m, n, k, dma), (bm, bn, splits, code, occ), us, auto in rows:
-            f.write("{%d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d},  // %.1f (%.1f)\n"
-                    % (orient, f32, m, n, k, dma, bm, bn, code, splits, occ, us, auto))
+        for row in rows:
+            (orient, f32, m, n, k, dma), (bm, bn, splits, code, occ), us, auto = row[:4]
+            nb = row[4] if len(row) > 4 else 1
+            batch = ", %d" % nb if nb > 1 else ""
+            f.write("{%d, %d, %d, %d, %d, %d, %d, %d, %d, %d, %d%s},  // %.1f (%.1f)\n"
+                    % (orient, f32, m, n, k, dma, bm, bn, code, splits, occ, batch, us, auto))
     log("wrote %s" % args.out)
     if args.all:
         args.out = args.out_bwd

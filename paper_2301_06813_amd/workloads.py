@@ -137,6 +137,30 @@ def transformer_3d() -> Workload:
     return Workload(6, "transformer_layer_3d_mesh2x2x2", torch.bfloat16, 8, lins, coords, mesh)
 
 
+@dataclasses.dataclass(frozen=True)
+class AttentionCore:
+    """The attention core of a Transformer layer under a head split: per
+    sequence and local head, scores S = Q K^T, context O = P V and their
+    backward products (Sec. 2: multi-head attention reduces to batched
+    matrix products)."""
+    name: str
+    batch: int        # sequences
+    heads: int        # global heads H
+    seq: int
+    head_dim: int
+    p: int            # devices splitting the heads
+    seed_base: int
+
+
+def attention_core() -> AttentionCore:
+    """Workload 7: the attention core of the 24-layer Transformer (16 heads of
+    64, sequence 1024) for 8 sequences (the 8192 tokens of workload 5), heads
+    split over 8 devices (2 per device). Q, K and V are views into a fused
+    [batch][seq][3][heads][head_dim] QKV activation drawn N(0,1); P is a
+    row-softmax of N(0,1) logits; dS and dO are N(0,1)."""
+    return AttentionCore("attention_core_h16x64_s1024_b8_p8", 8, 16, 1024, 64, 8, 7000)
+
+
 def all_workloads() -> list[Workload]:
     return tiny_fp32() + [ffn_shard(), attention_dp(), vgg_head(), transformer_step(),
                           transformer_3d()]
