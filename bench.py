@@ -391,9 +391,10 @@ def main():
     ap.add_argument("--dump", default=None, help="write per-launch shapes and durations (JSON)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (scale for HBM counters)")
-    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 4, 5, 6, 7),
-                    help="5 (default): the 24-layer step; 2-4, 6: per-call report of that "
-                         "workload's local products; 7: the attention core")
+    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 4, 5, 6, 7, 8),
+                    help="5 (default): the 24-layer step; 8: the same step with searched "
+                         "signatures; 2-4, 6: per-call report of that workload's local "
+                         "products; 7: the attention core")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build measures rank r's local products on a "
@@ -417,11 +418,12 @@ def main():
     if args.workload == 7:
         print(json.dumps(report_attention(0, reps=10)))
         return
-    if args.workload != 5:
+    if args.workload not in (5, 8):
         ranks = {4: (0, 1), 6: ((0, 0, 0),)}.get(args.workload, (0,))
         print(json.dumps(report_workload(args.workload, ranks, reps=10)))
         return
-    wl = workloads.transformer_step()
+    wl = workloads.transformer_step() if args.workload == 5 else \
+        workloads.transformer_step_searched()
     log("building step: %d linears, p=%d, rank 0" % (len(wl.linears), wl.p))
     step = Step(wl, 0)
     stream = torch.cuda.Stream()
@@ -543,7 +545,11 @@ def main():
                    "local_products_per_step": 3 * len(wl.linears),
                    "calls_per_step": n, "gflop_per_step": step.flops / 1e9,
                    "signatures": dict(collections.Counter(l.sig for l in wl.linears)),
-                   "mode": "eager" if args.eager else "hip_graph"},
+                   "mode": "eager" if args.eager else "hip_graph",
+                   **({"signature_choice": "coordinate-descent search, modelled communication "
+                       "%.2f ms per step (alpha %g s, beta %g s/B)" % (
+                           1e3 * workloads.searched_signatures()[1], workloads.XGMI_ALPHA,
+                           workloads.XGMI_BETA)} if args.workload == 8 else {})},
         "pct_of_bf16_peak": 100.0 * tflops / BF16_PEAK_TFLOPS,
         "per_signature_tflops": {s: v[1] / v[0] / 1e12 for s, v in sorted(by_sig.items())},
         "kernel_time_sum_ms": sum(v[0] for v in by_kernel.values()) * 1e3,

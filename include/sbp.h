@@ -333,6 +333,88 @@ int sbp_attn_context_bwd(const sbp_view4_t *dO, const sbp_view4_t *P,
                          const sbp_view4_t *V, sbp_view4_t *dP, sbp_view4_t *dV,
                          int32_t p, int32_t r, hipStream_t stream);
 
+/* ------------------------------------- cost model and strategy search --- */
+
+/* Collectives of the alpha-beta model (Sec. 3.1, Table 2). */
+enum {
+    SBP_COLL_ALLREDUCE = 0,      /* (2p-1) alpha + 2 (p-1)/p n beta          */
+    SBP_COLL_ALLGATHER = 1,      /* (p-1) alpha + (p-1)/p n beta             */
+    SBP_COLL_REDUCESCATTER = 2,  /* (p-1) alpha + (p-1)/p n beta             */
+    SBP_COLL_ALLTOALL = 3        /* (p-1) alpha + n beta                     */
+};
+
+/* Time of one collective over p devices for an n-byte message (the input
+ * of ReduceScatter, the output of the others, per device), latency alpha
+ * (seconds) and inverse bandwidth beta (seconds per byte): the formulas of
+ * Table 2 as printed. Pure host function. Errors: SBP_ERR_NULL,
+ * SBP_ERR_LAYOUT (p < 1, unknown collective), SBP_ERR_SHAPE (negative n,
+ * alpha or beta). */
+int sbp_collective_cost(int32_t coll, int32_t p, double n, double alpha, double beta,
+                        double *cost);
+
+/* Time to redistribute a tensor of `bytes` (global size) from 1-D state
+ * *from to 1-D state *to on the same p devices (Sec. 4.2 redistributions,
+ * Sec. 4.3 "Sources of Communication"): S(i)->S(j), i != j: AlltoAll of
+ * bytes/p; S->B: AllGather of bytes; P->S: ReduceScatter of bytes; P->B:
+ * AllReduce of bytes; every other change (B->S, B->P, S->P) and no change:
+ * 0 (local). *coll_out, if not NULL, receives the collective used, or -1.
+ * Errors: SBP_ERR_NULL, SBP_ERR_LAYOUT (bad states, p mismatch),
+ * SBP_ERR_SHAPE. */
+int sbp_boxing_cost(const sbp_layout_t *from, const sbp_layout_t *to, double bytes,
+                    double alpha, double beta, double *cost, int32_t *coll_out);
+
+/* Signature ids for the search: the rows of the table at the top of this
+ * file, in order. */
+enum { SBP_SIG_DP = 0, SBP_SIG_COL = 1, SBP_SIG_KS = 2, SBP_SIG_PB = 3, SBP_SIG_BP = 4,
+       SBP_SIG_BB = 5 };
+
+/* A chain of linear layers Y_l = X_l W_l (X_l: M x K[l], W_l: K[l] x N[l])
+ * on a 1-D mesh of p devices, one signature per layer. Between layers the
+ * previous output (M x N[l] elements; M is the same for every layer) is
+ * redistributed from layer l's output state to layer l+1's input state; an
+ * op between the two (an activation function, the attention core, which
+ * maps 3 x hidden to hidden columns) keeps the state, so K[l+1] may differ
+ * from N[l]. The network input (M x K[0]) starts in state (in_kind,
+ * in_axis) and the last output must end in (out_kind, out_axis). A
+ * Partial-sum output is never fed on as is (a nonlinearity separates the
+ * layers), so signatures with a Partial-sum X (PB) are not allowed. */
+typedef struct {
+    int32_t layers;
+    int32_t p;
+    double alpha, beta;          /* seconds, seconds per byte */
+    const int64_t *M, *K, *N;    /* per layer */
+    double act_bytes;            /* bytes per activation element */
+    double grad_bytes;           /* bytes per weight-gradient element */
+    int32_t in_kind, in_axis, out_kind, out_axis;
+    uint32_t allowed;            /* bit s: signature s may be chosen */
+} sbp_chain_t;
+
+/* Communication time of one training step of the chain under signatures
+ * sigs[0..layers): for every activation redistribution, its forward cost
+ * plus the backward cost of moving the gradient the other way (the dual
+ * states: grad of S(i) is S(i), of B is P, of P is B), plus an AllReduce of
+ * every weight gradient left Partial-sum (Sec. 4.3). Pure host function.
+ * Errors: SBP_ERR_NULL, SBP_ERR_SHAPE (layers < 1, extents), SBP_ERR_LAYOUT
+ * (p, boundary states), SBP_ERR_SIGNATURE (a signature not allowed). */
+int sbp_chain_cost(const sbp_chain_t *net, const int32_t *sigs, double *cost);
+
+/* Coordinate-descent search (Sec. 4.4): from an initial guess, each sweep
+ * sets every layer in turn to the allowed signature that minimises the
+ * chain cost with the others fixed (a change only on strict improvement, so
+ * the cost never rises); at a fixed point the run restarts from a new
+ * random guess, and the best strategy of `restarts` runs (>= 1; the first
+ * starts from all-DP where allowed) is returned in sigs_out with its cost.
+ * sweep_costs (may be NULL) receives, run after run, each run's starting
+ * cost followed by its cost after every sweep, up to max_sweeps entries;
+ * within a run the values strictly decrease until the final sweep, which
+ * changes nothing and repeats the previous value. *sweeps_out (may be
+ * NULL) receives the total count of entries.
+ * Random guesses come from splitmix64 seeded with `seed`. Pure host
+ * function. Errors: those of sbp_chain_cost, SBP_ERR_SHAPE (restarts < 1). */
+int sbp_search_strategy(const sbp_chain_t *net, int32_t restarts, uint64_t seed,
+                        int32_t *sigs_out, double *cost_out, double *sweep_costs,
+                        int32_t max_sweeps, int32_t *sweeps_out);
+
 /* --------------------------------------------------------- utilities --- */
 
 /* Static description of an error code (never NULL). */

@@ -38,7 +38,12 @@ EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd
            "sbp_profile_end", "sbp_mesh_coords", "sbp_nd_shard_index", "sbp_nd_signature",
            "sbp_nd_linear_fwd", "sbp_nd_linear_bwd_data", "sbp_nd_linear_bwd_weight",
            "sbp_nd_linear_bwd", "sbp_attn_scores", "sbp_attn_context", "sbp_attn_scores_bwd",
-           "sbp_attn_context_bwd", "sbp_set_override_orients")
+           "sbp_attn_context_bwd", "sbp_set_override_orients", "sbp_collective_cost",
+           "sbp_boxing_cost", "sbp_chain_cost", "sbp_search_strategy")
+
+SBP_COLL_ALLREDUCE, SBP_COLL_ALLGATHER, SBP_COLL_REDUCESCATTER, SBP_COLL_ALLTOALL = 0, 1, 2, 3
+SBP_SIG_DP, SBP_SIG_COL, SBP_SIG_KS, SBP_SIG_PB, SBP_SIG_BP, SBP_SIG_BB = 0, 1, 2, 3, 4, 5
+SIG_IDS = {"DP": 0, "COL": 1, "KS": 2, "PB": 3, "BP": 4, "BB": 5}
 
 SBP_MAX_MESH_DIMS = 4
 
@@ -90,6 +95,16 @@ class sbp_view4_t(ctypes.Structure):
                 ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
                 ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
                 ("ld", ctypes.c_int64), ("dtype", ctypes.c_int32), ("scope", ctypes.c_int32)]
+
+
+class sbp_chain_t(ctypes.Structure):
+    _fields_ = [("layers", ctypes.c_int32), ("p", ctypes.c_int32), ("alpha", ctypes.c_double),
+                ("beta", ctypes.c_double), ("M", ctypes.POINTER(ctypes.c_int64)),
+                ("K", ctypes.POINTER(ctypes.c_int64)), ("N", ctypes.POINTER(ctypes.c_int64)),
+                ("act_bytes", ctypes.c_double), ("grad_bytes", ctypes.c_double),
+                ("in_kind", ctypes.c_int32), ("in_axis", ctypes.c_int32),
+                ("out_kind", ctypes.c_int32), ("out_axis", ctypes.c_int32),
+                ("allowed", ctypes.c_uint32)]
 
 
 class sbp_shard_t(ctypes.Structure):
@@ -186,6 +201,14 @@ def lib():
         for fn in ("sbp_attn_scores_bwd", "sbp_attn_context_bwd"):
             getattr(L, fn).argtypes = [V4, V4, V4, V4, V4, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_void_p]
+        D = ctypes.c_double
+        L.sbp_collective_cost.argtypes = [ctypes.c_int32, ctypes.c_int32, D, D, D, P(D)]
+        L.sbp_boxing_cost.argtypes = [P(sbp_layout_t), P(sbp_layout_t), D, D, D, P(D),
+                                      P(ctypes.c_int32)]
+        L.sbp_chain_cost.argtypes = [P(sbp_chain_t), P(ctypes.c_int32), P(D)]
+        L.sbp_search_strategy.argtypes = [P(sbp_chain_t), ctypes.c_int32, ctypes.c_uint64,
+                                          P(ctypes.c_int32), P(D), P(D), ctypes.c_int32,
+                                          P(ctypes.c_int32)]
         for fn in EXPORTS:
             if fn != "sbp_strerror":
                 getattr(L, fn).restype = ctypes.c_int
@@ -377,6 +400,57 @@ def sbp_attn_context_bwd(dO, P_, V, dP, dV, p: int, r: int, stream=None):
     """dP = dO V^T and dV = P^T dO per (batch, local head)."""
     _check(lib().sbp_attn_context_bwd(ctypes.byref(dO), ctypes.byref(P_), ctypes.byref(V),
                                       ctypes.byref(dP), ctypes.byref(dV), p, r, _stream(stream)))
+
+
+# ------------------------------------------- cost model and search
+def sbp_collective_cost(coll: int, p: int, n: float, alpha: float, beta: float) -> float:
+    c = ctypes.c_double()
+    _check(lib().sbp_collective_cost(coll, p, n, alpha, beta, ctypes.byref(c)))
+    return c.value
+
+
+def sbp_boxing_cost(frm: sbp_layout_t, to: sbp_layout_t, nbytes: float, alpha: float,
+                    beta: float):
+    """(time, collective id or -1) of moving a tensor between two 1-D states."""
+    c, k = ctypes.c_double(), ctypes.c_int32()
+    _check(lib().sbp_boxing_cost(ctypes.byref(frm), ctypes.byref(to), nbytes, alpha, beta,
+                                 ctypes.byref(c), ctypes.byref(k)))
+    return c.value, k.value
+
+
+def make_chain(p, alpha, beta, M, K, N, act_bytes=2.0, grad_bytes=4.0, in_state=(0, 0),
+               out_state=(0, 0), allowed=("DP", "COL", "KS")):
+    """An sbp_chain_t (the arrays are kept alive on the returned object)."""
+    L = len(K)
+    arr = ctypes.c_int64 * L
+    net = sbp_chain_t()
+    net._M, net._K, net._N = arr(*([M] * L)), arr(*K), arr(*N)
+    net.layers, net.p, net.alpha, net.beta = L, p, alpha, beta
+    net.M, net.K, net.N = net._M, net._K, net._N
+    net.act_bytes, net.grad_bytes = act_bytes, grad_bytes
+    net.in_kind, net.in_axis = in_state
+    net.out_kind, net.out_axis = out_state
+    net.allowed = sum(1 << SIG_IDS[a] for a in allowed)
+    return net
+
+
+def sbp_chain_cost(net: sbp_chain_t, sigs) -> float:
+    a = (ctypes.c_int32 * len(sigs))(*sigs)
+    c = ctypes.c_double()
+    _check(lib().sbp_chain_cost(ctypes.byref(net), a, ctypes.byref(c)))
+    return c.value
+
+
+def sbp_search_strategy(net: sbp_chain_t, restarts: int = 16, seed: int = 0,
+                        max_sweeps: int = 4096):
+    """(signature ids, cost, per-sweep costs) of the coordinate-descent search."""
+    sigs = (ctypes.c_int32 * net.layers)()
+    cost = ctypes.c_double()
+    sweeps = (ctypes.c_double * max_sweeps)()
+    ns = ctypes.c_int32()
+    _check(lib().sbp_search_strategy(ctypes.byref(net), restarts, seed, sigs, ctypes.byref(cost),
+                                     sweeps, max_sweeps, ctypes.byref(ns)))
+    return list(sigs), cost.value, list(sweeps[:min(ns.value, max_sweeps)])
 
 
 def sbp_last_hip_error() -> int:

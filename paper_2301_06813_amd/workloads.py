@@ -120,6 +120,47 @@ def transformer_step(layers: int = 24) -> Workload:
     return Workload(5, "transformer_24L_step_rank0_p8", torch.bfloat16, 8, tuple(lins), (0,))
 
 
+# Network parameters the search assumes for one node of 8 MI355X GPUs (a
+# reading, not a measurement: the paper fits alpha and beta on its own
+# clusters): 10 us per message, and one xGMI link's ~153 GB/s per byte, as
+# a ring algorithm is bound by one link.
+XGMI_ALPHA = 10e-6
+XGMI_BETA = 1.0 / 153e9
+
+
+def searched_signatures(layers: int = 24, p: int = 8, tokens: int = 8192, restarts: int = 64,
+                        seed: int = 8000):
+    """Per-linear signatures of the 24-layer Transformer chosen by the
+    library's coordinate-descent search (Sec. 4.4) over DP, COL and KS,
+    minimising the alpha-beta communication cost (Table 2) of one step:
+    tokens enter and leave data parallel (S0); bf16 activations, fp32 weight
+    gradients. Returns (signature names, modelled seconds per step)."""
+    from . import sbp
+    dims = (("qkv", 1024, 3072), ("out", 1024, 1024), ("fc1", 1024, 4096), ("fc2", 4096, 1024))
+    K = [k for _ in range(layers) for _, k, _ in dims]
+    N = [n for _ in range(layers) for _, _, n in dims]
+    net = sbp.make_chain(p, XGMI_ALPHA, XGMI_BETA, tokens, K, N, 2.0, 4.0,
+                         (sbp.SBP_SPLIT, 0), (sbp.SBP_SPLIT, 0), ("DP", "COL", "KS"))
+    ids, cost, _ = sbp.sbp_search_strategy(net, restarts=restarts, seed=seed)
+    names = {v: k for k, v in sbp.SIG_IDS.items()}
+    return [names[i] for i in ids], cost
+
+
+def transformer_step_searched(layers: int = 24) -> Workload:
+    """Workload 8: workload 5's 96 linears with the signatures the strategy
+    search picks (searched_signatures) instead of a random draw; rank 0."""
+    sigs, _ = searched_signatures(layers)
+    dims = (("qkv", 1024, 3072), ("out", 1024, 1024), ("fc1", 1024, 4096), ("fc2", 4096, 1024))
+    lins = []
+    ell = 0
+    for layer in range(layers):
+        for nm, k, n in dims:
+            lins.append(Linear("L%02d_%s" % (layer, nm), 8192, k, n, sigs[ell], 8000 + 10 * ell))
+            ell += 1
+    return Workload(8, "transformer_24L_step_searched_rank0_p8", torch.bfloat16, 8, tuple(lins),
+                    (0,))
+
+
 def transformer_3d() -> Workload:
     """Workload 6: the four linears of one Transformer layer (8192 tokens,
     hidden 1024, ffn 4096) on a 2 x 2 x 2 mesh of 8 devices, each under the

@@ -114,3 +114,14 @@ def test_transformer_step_sampled_linears():
         Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
         _sampled_check(lin, wl, X, W, dY, Xh, Wh, dYh, (0,), nsamp=800, seed=lin.seed_base)
         del X, W, dY
+
+
+def test_transformer_step_searched_sampled_linears():
+    # Workload 8: the same 96 linears with the signatures the strategy search
+    # chooses; the first layer's four linears on rank 0
+    wl = workloads.transformer_step_searched()
+    for lin in wl.linears[:4]:
+        X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
+        Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+        _sampled_check(lin, wl, X, W, dY, Xh, Wh, dYh, (0,), nsamp=600, seed=lin.seed_base)
+        del X, W, dY
