@@ -45,6 +45,10 @@
  *     pick the split-reduction path use a workspace that the library keeps
  *     per (device, stream); two calls on the same stream are ordered by the
  *     stream, so they never share it concurrently.
+ *   - Memory: the first such call on a (device, stream) allocates its
+ *     workspace (128 MiB of fp32 partials, kept until the process ends);
+ *     make one eager call on a stream before capturing it into a graph, so
+ *     that the capture allocates nothing. Every other call allocates nothing.
  */
 #ifndef SBP_H
 #define SBP_H
