@@ -483,7 +483,11 @@ int sbp_profile_end(float *us, char *names, int name_len);
  *         eight (128x128) in LDS;
  *   10    as 5 with two stages, two workgroups per compute unit (128x128);
  *   11    pipelined with deep prefetch for operand streams that HBM latency
- *         bounds: six stages (128x64, 64x128) or eight (64x64) in LDS.
+ *         bounds: six stages (128x64, 64x128) or eight (64x64) in LDS;
+ *   12    as 5 with 128-wide reduction stages, two (128x128), three
+ *         (128x64, 64x128) or four (64x64) in LDS: half the barriers and
+ *         twice the bytes per operand row of 64-wide stages;
+ *   13    as 12 with the row-quad epilogue.
  * wgs_per_cu > 0 makes the launch persistent: at most wgs_per_cu workgroups
  * per compute unit, each taking every G-th work item (0 = one workgroup per
  * item; the grouped backward launch always runs one per item). A call whose

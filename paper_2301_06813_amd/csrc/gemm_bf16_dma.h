@@ -72,10 +72,11 @@ __device__ __forceinline__ void dma16(i32x4 r, char *lds, int voff) {
 
 // ---------------------------------------------------------------- k-major
 // LDS: BMN rows x RB bytes (RB = 2 BK: 64 reduction values in 8 chunks of
-// 16 B, or 32 in 4). Chunk c of row r sits at r*RB + 16*(c ^ f(r)); f makes
-// the 16-byte fragment reads of 8 consecutive rows (32 banks) and of 16
-// (64 banks) hit distinct banks: with 64-byte rows, 16 aligned rows cover
-// the 16 bank quads once as 4 (r % 4) + (c ^ (r / 4 % 4)).
+// 16 B, 32 in 4, or 128 in 16). Chunk c of row r sits at r*RB + 16*(c ^
+// f(r)); f makes the 16-byte fragment reads of 8 consecutive rows (32 banks)
+// and of 16 (64 banks) hit distinct banks: with 64-byte rows, 16 aligned
+// rows cover the 16 bank quads once as 4 (r % 4) + (c ^ (r / 4 % 4)); with
+// 256-byte rows (one row spans all 64 banks) f(r) = r % 16.
 template <int BMN, int NW, int BK_>
 struct KTileDma {
     static constexpr int RB = BK_ * 2;            // bytes per row
@@ -86,6 +87,7 @@ struct KTileDma {
     static_assert(SEGS % NW == 0, "tile too small for the wave count");
 
     __device__ __forceinline__ static int swz(int row) {
+        if constexpr (CPR == 16) return row & 15;
         return CPR == 8 ? ((row & 7) ^ ((row >> 3) & 7)) : ((row >> 2) & 3);
     }
     __device__ __forceinline__ static int off(int row, int c) {

@@ -61,7 +61,15 @@ namespace sbpi {
     X(64, 64, 64, SBP_NS_64x64, 2, 2, 2, sbpk::EPI_STAGED)         \
     X(128, 64, 64, SBP_NS_128x64, 2, 2, 2, sbpk::EPI_ROWQ)         \
     X(64, 128, 64, SBP_NS_128x64, 2, 2, 2, sbpk::EPI_ROWQ)         \
-    X(64, 64, 64, SBP_NS_64x64, 2, 2, 2, sbpk::EPI_ROWQ)
+    X(64, 64, 64, SBP_NS_64x64, 2, 2, 2, sbpk::EPI_ROWQ)         \
+    X(128, 128, 128, 2, 2, 2, 2, sbpk::EPI_STAGED)                 \
+    X(128, 64, 128, 3, 2, 2, 2, sbpk::EPI_STAGED)                  \
+    X(64, 128, 128, 3, 2, 2, 2, sbpk::EPI_STAGED)                  \
+    X(64, 64, 128, 4, 2, 2, 2, sbpk::EPI_STAGED)                   \
+    X(128, 128, 128, 2, 2, 2, 2, sbpk::EPI_ROWQ)                   \
+    X(128, 64, 128, 3, 2, 2, 2, sbpk::EPI_ROWQ)                    \
+    X(64, 128, 128, 3, 2, 2, 2, sbpk::EPI_ROWQ)                    \
+    X(64, 64, 128, 4, 2, 2, 2, sbpk::EPI_ROWQ)
 
 // Grid of a launch of `items` work items under plan p: one workgroup per item,
 // or (persistent plans) at most occ workgroups per compute unit, a multiple of 8.

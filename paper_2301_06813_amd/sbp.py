@@ -461,6 +461,7 @@ KERNEL_AUTO, KERNEL_PIPELINED, KERNEL_GENERIC, KERNEL_F32, KERNEL_PIPELINED_2STA
 KERNEL_GROUPS_STAGED, KERNEL_ROWQ, KERNEL_GROUPS_ROWQ = 5, 6, 7
 KERNEL_DEEP, KERNEL_GROUPS_DEEP = 8, 9
 KERNEL_GROUPS_2STAGE, KERNEL_DEEP_PREFETCH = 10, 11
+KERNEL_GROUPS_WIDE, KERNEL_GROUPS_WIDE_ROWQ = 12, 13
 
 
 def sbp_plan(op: int, m: int, n: int, k: int, in_dtype: int, out_dtype: int):

@@ -31,7 +31,7 @@ import time
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 TILES = [(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
-CODES = (1, 4, 5, 6, 7, 8, 9, 10, 11)   # pipelined instances; 2 (generic) for the rest
+CODES = (1, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13)   # pipelined instances; 2 (generic) for the rest
 SPLITS = (1, 2, 3, 4, 6, 8, 12, 16)
 ORIENT = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2}
 
@@ -146,7 +146,9 @@ def time_plan(torch, sbp, fn, plan, reps, stream, keep=False):
 GROUP_INSTANCES = [((128, 128), 1), ((128, 128), 4), ((128, 128), 5), ((256, 128), 5),
                    ((128, 256), 5), ((64, 64), 1), ((128, 64), 1), ((64, 128), 1),
                    ((256, 256), 1), ((128, 128), 7), ((128, 128), 10), ((64, 64), 5),
-                   ((64, 64), 7), ((128, 64), 5), ((64, 128), 5)]
+                   ((64, 64), 7), ((128, 64), 5), ((64, 128), 5), ((128, 128), 12),
+                   ((128, 64), 12), ((64, 128), 12), ((64, 64), 12), ((128, 128), 13),
+                   ((64, 64), 13)]
 
 
 def bwd_pairs(wl_ids):
@@ -345,8 +347,7 @@ def main():
     ap.add_argument("--out-bwd", default=os.path.join(HERE, "csrc", "tuned_bwd_plans.inc"))
     args = ap.parse_args()
     if args.out is None:
-        args.out = os.path.join(HERE, "csrc",
-                                "tuned_bwd_plans.inc" if args.bwd else "tuned_plans.inc")
+        args.out = args.out_bwd if args.bwd else os.path.join(HERE, "csrc", "tuned_plans.inc")
 
     import torch
     from . import linear, sbp, workloads

@@ -22,7 +22,9 @@ EXTRA_TILE_KERNELS = [((128, 128), 4), ((128, 128), 5), ((256, 128), 5), ((128, 
                       ((128, 128), 9), ((128, 128), 10), ((128, 64), 4), ((64, 128), 4),
                       ((64, 64), 4), ((128, 64), 11), ((64, 128), 11), ((64, 64), 11),
                       ((128, 64), 5), ((64, 128), 5), ((64, 64), 5), ((128, 64), 7),
-                      ((64, 128), 7), ((64, 64), 7)]
+                      ((64, 128), 7), ((64, 64), 7), ((128, 128), 12), ((128, 64), 12),
+                      ((64, 128), 12), ((64, 64), 12), ((128, 128), 13), ((128, 64), 13),
+                      ((64, 128), 13), ((64, 64), 13)]
 
 
 def say(*a):

@@ -250,7 +250,7 @@ def test_strerror_and_plan(L):
     tm, tn, s, kn = sbp.sbp_plan(2, 1024, 384, 8192, sbp.SBP_BF16, sbp.SBP_BF16)
     assert (tm, tn) in {(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128),
                         (64, 64)}
-    assert s >= 1 and kn in (1, 4, 5, 6, 7, 8, 9, 10, 11)   # pipelined bf16 instances
+    assert s >= 1 and kn in (1, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13)   # pipelined bf16 instances
     # a reduction that is not a multiple of 8 cannot use the pipelined kernel
     assert sbp.sbp_plan(0, 256, 256, 125, BF, BF)[3] == sbp.KERNEL_GENERIC
     assert sbp.sbp_plan(0, 64, 64, 64, F32, F32)[3] == sbp.KERNEL_F32
@@ -282,11 +282,14 @@ def test_strerror_and_plan(L):
                        ((256, 256), 8), ((256, 128), 9), ((128, 256), 9), ((128, 128), 9),
                        ((128, 128), 10), ((128, 64), 11), ((64, 128), 11), ((64, 64), 11),
                        ((128, 64), 5), ((64, 128), 5), ((64, 64), 5), ((128, 64), 7),
-                       ((64, 128), 7), ((64, 64), 7)):
+                       ((64, 128), 7), ((64, 64), 7), ((128, 128), 12), ((128, 64), 12),
+                       ((64, 128), 12), ((64, 64), 12), ((128, 128), 13), ((128, 64), 13),
+                       ((64, 128), 13), ((64, 64), 13)):
         sbp.sbp_set_plan_override(tile[0], tile[1], 2, code, 1)
         assert sbp.sbp_plan(0, 2048, 2048, 1024, BF, BF) == (tile[0], tile[1], 2, code)
     for tile, code in (((64, 64), 6), ((256, 256), 5), ((64, 128), 9), ((256, 128), 10),
-                       ((128, 128), 3), ((128, 128), 11), ((64, 64), 12)):
+                       ((128, 128), 3), ((128, 128), 11), ((256, 128), 12),
+                       ((256, 256), 13), ((64, 64), 14)):
         with pytest.raises(sbp.SbpError):
             sbp.sbp_set_plan_override(tile[0], tile[1], 1, code)
     with pytest.raises(sbp.SbpError):
