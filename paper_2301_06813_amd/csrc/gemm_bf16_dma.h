@@ -15,8 +15,9 @@
 //     allows) are in flight: the loads of step t + NS - 1 are issued while
 //     step t computes, hiding HBM latency behind NS - 1 steps of MFMA work.
 //     Chunks outside the operand get an out-of-range offset and read as 0.
-//   * The reduction step BKD is a template parameter: 64, or 32 for deeper
-//     pipelines (more stages in the same LDS).
+//   * The reduction step BKD is a template parameter: 64; 32 for deeper
+//     pipelines (more stages in the same LDS); or 128, with two reduction
+//     groups, for half the barriers per flop and 256-byte k-major rows.
 //   * k-major operand tiles keep their storage order in LDS: one row of BKD
 //     reduction values per output row, 16-byte chunks XOR-swizzled by row;
 //     fragments are read with ds_read_b128.
