@@ -38,9 +38,13 @@ const TileClass kGeneric[] = {
 // The two-stage 128 x 128 instance (64 KB of LDS) runs two workgroups per
 // CU: one's output stores overlap the other's loads, which pays off when the
 // reduction is short and the output large.
+// The 128-wide stages with two reduction groups (one workgroup of eight
+// waves per CU) stream their operands about 20 % faster per CU.
 const TileClass kDma[] = {
     {256, 256, 1, 1.0, 0}, {256, 128, 1, 1.0, 0}, {128, 256, 1, 1.0, 0}, {128, 128, 1, 1.0, 0},
     {128, 128, 2, 0.8, 2}, {128, 64, 1, 1.0, 0},  {64, 128, 1, 1.0, 0},  {64, 64, 2, 1.0, 0},
+    {128, 128, 1, 1.2, 2, 2, 1, 0, 128}, {128, 64, 1, 1.2, 3, 2, 1, 0, 128},
+    {64, 128, 1, 1.2, 3, 2, 1, 0, 128},  {64, 64, 1, 1.2, 4, 2, 1, 0, 128},
 };
 
 // Time model (measured on MI355X): a workgroup's 64-wide reduction step
