@@ -467,7 +467,7 @@ KERNEL_GROUPS_WIDE, KERNEL_GROUPS_WIDE_ROWQ = 12, 13
 def sbp_plan(op: int, m: int, n: int, k: int, in_dtype: int, out_dtype: int):
     """(tile_m, tile_n, splits, kernel) the library would launch for this product
     with aligned operands; kernel is KERNEL_F32 or one of the bf16 instance codes
-    of sbp_set_plan_override (KERNEL_PIPELINED ... KERNEL_GROUPS_ROWQ)."""
+    of sbp_set_plan_override (KERNEL_PIPELINED ... KERNEL_GROUPS_WIDE_ROWQ)."""
     tm, tn, sp, kn = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     _check(lib().sbp_plan(op, m, n, k, in_dtype, out_dtype, ctypes.byref(tm), ctypes.byref(tn),
                           ctypes.byref(sp), ctypes.byref(kn)))
