@@ -355,3 +355,39 @@ def test_plan_bwd(L):
     assert g in (0, 1) and sd >= 1 and sw >= 1
     assert (tm, tn) in {(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128),
                         (64, 64)}
+
+
+def _table_rows(name):
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "paper_2301_06813_amd", "csrc", name)
+    rows = []
+    for line in open(path):
+        m = re.match(r"\{([^}]*)\}", line.strip())
+        if m:
+            rows.append([int(x) for x in m.group(1).split(",")])
+    return rows
+
+
+def test_tuned_tables_name_built_instances(L):
+    # every tuned plan names a (tile, kernel) pair the library has, and the
+    # library then reports that plan back for the product
+    singles = _table_rows("tuned_plans.inc")
+    pairs = _table_rows("tuned_bwd_plans.inc")
+    assert len(singles) > 50 and len(pairs) > 15
+    try:
+        for orient, f32, m, n, k, dma, bm, bn, code, splits, occ, *nb in singles:
+            sbp.sbp_set_plan_override(bm, bn, 1, code)     # raises for an unknown pair
+            assert splits >= 1 and 0 <= occ <= 8
+            sbp.sbp_set_plan_override(0, 0, 1)
+            if dma and not nb:
+                out = F32 if f32 else BF
+                tm, tn, s, kn = sbp.sbp_plan(orient, m, n, k, BF, out)
+                assert (tm, tn, s, kn) == (bm, bn, splits, code), (orient, m, n, k)
+        for md, nd, kd, fd, mw, nw, kw, fw, bm, bn, code, sd, sw in pairs:
+            sbp.sbp_set_plan_override(bm, bn, sd, code)
+            sbp.sbp_set_plan_override(0, 0, 1)
+            g, tm, tn, psd, psw = sbp.sbp_plan_bwd(md, nd, kd, F32 if fd else BF,
+                                                     mw, nw, kw, F32 if fw else BF)
+            assert (g, tm, tn, psd, psw) == (1, bm, bn, sd, sw), (md, nd, kd)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
