@@ -103,25 +103,63 @@ def test_workload_full_size_sampled(make):
         del Xc, Wc, dYc
 
 
+def _sampled_bwd_pair(lin, wl, X, W, dY, Xh, Wh, dYh, r, nsamp, seed):
+    """Both backward products through sbp_linear_bwd (one grouped launch where
+    the tuned plans say so), as the benchmark calls them; sampled outputs."""
+    rng = np.random.default_rng(seed)
+    say(wl.name, lin.name, lin.sig, "bwd pair", "rank", r)
+    dX, dW, (sx, sw) = linear.call_bwd(lin.sig, wl.p, r, X, W, dY)
+    torch.cuda.synchronize()
+    expect_state("bwd_data", lin.sig, wl.p, r, sx)
+    expect_state("bwd_weight", lin.sig, wl.p, r, sw)
+    for op, out in (("bwd_data", dX), ("bwd_weight", dW)):
+        rows, cols = out.shape
+        ii = rng.integers(0, rows, nsamp)
+        jj = rng.integers(0, cols, nsamp)
+        ii[:4] = [0, 0, rows - 1, rows - 1]
+        jj[:4] = [0, cols - 1, 0, cols - 1]
+        got = decode(out[torch.as_tensor(ii, device="cuda"), torch.as_tensor(jj, device="cuda")])
+        want = oracle.linear_samples(SIG_ID[lin.sig], OP_ID[op], Xh, Wh, dYh, wl.p, r, ii, jj)
+        rel = normwise_rel(got, want)
+        assert rel <= TOL_BF16, (wl.name, lin.name, "pair", op, r, rel)
+
+
+def _one_per_shape(wl):
+    """The first linear of each (signature, layer position) of a step: every
+    distinct local product shape, hence every plan, the benchmark launches."""
+    seen, picked = set(), []
+    for lin in wl.linears:
+        key = (lin.sig, lin.name.split("_", 1)[1])
+        if key not in seen:
+            seen.add(key)
+            picked.append(lin)
+    return picked
+
+
 def test_transformer_step_sampled_linears():
-    # Workload 5 draws inputs on the GPU (as the benchmark does); every 8th
-    # linear is checked on rank 0, covering all three signatures.
+    # Workload 5 draws inputs on the GPU (as the benchmark does); one linear
+    # per distinct (signature, qkv/out/fc1/fc2) on rank 0: the forward and
+    # each backward product alone, and the backward pair as the benchmark
+    # calls it.
     wl = workloads.transformer_step()
-    picked = wl.linears[::8]
-    assert {l.sig for l in picked} == {"DP", "COL", "KS"}
+    picked = _one_per_shape(wl)
+    assert {l.sig for l in picked} == {"DP", "COL", "KS"} and len(picked) >= 10
     for lin in picked:
         X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
         Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
         _sampled_check(lin, wl, X, W, dY, Xh, Wh, dYh, (0,), nsamp=800, seed=lin.seed_base)
+        _sampled_bwd_pair(lin, wl, X, W, dY, Xh, Wh, dYh, 0, 800, lin.seed_base + 1)
         del X, W, dY
 
 
 def test_transformer_step_searched_sampled_linears():
     # Workload 8: the same 96 linears with the signatures the strategy search
-    # chooses; the first layer's four linears on rank 0
+    # chooses (all DP): one linear per layer position on rank 0, also as a
+    # backward pair
     wl = workloads.transformer_step_searched()
-    for lin in wl.linears[:4]:
+    for lin in _one_per_shape(wl):
         X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
         Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
         _sampled_check(lin, wl, X, W, dY, Xh, Wh, dYh, (0,), nsamp=600, seed=lin.seed_base)
+        _sampled_bwd_pair(lin, wl, X, W, dY, Xh, Wh, dYh, 0, 600, lin.seed_base + 1)
         del X, W, dY
