@@ -164,4 +164,22 @@ def test_workload6_full_size_sampled():
                 rel = normwise_rel(got, want)
                 assert rel <= TOL_BF16, (lin.name, op, c, rel)
                 del out
+            # the backward pair as the benchmark calls it (sbp_nd_linear_bwd)
+            say(wl.name, lin.name, "bwd pair", c)
+            dX, dW, (sx, sw) = linear.call_bwd_nd(lin.factors, wl.mesh, c, X, W, dY)
+            torch.cuda.synchronize()
+            _expect("bwd_data", lin.factors, wl.mesh, c, sx, lin.M, lin.K, lin.N)
+            _expect("bwd_weight", lin.factors, wl.mesh, c, sw, lin.M, lin.K, lin.N)
+            for op, out in (("bwd_data", dX), ("bwd_weight", dW)):
+                rows, cols = out.shape
+                ii = rng.integers(0, rows, 600)
+                jj = rng.integers(0, cols, 600)
+                ii[:4] = [0, 0, rows - 1, rows - 1]
+                jj[:4] = [0, cols - 1, 0, cols - 1]
+                got = decode(out[torch.as_tensor(ii, device="cuda"),
+                                 torch.as_tensor(jj, device="cuda")])
+                want = oracle.nd_linear_samples(OP_ID[op], Xh, Wh, dYh, xs, ws, wl.mesh, c, ii, jj)
+                rel = normwise_rel(got, want)
+                assert rel <= TOL_BF16, (lin.name, "pair", op, c, rel)
+            del dX, dW
         del X, W, dY
