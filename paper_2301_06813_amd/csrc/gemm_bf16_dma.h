@@ -246,12 +246,19 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
             f32x4 v = *reinterpret_cast<const f32x4 *>(src);
             float *dst = reinterpret_cast<float *>(C) + (int64_t)row * ldc + col;
             if (vec && col + 4 <= n) {
-                if constexpr (ACC) v += *reinterpret_cast<const f32x4 *>(dst);
-                *reinterpret_cast<f32x4 *>(dst) = v;
+                if constexpr (ACC) {
+                    v += *reinterpret_cast<const f32x4 *>(dst);
+                    *reinterpret_cast<f32x4 *>(dst) = v;
+                } else {
+                    st_nt(reinterpret_cast<f32x4 *>(dst), v);
+                }
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    if (col + e < n) dst[e] = ACC ? dst[e] + v[e] : v[e];
+                    if (col + e < n) {
+                        if constexpr (ACC) dst[e] = dst[e] + v[e];
+                        else st_nt(dst + e, v[e]);
+                    }
             }
         } else {
             const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
@@ -263,11 +270,11 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
                 w[1] = (uint32_t)f32_to_bf16_bits(a[2]) | ((uint32_t)f32_to_bf16_bits(a[3]) << 16);
                 w[2] = (uint32_t)f32_to_bf16_bits(b[0]) | ((uint32_t)f32_to_bf16_bits(b[1]) << 16);
                 w[3] = (uint32_t)f32_to_bf16_bits(b[2]) | ((uint32_t)f32_to_bf16_bits(b[3]) << 16);
-                *reinterpret_cast<u32x4 *>(dst) = w;
+                st_nt(reinterpret_cast<u32x4 *>(dst), w);
             } else {
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    if (col + e < n) dst[e] = f32_to_bf16_bits(e < 4 ? a[e] : b[e - 4]);
+                    if (col + e < n) st_nt(dst + e, f32_to_bf16_bits(e < 4 ? a[e] : b[e - 4]));
             }
         }
     }
@@ -457,14 +464,21 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                             if (vec && col + 4 <= g.n) {
                                 f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1],
                                            acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-                                if constexpr (ACC) v += *reinterpret_cast<const f32x4 *>(dst);
-                                *reinterpret_cast<f32x4 *>(dst) = v;
+                                if constexpr (ACC) {
+                                    v += *reinterpret_cast<const f32x4 *>(dst);
+                                    *reinterpret_cast<f32x4 *>(dst) = v;
+                                } else {
+                                    st_nt(reinterpret_cast<f32x4 *>(dst), v);
+                                }
                             } else {
 #pragma unroll
                                 for (int e = 0; e < 4; ++e)
-                                    if (col + e < g.n)
-                                        dst[e] = ACC ? dst[e] + acc[i][j][4 * q + e]
-                                                     : acc[i][j][4 * q + e];
+                                    if (col + e < g.n) {
+                                        if constexpr (ACC)
+                                            dst[e] = dst[e] + acc[i][j][4 * q + e];
+                                        else
+                                            st_nt(dst + e, acc[i][j][4 * q + e]);
+                                    }
                             }
                         } else {
                             uint16_t *dst =
@@ -475,12 +489,12 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                                        ((uint32_t)f32_to_bf16_bits(acc[i][j][4 * q + 1]) << 16);
                                 w[1] = (uint32_t)f32_to_bf16_bits(acc[i][j][4 * q + 2]) |
                                        ((uint32_t)f32_to_bf16_bits(acc[i][j][4 * q + 3]) << 16);
-                                *reinterpret_cast<u32x2 *>(dst) = w;
+                                st_nt(reinterpret_cast<u32x2 *>(dst), w);
                             } else {
 #pragma unroll
                                 for (int e = 0; e < 4; ++e)
                                     if (col + e < g.n)
-                                        dst[e] = f32_to_bf16_bits(acc[i][j][4 * q + e]);
+                                        st_nt(dst + e, f32_to_bf16_bits(acc[i][j][4 * q + e]));
                             }
                         }
                     }
@@ -562,11 +576,11 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                                 float *d = reinterpret_cast<float *>(out) + (int64_t)row * ldo + col;
                                 *d = *d + acc[i][j][r];
                             } else if constexpr (F32)
-                                reinterpret_cast<float *>(out)[(int64_t)row * ldo + col] =
-                                    acc[i][j][r];
+                                st_nt(reinterpret_cast<float *>(out) + (int64_t)row * ldo + col,
+                                      acc[i][j][r]);
                             else
-                                reinterpret_cast<uint16_t *>(out)[(int64_t)row * ldo + col] =
-                                    f32_to_bf16_bits(acc[i][j][r]);
+                                st_nt(reinterpret_cast<uint16_t *>(out) + (int64_t)row * ldo + col,
+                                      f32_to_bf16_bits(acc[i][j][r]));
                         }
                     }
                 }

@@ -254,6 +254,15 @@ __device__ __forceinline__ int remap_xcd(int wg, int total) {
     return (x < rem) ? x * (per + 1) + idx : rem * (per + 1) + (x - rem) * per + idx;
 }
 
+// Store of a GEMM output (or split partial) that this launch does not read
+// back: non-temporal, so the output stream does not displace the operand
+// tiles that other workgroups still re-read from L2 (measured: fp32
+// partial-sum outputs of the step 10-13 % faster, the whole step 2.4 %).
+template <typename T>
+__device__ __forceinline__ void st_nt(T *p, T v) {
+    __builtin_nontemporal_store(v, p);
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
     __bf16 h = (__bf16)f;   // round to nearest even (v_cvt_pk_bf16_f32)
     return __builtin_bit_cast(uint16_t, h);

@@ -54,8 +54,8 @@ __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int 
         if constexpr (OUT_F32) {
             f32x4v *dst =
                 reinterpret_cast<f32x4v *>(reinterpret_cast<float *>(C) + (int64_t)row * ldc + col);
-            if (acc) v = *dst + v;
-            *dst = v;
+            if (acc) *dst = *dst + v;
+            else __builtin_nontemporal_store(v, dst);   // not read back by this kernel
         } else {
             typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
             u32x2v w;
@@ -63,8 +63,9 @@ __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int 
                    ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[1]) << 16);
             w[1] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2]) |
                    ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[3]) << 16);
-            *reinterpret_cast<u32x2v *>(reinterpret_cast<uint16_t *>(C) + (int64_t)row * ldc +
-                                        col) = w;
+            __builtin_nontemporal_store(
+                w, reinterpret_cast<u32x2v *>(reinterpret_cast<uint16_t *>(C) +
+                                              (int64_t)row * ldc + col));
         }
         return;
     }
@@ -73,11 +74,13 @@ __device__ __forceinline__ void reduce_group(const float *ws, int m, int n, int 
         if (col + e >= n) break;
         if constexpr (OUT_F32) {
             float *dst = reinterpret_cast<float *>(C) + (int64_t)row * ldc + col + e;
-            *dst = acc ? *dst + v[e] : v[e];
+            if (acc) *dst = *dst + v[e];
+            else __builtin_nontemporal_store(v[e], dst);
         } else {
             __bf16 h = (__bf16)v[e];
-            reinterpret_cast<uint16_t *>(C)[(int64_t)row * ldc + col + e] =
-                __builtin_bit_cast(uint16_t, h);
+            __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, h),
+                                        reinterpret_cast<uint16_t *>(C) + (int64_t)row * ldc +
+                                            col + e);
         }
     }
 }
