@@ -369,7 +369,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
         }
     }
 
-    // ---- split reduction: partials to workspace, last workgroup adds them
+    // ---- split reduction: partials to the workspace; split_reduce_kernel adds them
     if (g.splits > 1) {
         // Split reduction: this workgroup's fp32 partial goes to slice
         // `split` of the workspace, laid out like the output (m x n, ld n);

@@ -15,10 +15,16 @@ paper states about specific strategies:
   forward and reduce-scatters its gradient backward (Sec. 4.2);
 * the AlltoAll of a split-axis change sends each device's share, so its
   bandwidth term is the tensor over p;
-* planted mistakes in copies of search.py are caught by these checks.
+* every collective's time equals Table 2's formula evaluated by hand at fixed
+  points (tests/golden/table2_collectives.json), where latency-only and
+  bandwidth-only points separate each coefficient;
+* planted mistakes in copies of search.py are caught by these checks, one
+  per coefficient of Table 2 among them.
 """
 import importlib.util
 import itertools
+import json
+import os
 
 import pytest
 
@@ -27,6 +33,12 @@ from oracle import search as S
 
 S0, S1, B, P = (oracle.SPLIT, 0), (oracle.SPLIT, 1), (oracle.BCAST, -1), (oracle.PARTIAL, -1)
 STATES = (S0, S1, B, P)
+TABLE2 = os.path.join(os.path.dirname(__file__), "golden", "table2_collectives.json")
+
+
+def table2_cases():
+    with open(TABLE2) as f:
+        return json.load(f)["cases"]
 
 
 def _net(K, N, p=8, alpha=1e-5, beta=1e-10, M=4096, ins=S0, outs=S0):
@@ -37,6 +49,15 @@ def _net(K, N, p=8, alpha=1e-5, beta=1e-10, M=4096, ins=S0, outs=S0):
 def checks(mod):
     """Names of the pins that fail for search module `mod`."""
     bad = []
+    # Table 2 as printed, evaluated by hand (exact in binary floating point)
+    names = (("allreduce", mod.ALLREDUCE), ("allgather", mod.ALLGATHER),
+             ("reducescatter", mod.REDUCESCATTER), ("alltoall", mod.ALLTOALL))
+    for c in table2_cases():
+        for name, coll in names:
+            got = mod.collective(coll, c["p"], c["n"], c["alpha"], c["beta"])
+            if abs(got - c[name]) > 1e-12 * max(1.0, abs(c[name])):
+                bad.append("table 2 %s at p=%d n=%g alpha=%g beta=%g" % (
+                    name, c["p"], c["n"], c["alpha"], c["beta"]))
     for p in (2, 4, 8):
         net = _net([1024, 3072, 1024], [3072, 1024, 4096], p=p)
         dp = mod.chain_cost(net, [oracle.DP] * 3)
@@ -116,6 +137,27 @@ SEARCH_MUTATIONS = [
      "        total += 0.0"),
     ("alltoall sends the whole tensor", "    n = nbytes / p if coll == ALLTOALL else nbytes",
      "    n = nbytes"),
+    ("allreduce latency term as an allgather's",
+     "        return (2 * p - 1) * alpha + 2 * (p - 1) / p * n * beta",
+     "        return (p - 1) * alpha + 2 * (p - 1) / p * n * beta"),
+    ("allreduce bandwidth term without its factor 2",
+     "        return (2 * p - 1) * alpha + 2 * (p - 1) / p * n * beta",
+     "        return (2 * p - 1) * alpha + (p - 1) / p * n * beta"),
+    ("allreduce priced as an allgather",
+     "        return (2 * p - 1) * alpha + 2 * (p - 1) / p * n * beta",
+     "        return (p - 1) * alpha + (p - 1) / p * n * beta"),
+    ("allgather/reducescatter bandwidth term without (p-1)/p",
+     "        return (p - 1) * alpha + (p - 1) / p * n * beta",
+     "        return (p - 1) * alpha + n * beta"),
+    ("allgather/reducescatter latency term with p",
+     "        return (p - 1) * alpha + (p - 1) / p * n * beta",
+     "        return p * alpha + (p - 1) / p * n * beta"),
+    ("alltoall bandwidth term with (p-1)/p",
+     "        return (p - 1) * alpha + n * beta",
+     "        return (p - 1) * alpha + (p - 1) / p * n * beta"),
+    ("alltoall latency term dropped",
+     "        return (p - 1) * alpha + n * beta",
+     "        return n * beta"),
     ("gradient of a broadcast stays broadcast",
      "    return {oracle.BCAST: (oracle.PARTIAL, -1), oracle.PARTIAL: (oracle.BCAST, -1)}.get(k, st)",
      "    return {oracle.PARTIAL: (oracle.BCAST, -1)}.get(k, st)"),

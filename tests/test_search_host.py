@@ -38,6 +38,20 @@ def test_collective_costs_match_oracle():
         assert abs(got - want) <= REL * max(1e-30, abs(want))
 
 
+def test_collective_costs_match_table2_golden():
+    """The library's collective costs at the hand-evaluated points of Table 2
+    (Sec. 3.1), the same fixture that pins the oracle."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "table2_collectives.json")
+    ids = {"allreduce": sbp.SBP_COLL_ALLREDUCE, "allgather": sbp.SBP_COLL_ALLGATHER,
+           "reducescatter": sbp.SBP_COLL_REDUCESCATTER, "alltoall": sbp.SBP_COLL_ALLTOALL}
+    for c in json.load(open(path))["cases"]:
+        for name, coll in ids.items():
+            got = sbp.sbp_collective_cost(coll, c["p"], c["n"], c["alpha"], c["beta"])
+            assert abs(got - c[name]) <= 1e-12 * max(1.0, abs(c[name])), (name, c)
+
+
 def test_boxing_costs_match_oracle():
     coll_map = {-1: None, 0: OS.ALLREDUCE, 1: OS.ALLGATHER, 2: OS.REDUCESCATTER, 3: OS.ALLTOALL}
     for frm, to in itertools.product(STATES, STATES):
