@@ -122,14 +122,19 @@ class Step:
         self._lo = sbp.sbp_layout_t()
         self._lo2 = sbp.sbp_layout_t()
         lo, lo2 = ctypes.byref(self._lo), ctypes.byref(self._lo2)
+        # the split reductions' workspace (caller-owned; every call of the
+        # step runs in order on one stream, so they share it)
+        self.ws_mem = torch.empty(sbp.SBP_WORKSPACE_BYTES, dtype=torch.uint8, device=device)
+        self._ws = sbp.workspace(self.ws_mem)
+        ws = ctypes.byref(self._ws)
         self._bound = []
         for name, args, extra in self.calls:
             fn = getattr(L_, name)
             refs = tuple(ctypes.byref(a) for a in args)
             if name == "sbp_linear_bwd":
-                refs = refs + (lo, ctypes.byref(extra[0]), lo2)
+                refs = refs + (lo, ctypes.byref(extra[0]), lo2, ws)
             else:
-                refs = refs + (lo,)
+                refs = refs + (lo, ws)
             self._bound.append((fn, refs))
 
     def launch_all(self, stream):

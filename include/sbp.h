@@ -41,14 +41,13 @@
  *   - Compute calls are asynchronous on the given stream (0 = the null
  *     stream) and never synchronise. Inputs must stay valid, and outputs
  *     untouched, until the stream has run the call.
- *   - Thread safety: calls on different host threads are safe. Calls that
- *     pick the split-reduction path use a workspace that the library keeps
- *     per (device, stream); two calls on the same stream are ordered by the
- *     stream, so they never share it concurrently.
- *   - Memory: the first such call on a (device, stream) allocates its
- *     workspace (128 MiB of fp32 partials, kept until the process ends);
- *     make one eager call on a stream before capturing it into a graph, so
- *     that the capture allocates nothing. Every other call allocates nothing.
+ *   - Memory: the library allocates nothing and keeps no device state.
+ *     The linear calls take a caller-owned workspace (sbp_workspace_t) for
+ *     the fp32 partials of split reductions; see below. Every call can be
+ *     captured into a HIP graph, including the first on a stream.
+ *   - Thread safety: calls on different host threads are safe. Two calls
+ *     may share a workspace only if they cannot run at the same time (e.g.
+ *     they are on the same stream).
  */
 #ifndef SBP_H
 #define SBP_H
@@ -75,7 +74,9 @@ enum {
                                output of fp32 inputs                            */
     SBP_ERR_ALIAS = -6,     /* the output's memory overlaps an input's          */
     SBP_ERR_ALIGN = -7,     /* a data pointer is not aligned to its element size */
-    SBP_ERR_HIP = -8        /* a HIP call failed; see sbp_last_hip_error()      */
+    SBP_ERR_HIP = -8,       /* a HIP call failed; see sbp_last_hip_error()      */
+    SBP_ERR_WORKSPACE = -9  /* the split partials of the call's plan do not fit
+                               the workspace it runs with                       */
 };
 
 /* ------------------------------------------------------------ types --- */
@@ -114,6 +115,26 @@ typedef struct {
                       adds to them, any other value overwrites them */
 } sbp_view_t;
 
+/* Caller-owned device memory for split reductions. A product with a long
+ * reduction and few output tiles runs faster with its reduction split over
+ * several workgroups; each split writes an fp32 partial of the m x n output
+ * (splits x m x n x 4 bytes in all) that a second kernel adds up in split
+ * order. The linear calls take a workspace; data = NULL (or bytes = 0, or a
+ * NULL sbp_workspace_t pointer) means none, and then no reduction is split.
+ * With bytes >= SBP_WORKSPACE_BYTES every call gets the library's preferred
+ * plan; a smaller workspace limits the splits to what fits (results are the
+ * same up to fp32 summation order; identical for identical workspace
+ * sizes). The library never reads the workspace's contents before writing
+ * them, so it needs no clearing. data must be 16-byte aligned (else
+ * SBP_ERR_ALIGN), must not overlap the call's inputs or outputs (else
+ * SBP_ERR_ALIAS), and must not be used by another call at the same time. */
+typedef struct {
+    void *data;    /* device pointer on the current device, or NULL */
+    int64_t bytes; /* its size in bytes (>= 0, else SBP_ERR_SHAPE)   */
+} sbp_workspace_t;
+
+#define SBP_WORKSPACE_BYTES ((int64_t)64 << 20)
+
 /* Rank r's share of a tensor: rows [row_off, row_off+rows) x cols
  * [col_off, col_off+cols) of the global tensor. */
 typedef struct {
@@ -149,10 +170,12 @@ int sbp_signature(const sbp_layout_t *x, const sbp_layout_t *w,
  *    PB and BP M x N (Partial-sum, fp32), BB M x N (Broadcast).
  * Inputs bf16 or fp32 (same dtype); Y is fp32, or bf16 for bf16 inputs and
  * a Split/Broadcast output (rounded to nearest even from the fp32
- * accumulator). */
+ * accumulator). ws: workspace for a split reduction (may be NULL; see
+ * sbp_workspace_t). */
 int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx,
                    const sbp_view_t *W, const sbp_layout_t *lw, sbp_view_t *Y,
-                   sbp_layout_t *ly_out, hipStream_t stream);
+                   sbp_layout_t *ly_out, const sbp_workspace_t *ws,
+                   hipStream_t stream);
 
 /* Backward-data local matmul dX_r = dY_r W_r^T (Sec. 4.2: the redistributions
  * of the forward path have backward counterparts; Sec. 4.3).
@@ -160,22 +183,24 @@ int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx,
  *     BB); W: state *lw.
  * dX: rank r's local output, state to *ldx_out: DP m_r x K (S(0)),
  *     COL M x K (Partial-sum, fp32), KS M x k_r (S(1)); PB M x K (B), BP
- *     and BB M x K (Partial-sum, fp32). */
+ *     and BB M x K (Partial-sum, fp32).
+ * ws as for sbp_linear_fwd. */
 int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy,
                         const sbp_view_t *W, const sbp_layout_t *lw,
                         sbp_view_t *dX, sbp_layout_t *ldx_out,
-                        hipStream_t stream);
+                        const sbp_workspace_t *ws, hipStream_t stream);
 
 /* Backward-weight local matmul dW_r = X_r^T dY_r (Sec. 4.3: a broadcast
  * weight receives partial-sum gradients).
  * X: state *lx; dY: state *ldy.
  * dW: rank r's local output, state to *ldw_out: DP K x N (Partial-sum,
  *     fp32), COL K x n_r (S(1)), KS k_r x N (S(0)); PB and BB K x N
- *     (Partial-sum, fp32), BP K x N (B). */
+ *     (Partial-sum, fp32), BP K x N (B).
+ * ws as for sbp_linear_fwd. */
 int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx,
                           const sbp_view_t *dY, const sbp_layout_t *ldy,
                           sbp_view_t *dW, sbp_layout_t *ldw_out,
-                          hipStream_t stream);
+                          const sbp_workspace_t *ws, hipStream_t stream);
 
 /* Both backward products of the linear, dX_r = dY_r W_r^T and
  * dW_r = X_r^T dY_r, in one call (one grouped launch when the planner
@@ -187,12 +212,14 @@ int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx,
  * of sbp_linear_bwd_data and sbp_linear_bwd_weight; the three input states
  * must form one signature (else SBP_ERR_SIGNATURE), and dX and dW must not
  * overlap (SBP_ERR_ALIAS). Results equal the two separate calls up to fp32
- * summation order. */
+ * summation order. ws as for sbp_linear_fwd: a grouped launch holds the
+ * partials of both products in it at once, two separate launches use it in
+ * turn. */
 int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy,
                    const sbp_view_t *X, const sbp_layout_t *lx,
                    const sbp_view_t *W, const sbp_layout_t *lw, sbp_view_t *dX,
                    sbp_layout_t *ldx_out, sbp_view_t *dW, sbp_layout_t *ldw_out,
-                   hipStream_t stream);
+                   const sbp_workspace_t *ws, hipStream_t stream);
 
 /* ------------------------------------------- nd-SBP on device meshes --- */
 
@@ -259,8 +286,8 @@ int sbp_nd_signature(const sbp_nd_layout_t *x, const sbp_nd_layout_t *w,
                      sbp_nd_layout_t *dx, sbp_nd_layout_t *dw);
 
 /* nd forms of the four compute calls: the device's local products on its
- * nd shares, on the same kernels. Views, dtypes, scopes, streams and errors
- * are those of the 1-D calls, with nd layouts in place of 1-D ones (all
+ * nd shares, on the same kernels. Views, dtypes, scopes, workspaces, streams
+ * and errors are those of the 1-D calls, with nd layouts in place of 1-D ones (all
  * layouts of one call agree on ndim, p and c, else SBP_ERR_LAYOUT).
  * Local output shapes: X_r is the nd share of X, and so on; Y_r = X_r W_r,
  * dX_r = dY_r W_r^T, dW_r = X_r^T dY_r. An output is Partial-sum -- and must
@@ -269,21 +296,21 @@ int sbp_nd_signature(const sbp_nd_layout_t *x, const sbp_nd_layout_t *w,
 int sbp_nd_linear_fwd(const sbp_view_t *X, const sbp_nd_layout_t *lx,
                       const sbp_view_t *W, const sbp_nd_layout_t *lw,
                       sbp_view_t *Y, sbp_nd_layout_t *ly_out,
-                      hipStream_t stream);
+                      const sbp_workspace_t *ws, hipStream_t stream);
 int sbp_nd_linear_bwd_data(const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
                            const sbp_view_t *W, const sbp_nd_layout_t *lw,
                            sbp_view_t *dX, sbp_nd_layout_t *ldx_out,
-                           hipStream_t stream);
+                           const sbp_workspace_t *ws, hipStream_t stream);
 int sbp_nd_linear_bwd_weight(const sbp_view_t *X, const sbp_nd_layout_t *lx,
                              const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
                              sbp_view_t *dW, sbp_nd_layout_t *ldw_out,
-                             hipStream_t stream);
+                             const sbp_workspace_t *ws, hipStream_t stream);
 int sbp_nd_linear_bwd(const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
                       const sbp_view_t *X, const sbp_nd_layout_t *lx,
                       const sbp_view_t *W, const sbp_nd_layout_t *lw,
                       sbp_view_t *dX, sbp_nd_layout_t *ldx_out,
                       sbp_view_t *dW, sbp_nd_layout_t *ldw_out,
-                      hipStream_t stream);
+                      const sbp_workspace_t *ws, hipStream_t stream);
 
 /* ------------------------------ attention core under a head split --- */
 
@@ -325,7 +352,8 @@ typedef struct {
  * extent or stride, an output whose elements overlap one another, or an
  * output of the wrong shape), SBP_ERR_DTYPE, SBP_ERR_ALIGN, SBP_ERR_ALIAS
  * (an output's span overlaps an input's or the other output's span),
- * SBP_ERR_HIP. */
+ * SBP_ERR_HIP. Batched products never split their reduction, so these calls
+ * take no workspace. */
 int sbp_attn_scores(const sbp_view4_t *Q, const sbp_view4_t *K, sbp_view4_t *S,
                     int32_t p, int32_t r, hipStream_t stream);
 int sbp_attn_context(const sbp_view4_t *P, const sbp_view4_t *V, sbp_view4_t *O,
@@ -433,7 +461,8 @@ int sbp_last_hip_error(void);
  * dimensions, for input dtype in_dtype, output dtype out_dtype and operand
  * orientation op (0 forward, 1 backward-data, 2 backward-weight). Writes
  * the tile rows and columns, the number of reduction splits and the kernel
- * (3 fp32, else the bf16 instance code of sbp_set_plan_override). For benchmarks and
+ * (3 fp32, else the bf16 instance code of sbp_set_plan_override), as
+ * planned with a workspace of SBP_WORKSPACE_BYTES. For benchmarks and
  * tests; pure host function.
  * Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
 int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype,
@@ -445,8 +474,8 @@ int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype,
  * reduction of kd with output dtype out_d, the backward-weight product
  * mw x nw over kw with out_w. Writes whether both run as one grouped launch,
  * the tile of the backward-data product (shared when grouped), and the
- * splits and kernel of each product (kernel as in sbp_plan). Pure host
- * function. Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
+ * splits of each product, as planned with a workspace of
+ * SBP_WORKSPACE_BYTES. Pure host function. Errors: SBP_ERR_NULL, SBP_ERR_SHAPE, SBP_ERR_DTYPE. */
 int sbp_plan_bwd(int64_t md, int64_t nd, int64_t kd, int32_t out_d, int64_t mw,
                  int64_t nw, int64_t kw, int32_t out_w, int32_t *grouped,
                  int32_t *tile_m, int32_t *tile_n, int32_t *splits_d,
@@ -493,7 +522,7 @@ int sbp_profile_end(float *us, char *names, int name_len);
  * item; the grouped backward launch always runs one per item). A call whose
  * operands the pipelined kernel cannot read runs the generic kernel, where
  * 256x256 becomes 256x128; splits are clamped to the reduction blocks and to
- * the workspace. tile_m = 0 clears the override.
+ * the call's workspace. tile_m = 0 clears the override.
  * Errors: SBP_ERR_SHAPE for a (tile, kernel) pair not listed above,
  * splits < 1, or wgs_per_cu outside [0, 8]. */
 int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits,

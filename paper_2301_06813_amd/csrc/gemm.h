@@ -28,6 +28,9 @@ struct Gemm {
     int64_t ldc;
     int64_t m, n, k;
     int accumulate = 0;    // fp32 output only: C += product instead of C = product
+    // fp32 elements of caller workspace this product may use for split
+    // partials (0: the reduction is never split)
+    size_t ws_floats = 0;
     // batched products (attention core): batches x heads independent
     // products; element strides between consecutive batches / heads of A, B, C
     int64_t batches = 1, heads = 1;
@@ -55,12 +58,15 @@ int device_cus();
 // multiples of 8 elements, and tile offsets that fit 31-bit buffer offsets.
 bool dma_eligible(const Gemm &g);
 
-// Workspace the split reduction needs, per (device, stream): splits slices
-// of m x n fp32 partials.
-constexpr size_t WS_FLOATS = size_t(32) << 20;   // 128 MiB
+// Workspace of the split reduction: `splits` slices of m x n fp32 partials.
+// Plans never use more than WS_FLOATS_PREFERRED floats, however large the
+// caller's workspace, so that a workspace of that size always gets the
+// library's preferred plan (the value of SBP_WORKSPACE_BYTES / 4).
+constexpr size_t WS_FLOATS_PREFERRED = size_t(16) << 20;   // 64 MiB
 
 // bf16 planning: heuristic choice of tile and splits (an override may be set
-// per thread through sbp_set_plan_override). Always fits the workspace.
+// per thread through sbp_set_plan_override). The partials of a split plan
+// always fit g.ws_floats; with no workspace the reduction is not split.
 Plan plan_bf16(const Gemm &g);
 bool tile_supported(int bm, int bn, bool dma);
 void set_override(int bm, int bn, int splits, int kernel);   // bm = 0 clears
@@ -69,6 +75,9 @@ void set_override_orients(int mask);   // bit o: the override applies to orienta
 void set_bwd_override(int mode, int splits_w);   // 0 default, 1 separate, 2 grouped
 bool override_supported(int bm, int bn, int kernel);
 int kernel_code(const Plan &p);   // kernel code of a plan, as sbp_plan reports it
+
+// Workspace floats a plan's partials take (0 without splits).
+size_t plan_ws_floats(const Gemm &g, const Plan &p);
 
 // GEMM of plan p; with p.splits > 1 it writes partials to ws and then runs
 // the split reduction into g.C.
@@ -84,6 +93,8 @@ hipError_t launch_split_reduce_pair(const Gemm &gd, int sd, const float *wsd, co
 // plan_bf16_bwd returns true, *pd and *pw share a pipelined tile and
 // launch_bf16_bwd_group runs both in one grid (then the split reductions);
 // otherwise the two products run as separate launches of their own plans.
+// Both products share one workspace of gd.ws_floats floats (gw.ws_floats
+// must be equal): a grouped plan's partials of both fit it together.
 bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw);
 hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
                                  const Plan &pw, float *ws, hipStream_t s);

@@ -142,11 +142,16 @@ void split_of(int kb_total, int s, int *splits, int *per) {
     *splits = (kb_total + p - 1) / p;
 }
 
+// Workspace floats available to a product: the caller's, capped at the
+// preferred size so that plans do not depend on workspaces beyond it.
+double ws_budget(const Gemm &g) {
+    return (double)std::min(g.ws_floats, WS_FLOATS_PREFERRED);
+}
+
 bool fits_ws(const Gemm &g, int splits) {
     if (splits == 1) return true;
     if (g.nbatch() > 1) return false;   // batched launches never split
-
-    return (double)splits * (double)g.m * (double)g.n <= (double)WS_FLOATS;
+    return (double)splits * (double)g.m * (double)g.n <= ws_budget(g);
 }
 
 // Work items of one product under (tile, splits): count, time per item, and
@@ -285,9 +290,9 @@ int device_cus() {
 
 namespace {
 struct Key {
-    int64_t v[10];
+    int64_t v[11];
     bool operator==(const Key &o) const {
-        for (int i = 0; i < 10; ++i)
+        for (int i = 0; i < 11; ++i)
             if (v[i] != o.v[i]) return false;
         return true;
     }
@@ -295,14 +300,14 @@ struct Key {
 struct KeyHash {
     size_t operator()(const Key &k) const {
         size_t h = 1469598103934665603ull;
-        for (int i = 0; i < 10; ++i) h = (h ^ (size_t)k.v[i]) * 1099511628211ull;
+        for (int i = 0; i < 11; ++i) h = (h ^ (size_t)k.v[i]) * 1099511628211ull;
         return h;
     }
 };
 Key key_of(const Gemm &g, bool dma) {
     return Key{{g.orient, g.in_dtype, g.out_dtype, g.m, g.n, g.k, dma ? 1 : 0,
                 ov_bm * 1000 + ov_bn, ((ov_splits * 100 + ov_kernel) * 100 + ov_occ) * 8 + ov_orients,
-                g.nbatch()}};
+                g.nbatch(), (int64_t)std::min(g.ws_floats, WS_FLOATS_PREFERRED)}};
 }
 thread_local std::unordered_map<Key, Plan, KeyHash> plan_cache;
 }  // namespace
@@ -329,7 +334,11 @@ static bool grouped_plan(const Gemm &gd, const Gemm &gw, const Instance *in, int
     }
     return (pd->splits > 1 ? (double)pd->splits * gd.m * gd.n : 0.0) +
                (pw->splits > 1 ? (double)pw->splits * gw.m * gw.n : 0.0) <=
-           (double)WS_FLOATS;
+           ws_budget(gd);
+}
+
+size_t plan_ws_floats(const Gemm &g, const Plan &p) {
+    return p.splits > 1 ? (size_t)p.splits * (size_t)g.m * (size_t)g.n : 0;
 }
 
 bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
@@ -375,8 +384,8 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
         pw->bk = pd->bk;
         pd->occ = pw->occ = 0;   // the grouped launch runs one workgroup per item
         return pd->dma && pw->dma &&
-               (double)pd->splits * gd.m * gd.n + (double)pw->splits * gw.m * gw.n <=
-                   (double)WS_FLOATS;
+               (double)plan_ws_floats(gd, *pd) + (double)plan_ws_floats(gw, *pw) <=
+                   ws_budget(gd);
     }
     const TileClass *sep_d = nullptr, *sep_w = nullptr;
     for (const TileClass &t : kDma) {
@@ -409,7 +418,7 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
                 if (sw > 1 && perw < 2) continue;
                 const double wsz = (sd > 1 ? (double)sd * gd.m * gd.n : 0.0) +
                                    (sw > 1 ? (double)sw * gw.m * gw.n : 0.0);
-                if (wsz > (double)WS_FLOATS) continue;
+                if (wsz > ws_budget(gd)) continue;
                 const double tm = model_pair(gd, gw, t, sd, perd, sw, perw);
                 if (tm < best * 0.97) {
                     best = tm;

@@ -10,8 +10,6 @@
 #include <stdint.h>
 #include <string.h>
 
-#include <map>
-#include <mutex>
 #include <utility>
 
 #include "../../include/sbp.h"
@@ -192,46 +190,51 @@ int check_output(const sbp_view_t *o, int64_t rows, int64_t cols, int32_t in_dty
 }
 
 // ---------------------------------------------------------------- workspace
-struct Workspace {
-    float *ws = nullptr;
-};
-std::mutex g_ws_mu;
-std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+static_assert(SBP_WORKSPACE_BYTES == (int64_t)(sbpi::WS_FLOATS_PREFERRED * sizeof(float)),
+              "preferred workspace size");
 
-int workspace_for(hipStream_t s, Workspace *out) {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) {
-        g_last_hip = (int)e;
-        return SBP_ERR_HIP;
-    }
-    std::lock_guard<std::mutex> lk(g_ws_mu);
-    Workspace &w = g_ws[{dev, s}];
-    if (!w.ws) {
-        e = hipMalloc(&w.ws, sbpi::WS_FLOATS * sizeof(float));
-        if (e != hipSuccess) {
-            w = Workspace{};
-            g_last_hip = (int)e;
-            return SBP_ERR_HIP;
-        }
-    }
-    *out = w;
+// A caller's workspace (NULL: none): the split partials it can hold.
+struct Ws {
+    float *ptr = nullptr;
+    size_t floats = 0;
+    std::pair<uintptr_t, uintptr_t> span{0, 0};
+};
+
+int check_ws(const sbp_workspace_t *ws, Ws *out) {
+    *out = Ws{};
+    if (!ws || ws->bytes == 0) return SBP_OK;
+    if (ws->bytes < 0) return SBP_ERR_SHAPE;
+    if (!ws->data) return SBP_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(ws->data) & 15) return SBP_ERR_ALIGN;
+    out->ptr = static_cast<float *>(ws->data);
+    out->floats = (size_t)ws->bytes / sizeof(float);
+    const uintptr_t b = reinterpret_cast<uintptr_t>(ws->data);
+    out->span = {b, b + (uintptr_t)ws->bytes};
     return SBP_OK;
 }
 
-int run(const sbpi::Gemm &g, hipStream_t s) {
+// The workspace overlaps none of a product's operands or its output.
+bool ws_disjoint(const Ws &w, const sbpi::Gemm &g) {
+    if (!w.ptr) return true;
+    const bool a_km = g.orient != sbpi::OR_BWD_WEIGHT, b_km = g.orient == sbpi::OR_BWD_DATA;
+    const auto a = a_km ? extent(g.A, g.m, g.k, g.lda, g.in_dtype)
+                        : extent(g.A, g.k, g.m, g.lda, g.in_dtype);
+    const auto b = b_km ? extent(g.B, g.n, g.k, g.ldb, g.in_dtype)
+                        : extent(g.B, g.k, g.n, g.ldb, g.in_dtype);
+    const auto c = extent(g.C, g.m, g.n, g.ldc, g.out_dtype);
+    return !overlaps(w.span, a) && !overlaps(w.span, b) && !overlaps(w.span, c);
+}
+
+int run(sbpi::Gemm g, const Ws &w, hipStream_t s) {
     if (g.m == 0 || g.n == 0) return SBP_OK;
     hipError_t e;
     if (g.in_dtype == SBP_F32) {
         e = sbpi::launch_f32(g, s);
     } else {
-        sbpi::Plan p = sbpi::plan_bf16(g);
-        Workspace w;
-        if (p.splits > 1) {
-            int rc = workspace_for(s, &w);
-            if (rc) return rc;
-        }
-        e = sbpi::launch_bf16(g, p, w.ws, s);
+        g.ws_floats = w.floats;
+        const sbpi::Plan p = sbpi::plan_bf16(g);
+        if (sbpi::plan_ws_floats(g, p) > w.floats) return SBP_ERR_WORKSPACE;
+        e = sbpi::launch_bf16(g, p, w.ptr, s);
     }
     if (e != hipSuccess) {
         g_last_hip = (int)e;
@@ -239,7 +242,6 @@ int run(const sbpi::Gemm &g, hipStream_t s) {
     }
     return SBP_OK;
 }
-
 
 // ------------------------------------------------------------ nd layouts
 // The 1-D layout (kind, axis, p, r) of mesh axis a of an nd layout.
@@ -435,24 +437,23 @@ int hip_fail(hipError_t e) {
     return SBP_ERR_HIP;
 }
 
-int run_pair(const sbpi::Gemm &gd, const sbpi::Gemm &gw, hipStream_t s) {
+int run_pair(sbpi::Gemm gd, sbpi::Gemm gw, const Ws &w, hipStream_t s) {
     const bool ed = gd.m == 0 || gd.n == 0, ew = gw.m == 0 || gw.n == 0;
     if (gd.in_dtype == SBP_BF16 && !ed && !ew) {
+        gd.ws_floats = gw.ws_floats = w.floats;
         sbpi::Plan pd, pw;
         if (sbpi::plan_bf16_bwd(gd, gw, &pd, &pw)) {
-            Workspace w;
-            if (pd.splits > 1 || pw.splits > 1) {
-                int rc = workspace_for(s, &w);
-                if (rc) return rc;
-            }
-            hipError_t e = sbpi::launch_bf16_bwd_group(gd, pd, gw, pw, w.ws, s);
+            if (sbpi::plan_ws_floats(gd, pd) + sbpi::plan_ws_floats(gw, pw) > w.floats)
+                return SBP_ERR_WORKSPACE;
+            hipError_t e = sbpi::launch_bf16_bwd_group(gd, pd, gw, pw, w.ptr, s);
             if (e != hipSuccess) return hip_fail(e);
             return SBP_OK;
         }
     }
-    int rc = run(gd, s);
+    // two launches in stream order: each may use the whole workspace
+    int rc = run(gd, w, s);
     if (rc) return rc;
-    return run(gw, s);
+    return run(gw, w, s);
 }
 
 // The three input states of a backward call describe one signature: the
@@ -475,62 +476,85 @@ bool one_signature(const sbp_nd_layout_t *lx, const sbp_nd_layout_t *lw,
 
 template <class L>
 int linear_fwd(const sbp_view_t *X, const L *lx, const sbp_view_t *W, const L *lw,
-               sbp_view_t *Y, L *ly_out, hipStream_t stream) {
+               sbp_view_t *Y, L *ly_out, const sbp_workspace_t *ws, hipStream_t stream) {
     sbpi::Gemm g;
     L st;
     int rc = prep_fwd(X, lx, W, lw, Y, &g, &st);
     if (rc) return rc;
-    if ((rc = run(g, stream))) return rc;
+    Ws w;
+    if ((rc = check_ws(ws, &w))) return rc;
+    if (!ws_disjoint(w, g)) return SBP_ERR_ALIAS;
+    if ((rc = run(g, w, stream))) return rc;
     if (ly_out) *ly_out = st;
     return SBP_OK;
 }
 
 template <class L>
 int linear_bwd_data(const sbp_view_t *dY, const L *ldy, const sbp_view_t *W, const L *lw,
-                    sbp_view_t *dX, L *ldx_out, hipStream_t stream) {
+                    sbp_view_t *dX, L *ldx_out, const sbp_workspace_t *ws, hipStream_t stream) {
     sbpi::Gemm g;
     L st;
     int rc = prep_bwd_data(dY, ldy, W, lw, dX, &g, &st);
     if (rc) return rc;
-    if ((rc = run(g, stream))) return rc;
+    Ws w;
+    if ((rc = check_ws(ws, &w))) return rc;
+    if (!ws_disjoint(w, g)) return SBP_ERR_ALIAS;
+    if ((rc = run(g, w, stream))) return rc;
     if (ldx_out) *ldx_out = st;
     return SBP_OK;
 }
 
 template <class L>
 int linear_bwd_weight(const sbp_view_t *X, const L *lx, const sbp_view_t *dY, const L *ldy,
-                      sbp_view_t *dW, L *ldw_out, hipStream_t stream) {
+                      sbp_view_t *dW, L *ldw_out, const sbp_workspace_t *ws,
+                      hipStream_t stream) {
     sbpi::Gemm g;
     L st;
     int rc = prep_bwd_weight(X, lx, dY, ldy, dW, &g, &st);
     if (rc) return rc;
-    if ((rc = run(g, stream))) return rc;
+    Ws w;
+    if ((rc = check_ws(ws, &w))) return rc;
+    if (!ws_disjoint(w, g)) return SBP_ERR_ALIAS;
+    if ((rc = run(g, w, stream))) return rc;
     if (ldw_out) *ldw_out = st;
     return SBP_OK;
 }
 
+// Validation and operand mapping of both backward products (no HIP calls).
 template <class L>
-int linear_bwd(const sbp_view_t *dY, const L *ldy, const sbp_view_t *X, const L *lx,
-               const sbp_view_t *W, const L *lw, sbp_view_t *dX, L *ldx_out, sbp_view_t *dW,
-               L *ldw_out, hipStream_t stream) {
+int prep_bwd_pair(const sbp_view_t *dY, const L *ldy, const sbp_view_t *X, const L *lx,
+                  const sbp_view_t *W, const L *lw, sbp_view_t *dX, sbp_view_t *dW,
+                  sbpi::Gemm *gd, L *sd, sbpi::Gemm *gw, L *sw) {
     if (!dY || !X || !W || !dX || !dW || !ldy || !lx || !lw) return SBP_ERR_NULL;
     int rc = check_pair(lx, lw);
     if (rc) return rc;
     if ((rc = check_pair(ldy, lw))) return rc;
     // the three input states must describe one signature
     if (!one_signature(lx, lw, ldy)) return SBP_ERR_SIGNATURE;
-    sbpi::Gemm gd, gw;
-    L sd, sw;
-    if ((rc = prep_bwd_data(dY, ldy, W, lw, dX, &gd, &sd))) return rc;
-    if ((rc = prep_bwd_weight(X, lx, dY, ldy, dW, &gw, &sw))) return rc;
+    if ((rc = prep_bwd_data(dY, ldy, W, lw, dX, gd, sd))) return rc;
+    if ((rc = prep_bwd_weight(X, lx, dY, ldy, dW, gw, sw))) return rc;
     // no output may overlap the other output or the input it is not checked
     // against above (dX vs X, dW vs W)
     const auto ex = extent(dX->data, dX->rows, dX->cols, dX->ld, dX->dtype);
     const auto ew = extent(dW->data, dW->rows, dW->cols, dW->ld, dW->dtype);
-    const auto xr = extent(gw.A, gw.k, gw.m, gw.lda, gw.in_dtype);   // X_r: k x m view
-    const auto wr = extent(gd.B, gd.n, gd.k, gd.ldb, gd.in_dtype);   // W_r: n x k view
+    const auto xr = extent(gw->A, gw->k, gw->m, gw->lda, gw->in_dtype);   // X_r: k x m view
+    const auto wr = extent(gd->B, gd->n, gd->k, gd->ldb, gd->in_dtype);   // W_r: n x k view
     if (overlaps(ex, ew) || overlaps(ex, xr) || overlaps(ew, wr)) return SBP_ERR_ALIAS;
-    if ((rc = run_pair(gd, gw, stream))) return rc;
+    return SBP_OK;
+}
+
+template <class L>
+int linear_bwd(const sbp_view_t *dY, const L *ldy, const sbp_view_t *X, const L *lx,
+               const sbp_view_t *W, const L *lw, sbp_view_t *dX, L *ldx_out, sbp_view_t *dW,
+               L *ldw_out, const sbp_workspace_t *ws, hipStream_t stream) {
+    sbpi::Gemm gd, gw;
+    L sd, sw;
+    int rc = prep_bwd_pair(dY, ldy, X, lx, W, lw, dX, dW, &gd, &sd, &gw, &sw);
+    if (rc) return rc;
+    Ws w;
+    if ((rc = check_ws(ws, &w))) return rc;
+    if (!ws_disjoint(w, gd) || !ws_disjoint(w, gw)) return SBP_ERR_ALIAS;
+    if ((rc = run_pair(gd, gw, w, stream))) return rc;
     if (ldx_out) *ldx_out = sd;
     if (ldw_out) *ldw_out = sw;
     return SBP_OK;
@@ -539,7 +563,7 @@ int linear_bwd(const sbp_view_t *dY, const L *ldy, const sbp_view_t *X, const L 
 }  // namespace
 
 namespace sbpa {
-int run_gemm(const sbpi::Gemm &g, hipStream_t s) { return run(g, s); }
+int run_gemm(const sbpi::Gemm &g, hipStream_t s) { return run(g, Ws{}, s); }
 }  // namespace sbpa
 
 extern "C" {
@@ -585,27 +609,27 @@ int sbp_signature(const sbp_layout_t *x, const sbp_layout_t *w, sbp_layout_t *y,
 
 int sbp_linear_fwd(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *W,
                    const sbp_layout_t *lw, sbp_view_t *Y, sbp_layout_t *ly_out,
-                   hipStream_t stream) {
-    return linear_fwd(X, lx, W, lw, Y, ly_out, stream);
+                   const sbp_workspace_t *ws, hipStream_t stream) {
+    return linear_fwd(X, lx, W, lw, Y, ly_out, ws, stream);
 }
 
 int sbp_linear_bwd_data(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *W,
                         const sbp_layout_t *lw, sbp_view_t *dX, sbp_layout_t *ldx_out,
-                        hipStream_t stream) {
-    return linear_bwd_data(dY, ldy, W, lw, dX, ldx_out, stream);
+                        const sbp_workspace_t *ws, hipStream_t stream) {
+    return linear_bwd_data(dY, ldy, W, lw, dX, ldx_out, ws, stream);
 }
 
 int sbp_linear_bwd_weight(const sbp_view_t *X, const sbp_layout_t *lx, const sbp_view_t *dY,
                           const sbp_layout_t *ldy, sbp_view_t *dW, sbp_layout_t *ldw_out,
-                          hipStream_t stream) {
-    return linear_bwd_weight(X, lx, dY, ldy, dW, ldw_out, stream);
+                          const sbp_workspace_t *ws, hipStream_t stream) {
+    return linear_bwd_weight(X, lx, dY, ldy, dW, ldw_out, ws, stream);
 }
 
 int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *X,
                    const sbp_layout_t *lx, const sbp_view_t *W, const sbp_layout_t *lw,
                    sbp_view_t *dX, sbp_layout_t *ldx_out, sbp_view_t *dW,
-                   sbp_layout_t *ldw_out, hipStream_t stream) {
-    return linear_bwd(dY, ldy, X, lx, W, lw, dX, ldx_out, dW, ldw_out, stream);
+                   sbp_layout_t *ldw_out, const sbp_workspace_t *ws, hipStream_t stream) {
+    return linear_bwd(dY, ldy, X, lx, W, lw, dX, ldx_out, dW, ldw_out, ws, stream);
 }
 
 int sbp_mesh_coords(int32_t ndim, const int32_t *nodes, const int32_t *gpus, int64_t node,
@@ -673,27 +697,29 @@ int sbp_nd_signature(const sbp_nd_layout_t *x, const sbp_nd_layout_t *w, sbp_nd_
 
 int sbp_nd_linear_fwd(const sbp_view_t *X, const sbp_nd_layout_t *lx, const sbp_view_t *W,
                       const sbp_nd_layout_t *lw, sbp_view_t *Y, sbp_nd_layout_t *ly_out,
-                      hipStream_t stream) {
-    return linear_fwd(X, lx, W, lw, Y, ly_out, stream);
+                      const sbp_workspace_t *ws, hipStream_t stream) {
+    return linear_fwd(X, lx, W, lw, Y, ly_out, ws, stream);
 }
 
 int sbp_nd_linear_bwd_data(const sbp_view_t *dY, const sbp_nd_layout_t *ldy,
                            const sbp_view_t *W, const sbp_nd_layout_t *lw, sbp_view_t *dX,
-                           sbp_nd_layout_t *ldx_out, hipStream_t stream) {
-    return linear_bwd_data(dY, ldy, W, lw, dX, ldx_out, stream);
+                           sbp_nd_layout_t *ldx_out, const sbp_workspace_t *ws,
+                           hipStream_t stream) {
+    return linear_bwd_data(dY, ldy, W, lw, dX, ldx_out, ws, stream);
 }
 
 int sbp_nd_linear_bwd_weight(const sbp_view_t *X, const sbp_nd_layout_t *lx,
                              const sbp_view_t *dY, const sbp_nd_layout_t *ldy, sbp_view_t *dW,
-                             sbp_nd_layout_t *ldw_out, hipStream_t stream) {
-    return linear_bwd_weight(X, lx, dY, ldy, dW, ldw_out, stream);
+                             sbp_nd_layout_t *ldw_out, const sbp_workspace_t *ws,
+                             hipStream_t stream) {
+    return linear_bwd_weight(X, lx, dY, ldy, dW, ldw_out, ws, stream);
 }
 
 int sbp_nd_linear_bwd(const sbp_view_t *dY, const sbp_nd_layout_t *ldy, const sbp_view_t *X,
                       const sbp_nd_layout_t *lx, const sbp_view_t *W, const sbp_nd_layout_t *lw,
                       sbp_view_t *dX, sbp_nd_layout_t *ldx_out, sbp_view_t *dW,
-                      sbp_nd_layout_t *ldw_out, hipStream_t stream) {
-    return linear_bwd(dY, ldy, X, lx, W, lw, dX, ldx_out, dW, ldw_out, stream);
+                      sbp_nd_layout_t *ldw_out, const sbp_workspace_t *ws, hipStream_t stream) {
+    return linear_bwd(dY, ldy, X, lx, W, lw, dX, ldx_out, dW, ldw_out, ws, stream);
 }
 
 const char *sbp_strerror(int code) {
@@ -707,6 +733,7 @@ const char *sbp_strerror(int code) {
         case SBP_ERR_ALIAS: return "the output overlaps an input";
         case SBP_ERR_ALIGN: return "a data pointer is not aligned to its element size";
         case SBP_ERR_HIP: return "a HIP runtime call failed";
+        case SBP_ERR_WORKSPACE: return "the split partials of the call's plan do not fit its workspace";
     }
     return "unknown error code";
 }
@@ -733,6 +760,7 @@ int sbp_plan(int op, int64_t m, int64_t n, int64_t k, int32_t in_dtype, int32_t 
     static const char aligned[16] __attribute__((aligned(16))) = {0};
     const int64_t lda = (op == 2) ? m : k, ldb = (op == 1) ? k : n;
     sbpi::Gemm g{op, in_dtype, out_dtype, aligned, lda, aligned, ldb, nullptr, 0, m, n, k};
+    g.ws_floats = sbpi::WS_FLOATS_PREFERRED;
     sbpi::Plan p = sbpi::plan_bf16(g);
     *tile_m = p.bm;
     *tile_n = p.bn;
@@ -755,6 +783,7 @@ int sbp_plan_bwd(int64_t md, int64_t nd, int64_t kd, int32_t out_d, int64_t mw, 
                   md, nd, kd};
     sbpi::Gemm gw{sbpi::OR_BWD_WEIGHT, SBP_BF16, out_w, aligned, mw, aligned, nw, nullptr, 0,
                   mw, nw, kw};
+    gd.ws_floats = gw.ws_floats = sbpi::WS_FLOATS_PREFERRED;
     sbpi::Plan pd, pw;
     *grouped = sbpi::plan_bf16_bwd(gd, gw, &pd, &pw) ? 1 : 0;
     *tile_m = pd.bm;

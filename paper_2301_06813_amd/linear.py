@@ -121,20 +121,21 @@ def run(op: str, sig: str, p: int, r: int, X, W, dY, out, stream=None):
     return run_L(op, layouts(sig, p, r), X, W, dY, out, stream)
 
 
-def run_L(op: str, L: dict, X, W, dY, out, stream=None, accumulate=False):
+def run_L(op: str, L: dict, X, W, dY, out, stream=None, accumulate=False, ws=None):
     """As run, for the states in L (1-D or nd). accumulate: add the product
-    to out's fp32 contents (gradient accumulation)."""
+    to out's fp32 contents (gradient accumulation); ws: the workspace
+    argument of the binding (None: its default workspace)."""
     nd = isinstance(L["x"], sbp.sbp_nd_layout_t)
     fns = {"fwd": sbp.sbp_nd_linear_fwd if nd else sbp.sbp_linear_fwd,
            "bwd_data": sbp.sbp_nd_linear_bwd_data if nd else sbp.sbp_linear_bwd_data,
            "bwd_weight": sbp.sbp_nd_linear_bwd_weight if nd else sbp.sbp_linear_bwd_weight}
     o = sbp.view(out, sbp.SBP_ACCUMULATE if accumulate else sbp.SBP_LOCAL)
     if op == "fwd":
-        return fns[op](sbp.view(X), L["x"], sbp.view(W), L["w"], o, stream)
+        return fns[op](sbp.view(X), L["x"], sbp.view(W), L["w"], o, stream, ws)
     if op == "bwd_data":
-        return fns[op](sbp.view(dY), L["dy"], sbp.view(W), L["w"], o, stream)
+        return fns[op](sbp.view(dY), L["dy"], sbp.view(W), L["w"], o, stream, ws)
     if op == "bwd_weight":
-        return fns[op](sbp.view(X), L["x"], sbp.view(dY), L["dy"], o, stream)
+        return fns[op](sbp.view(X), L["x"], sbp.view(dY), L["dy"], o, stream, ws)
     raise ValueError(op)
 
 
@@ -144,13 +145,13 @@ def run_bwd(sig: str, p: int, r: int, X, W, dY, dX, dW, stream=None):
     return run_bwd_L(layouts(sig, p, r), X, W, dY, dX, dW, stream)
 
 
-def run_bwd_L(L: dict, X, W, dY, dX, dW, stream=None, accumulate_dw=False):
+def run_bwd_L(L: dict, X, W, dY, dX, dW, stream=None, accumulate_dw=False, ws=None):
     """Both backward products in one call; accumulate_dw adds dW to its fp32
     contents (gradient accumulation over micro-batches)."""
     fn = sbp.sbp_nd_linear_bwd if isinstance(L["x"], sbp.sbp_nd_layout_t) else sbp.sbp_linear_bwd
     return fn(sbp.view(dY), L["dy"], sbp.view(X), L["x"], sbp.view(W), L["w"],
               sbp.view(dX, sbp.SBP_LOCAL),
-              sbp.view(dW, sbp.SBP_ACCUMULATE if accumulate_dw else sbp.SBP_LOCAL), stream)
+              sbp.view(dW, sbp.SBP_ACCUMULATE if accumulate_dw else sbp.SBP_LOCAL), stream, ws)
 
 
 def call_bwd(sig: str, p: int, r: int, X, W, dY, stream=None):

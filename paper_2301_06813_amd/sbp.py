@@ -8,6 +8,12 @@ Loading fails loudly when the library has not been built
 ``view(tensor, scope)`` turns a 2-D torch tensor with unit column stride into
 an ``sbp_view_t`` (pointer, rows, cols, ld, dtype, scope); torch is used only
 for device memory and streams.
+
+The linear calls take a caller-owned workspace for split reductions
+(``sbp_workspace_t``). Their ``ws`` argument: None (default) uses a
+workspace of SBP_WORKSPACE_BYTES that this module allocates with torch once
+per (device, stream) and keeps; NO_WORKSPACE runs without one (no split
+reductions); a torch tensor or an ``sbp_workspace_t`` is used as given.
 """
 from __future__ import annotations
 
@@ -27,6 +33,8 @@ SBP_ERR_DTYPE = -5
 SBP_ERR_ALIAS = -6
 SBP_ERR_ALIGN = -7
 SBP_ERR_HIP = -8
+SBP_ERR_WORKSPACE = -9
+SBP_WORKSPACE_BYTES = 64 << 20
 
 SBP_SPLIT, SBP_BROADCAST, SBP_PARTIAL = 0, 1, 2
 SBP_BF16, SBP_F32 = 0, 1
@@ -107,6 +115,13 @@ class sbp_chain_t(ctypes.Structure):
                 ("allowed", ctypes.c_uint32)]
 
 
+class sbp_workspace_t(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("bytes", ctypes.c_int64)]
+
+
+NO_WORKSPACE = sbp_workspace_t(None, 0)
+
+
 class sbp_shard_t(ctypes.Structure):
     _fields_ = [("row_off", ctypes.c_int64), ("col_off", ctypes.c_int64),
                 ("rows", ctypes.c_int64), ("cols", ctypes.c_int64)]
@@ -164,14 +179,15 @@ def lib():
         L.sbp_shard_index.argtypes = [P(sbp_layout_t), ctypes.c_int64, ctypes.c_int64,
                                       P(sbp_shard_t)]
         L.sbp_signature.argtypes = [P(sbp_layout_t)] * 6
+        WS = P(sbp_workspace_t)
         for fn in ("sbp_linear_fwd", "sbp_linear_bwd_data", "sbp_linear_bwd_weight"):
             getattr(L, fn).argtypes = [P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
                                        P(sbp_layout_t), P(sbp_view_t), P(sbp_layout_t),
-                                       ctypes.c_void_p]
+                                       WS, ctypes.c_void_p]
         L.sbp_linear_bwd.argtypes = [P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
                                      P(sbp_layout_t), P(sbp_view_t), P(sbp_layout_t),
                                      P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
-                                     P(sbp_layout_t), ctypes.c_void_p]
+                                     P(sbp_layout_t), WS, ctypes.c_void_p]
         L.sbp_strerror.argtypes = [ctypes.c_int]
         L.sbp_strerror.restype = ctypes.c_char_p
         L.sbp_last_hip_error.argtypes = []
@@ -192,9 +208,10 @@ def lib():
         L.sbp_nd_signature.argtypes = [ND] * 6
         for fn in ("sbp_nd_linear_fwd", "sbp_nd_linear_bwd_data", "sbp_nd_linear_bwd_weight"):
             getattr(L, fn).argtypes = [P(sbp_view_t), ND, P(sbp_view_t), ND, P(sbp_view_t), ND,
-                                       ctypes.c_void_p]
+                                       WS, ctypes.c_void_p]
         L.sbp_nd_linear_bwd.argtypes = [P(sbp_view_t), ND, P(sbp_view_t), ND, P(sbp_view_t), ND,
-                                        P(sbp_view_t), ND, P(sbp_view_t), ND, ctypes.c_void_p]
+                                        P(sbp_view_t), ND, P(sbp_view_t), ND, WS,
+                                        ctypes.c_void_p]
         V4 = P(sbp_view4_t)
         for fn in ("sbp_attn_scores", "sbp_attn_context"):
             getattr(L, fn).argtypes = [V4, V4, V4, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
@@ -262,6 +279,35 @@ def current_stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+_default_ws = {}
+
+
+def workspace(t) -> sbp_workspace_t:
+    """sbp_workspace_t over a device tensor's bytes (kept alive by the caller)."""
+    return sbp_workspace_t(t.data_ptr(), t.numel() * t.element_size())
+
+
+def default_workspace(stream) -> sbp_workspace_t:
+    """This module's workspace for (current device, stream): SBP_WORKSPACE_BYTES
+    allocated with torch on first use and kept (calls on one stream run in
+    order, so they can share it)."""
+    import torch
+    key = (torch.cuda.current_device(), int(stream or 0))
+    t = _default_ws.get(key)
+    if t is None:
+        t = torch.empty(SBP_WORKSPACE_BYTES, dtype=torch.uint8, device="cuda")
+        _default_ws[key] = t
+    return workspace(t)
+
+
+def _ws(ws, stream):
+    if ws is None:
+        return default_workspace(stream)
+    if isinstance(ws, sbp_workspace_t):
+        return ws
+    return workspace(ws)
+
+
 # ------------------------------------------------------------- functions
 def sbp_strerror(code: int) -> str:
     return lib().sbp_strerror(code).decode()
@@ -281,43 +327,45 @@ def sbp_signature(x: sbp_layout_t, w: sbp_layout_t):
     return y, dy, dx, dw
 
 
-def _compute(fn, a, la, b, lb, out, stream):
+def _compute(fn, a, la, b, lb, out, stream, ws):
     lo = type(la)()
     s = current_stream() if stream is None else stream
+    w = _ws(ws, s)
     _check(getattr(lib(), fn)(ctypes.byref(a), ctypes.byref(la), ctypes.byref(b),
                               ctypes.byref(lb), ctypes.byref(out), ctypes.byref(lo),
-                              ctypes.c_void_p(s)))
+                              ctypes.byref(w), ctypes.c_void_p(s)))
     return lo
 
 
 def sbp_linear_fwd(X: sbp_view_t, lx: sbp_layout_t, W: sbp_view_t, lw: sbp_layout_t,
-                   Y: sbp_view_t, stream=None) -> sbp_layout_t:
+                   Y: sbp_view_t, stream=None, ws=None) -> sbp_layout_t:
     """Y_r = X_r W_r on `stream` (default: torch's current stream); returns Y's state."""
-    return _compute("sbp_linear_fwd", X, lx, W, lw, Y, stream)
+    return _compute("sbp_linear_fwd", X, lx, W, lw, Y, stream, ws)
 
 
 def sbp_linear_bwd_data(dY: sbp_view_t, ldy: sbp_layout_t, W: sbp_view_t, lw: sbp_layout_t,
-                        dX: sbp_view_t, stream=None) -> sbp_layout_t:
+                        dX: sbp_view_t, stream=None, ws=None) -> sbp_layout_t:
     """dX_r = dY_r W_r^T; returns dX's state."""
-    return _compute("sbp_linear_bwd_data", dY, ldy, W, lw, dX, stream)
+    return _compute("sbp_linear_bwd_data", dY, ldy, W, lw, dX, stream, ws)
 
 
 def sbp_linear_bwd_weight(X: sbp_view_t, lx: sbp_layout_t, dY: sbp_view_t, ldy: sbp_layout_t,
-                          dW: sbp_view_t, stream=None) -> sbp_layout_t:
+                          dW: sbp_view_t, stream=None, ws=None) -> sbp_layout_t:
     """dW_r = X_r^T dY_r; returns dW's state."""
-    return _compute("sbp_linear_bwd_weight", X, lx, dY, ldy, dW, stream)
+    return _compute("sbp_linear_bwd_weight", X, lx, dY, ldy, dW, stream, ws)
 
 
 def sbp_linear_bwd(dY: sbp_view_t, ldy: sbp_layout_t, X: sbp_view_t, lx: sbp_layout_t,
                    W: sbp_view_t, lw: sbp_layout_t, dX: sbp_view_t, dW: sbp_view_t,
-                   stream=None):
+                   stream=None, ws=None):
     """dX_r = dY_r W_r^T and dW_r = X_r^T dY_r in one call; returns (dX state, dW state)."""
     sx, sw = sbp_layout_t(), sbp_layout_t()
     s = current_stream() if stream is None else stream
+    w = _ws(ws, s)
     _check(lib().sbp_linear_bwd(ctypes.byref(dY), ctypes.byref(ldy), ctypes.byref(X),
                                 ctypes.byref(lx), ctypes.byref(W), ctypes.byref(lw),
                                 ctypes.byref(dX), ctypes.byref(sx), ctypes.byref(dW),
-                                ctypes.byref(sw), ctypes.c_void_p(s)))
+                                ctypes.byref(sw), ctypes.byref(w), ctypes.c_void_p(s)))
     return sx, sw
 
 
@@ -347,29 +395,32 @@ def sbp_nd_signature(x: sbp_nd_layout_t, w: sbp_nd_layout_t):
     return tuple(outs)
 
 
-def sbp_nd_linear_fwd(X, lx: sbp_nd_layout_t, W, lw: sbp_nd_layout_t, Y, stream=None):
+def sbp_nd_linear_fwd(X, lx: sbp_nd_layout_t, W, lw: sbp_nd_layout_t, Y, stream=None, ws=None):
     """Y_r = X_r W_r on nd shares; returns Y's nd state."""
-    return _compute("sbp_nd_linear_fwd", X, lx, W, lw, Y, stream)
+    return _compute("sbp_nd_linear_fwd", X, lx, W, lw, Y, stream, ws)
 
 
-def sbp_nd_linear_bwd_data(dY, ldy: sbp_nd_layout_t, W, lw: sbp_nd_layout_t, dX, stream=None):
+def sbp_nd_linear_bwd_data(dY, ldy: sbp_nd_layout_t, W, lw: sbp_nd_layout_t, dX, stream=None,
+                           ws=None):
     """dX_r = dY_r W_r^T on nd shares; returns dX's nd state."""
-    return _compute("sbp_nd_linear_bwd_data", dY, ldy, W, lw, dX, stream)
+    return _compute("sbp_nd_linear_bwd_data", dY, ldy, W, lw, dX, stream, ws)
 
 
-def sbp_nd_linear_bwd_weight(X, lx: sbp_nd_layout_t, dY, ldy: sbp_nd_layout_t, dW, stream=None):
+def sbp_nd_linear_bwd_weight(X, lx: sbp_nd_layout_t, dY, ldy: sbp_nd_layout_t, dW, stream=None,
+                             ws=None):
     """dW_r = X_r^T dY_r on nd shares; returns dW's nd state."""
-    return _compute("sbp_nd_linear_bwd_weight", X, lx, dY, ldy, dW, stream)
+    return _compute("sbp_nd_linear_bwd_weight", X, lx, dY, ldy, dW, stream, ws)
 
 
-def sbp_nd_linear_bwd(dY, ldy, X, lx, W, lw, dX, dW, stream=None):
+def sbp_nd_linear_bwd(dY, ldy, X, lx, W, lw, dX, dW, stream=None, ws=None):
     """Both backward products on nd shares in one call; returns (dX state, dW state)."""
     sx, sw = sbp_nd_layout_t(), sbp_nd_layout_t()
     s = current_stream() if stream is None else stream
+    w = _ws(ws, s)
     _check(lib().sbp_nd_linear_bwd(ctypes.byref(dY), ctypes.byref(ldy), ctypes.byref(X),
                                    ctypes.byref(lx), ctypes.byref(W), ctypes.byref(lw),
                                    ctypes.byref(dX), ctypes.byref(sx), ctypes.byref(dW),
-                                   ctypes.byref(sw), ctypes.c_void_p(s)))
+                                   ctypes.byref(sw), ctypes.byref(w), ctypes.c_void_p(s)))
     return sx, sw
 
 

@@ -144,7 +144,7 @@ def _code(c, fn="sbp_linear_fwd"):
     lo = sbp.sbp_layout_t()
     args = [c["x"], c["lx"], c["w"], c["lw"], c["y"]]
     return getattr(sbp.lib(), fn)(*(ctypes.byref(a) if a is not None else None for a in args),
-                                  ctypes.byref(lo), None)
+                                  ctypes.byref(lo), None, None)
 
 
 ERR_CASES = [
@@ -190,6 +190,41 @@ def test_forward_validation_errors(L, name, change, code):
     assert _code(_fwd_case(**change)) == code
 
 
+WS_ERR_CASES = [
+    ("negative size", sbp.sbp_workspace_t(0x60000000, -16), sbp.SBP_ERR_SHAPE),
+    ("null data", sbp.sbp_workspace_t(None, 4096), sbp.SBP_ERR_NULL),
+    ("misaligned", sbp.sbp_workspace_t(0x60000008, 4096), sbp.SBP_ERR_ALIGN),
+    ("overlaps X", sbp.sbp_workspace_t(XA + 1024, 4096), sbp.SBP_ERR_ALIAS),
+    ("overlaps W", sbp.sbp_workspace_t(WA - 1024, 4096), sbp.SBP_ERR_ALIAS),
+    ("overlaps Y", sbp.sbp_workspace_t(YA, 16), sbp.SBP_ERR_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,ws,code", WS_ERR_CASES, ids=[c[0] for c in WS_ERR_CASES])
+def test_workspace_validation(L, name, ws, code):
+    """The caller's workspace is checked on the host before any HIP call:
+    size, pointer, 16-byte alignment, and no overlap with the call's
+    operands or output."""
+    import ctypes
+    c = _fwd_case()
+    lo = sbp.sbp_layout_t()
+    args = [c["x"], c["lx"], c["w"], c["lw"], c["y"]]
+    rc = L.sbp_linear_fwd(*(ctypes.byref(a) for a in args), ctypes.byref(lo), ctypes.byref(ws),
+                          None)
+    assert rc == code
+    # the two-product call checks it against both products
+    dy = sbp.raw_view(YA, 64, 48, 48, BF)
+    dx = sbp.raw_view(0x40000000, 16, 32, 32, BF, sbp.SBP_LOCAL)
+    dw = sbp.raw_view(0x50000000, 32, 48, 48, F32, sbp.SBP_LOCAL)
+    if name == "overlaps Y":
+        ws = sbp.sbp_workspace_t(0x50000000 + 64, 16)   # inside dW
+    rc = L.sbp_linear_bwd(ctypes.byref(dy), ctypes.byref(sbp.split(0, 4, 1)), ctypes.byref(c["x"]),
+                          ctypes.byref(c["lx"]), ctypes.byref(c["w"]), ctypes.byref(c["lw"]),
+                          ctypes.byref(dx), ctypes.byref(lo), ctypes.byref(dw), ctypes.byref(lo),
+                          ctypes.byref(ws), None)
+    assert rc == code, (name, rc)
+
+
 def test_partial_output_must_be_fp32(L):
     # K-split forward: X S(1), W S(0) -> P; a bf16 output is rejected.
     c = dict(x=sbp.raw_view(XA, 64, 32, 32, BF), lx=sbp.split(1, 4, 1),
@@ -216,21 +251,21 @@ def test_backward_signature_errors(L):
     # bwd_data: (dY P, W S(0)) is no signature (dY is P only under BB, with W B)
     rc = sbp.lib().sbp_linear_bwd_data(ctypes.byref(dy), ctypes.byref(sbp.partial(4, 1)),
                                        ctypes.byref(w), ctypes.byref(sbp.split(0, 4, 1)),
-                                       ctypes.byref(dx), ctypes.byref(lo), None)
+                                       ctypes.byref(dx), ctypes.byref(lo), None, None)
     assert rc == sbp.SBP_ERR_SIGNATURE
     # bwd_weight: (X S(0), dY B) is no signature
     x = sbp.raw_view(XA, 64, 32, 32, BF)
     dw = sbp.raw_view(YA, 32, 48, 48, F32, sbp.SBP_LOCAL)
     rc = sbp.lib().sbp_linear_bwd_weight(ctypes.byref(x), ctypes.byref(sbp.split(0, 4, 1)),
                                          ctypes.byref(dy), ctypes.byref(sbp.broadcast(4, 1)),
-                                         ctypes.byref(dw), ctypes.byref(lo), None)
+                                         ctypes.byref(dw), ctypes.byref(lo), None, None)
     assert rc == sbp.SBP_ERR_SIGNATURE
     # bwd_weight DP: the dW output is Partial-sum, so a bf16 dW is rejected
     dyl = sbp.raw_view(XA + (1 << 20), 64, 48, 48, BF)
     dwb = sbp.raw_view(YA, 32, 48, 48, BF, sbp.SBP_LOCAL)
     rc = sbp.lib().sbp_linear_bwd_weight(ctypes.byref(x), ctypes.byref(sbp.split(0, 4, 1)),
                                          ctypes.byref(dyl), ctypes.byref(sbp.split(0, 4, 1)),
-                                         ctypes.byref(dwb), ctypes.byref(lo), None)
+                                         ctypes.byref(dwb), ctypes.byref(lo), None, None)
     assert rc == sbp.SBP_ERR_DTYPE
 
 
@@ -312,7 +347,7 @@ def _bwd_code(dy, ldy, x, lx, w, lw, dx, dw):
     return sbp.lib().sbp_linear_bwd(ctypes.byref(dy), ctypes.byref(ldy), ctypes.byref(x),
                                     ctypes.byref(lx), ctypes.byref(w), ctypes.byref(lw),
                                     ctypes.byref(dx), ctypes.byref(a), ctypes.byref(dw),
-                                    ctypes.byref(b), None)
+                                    ctypes.byref(b), None, None)
 
 
 def test_grouped_backward_validation(L):
@@ -347,7 +382,7 @@ def test_grouped_backward_validation(L):
     lo = sbp.sbp_layout_t()
     assert sbp.lib().sbp_linear_bwd_data(ctypes.byref(dy3), ctypes.byref(s3), ctypes.byref(w),
                                          ctypes.byref(b3), ctypes.byref(dx0), ctypes.byref(lo),
-                                         None) == sbp.SBP_OK
+                                         None, None) == sbp.SBP_OK
 
 
 def test_plan_bwd(L):

@@ -2,14 +2,18 @@
 
 The benchmark times its step by replaying a graph of library calls, so the
 replays must compute what the eager calls compute. A set of calls covering
-every signature and operation, the split reduction (which runs out of the
-per-stream workspace), the grouped backward launch and an accumulating
-weight gradient is made once eagerly on a side stream (this allocates the
-workspace) and then captured on that stream. The graph is replayed several
-times with other eager library calls on the same stream (same workspace) and
-synchronisations in between; after every replay each output must be
-bit-identical to the eager result (the kernels are deterministic), and the
-eager results themselves are exact against the oracle (integer inputs).
+every signature and operation, the split reduction (whose partials go to the
+caller's workspace), the grouped backward launch and an accumulating weight
+gradient is made once eagerly on a side stream and then captured on that
+stream. The graph is replayed several times with other eager library calls
+on the same stream (same workspace) and synchronisations in between; after
+every replay each output must be bit-identical to the eager result (the
+kernels are deterministic), and the eager results themselves are exact
+against the oracle (integer inputs).
+
+The library allocates nothing, so a capture needs no eager call first: the
+second test captures split and grouped calls on a fresh stream, with a
+workspace the caller allocated, and checks every replay against the oracle.
 """
 import numpy as np
 import pytest
@@ -133,3 +137,70 @@ def test_graph_replays_match_eager():
         for i, (g, w) in enumerate(zip(got, want)):
             assert np.array_equal(_bits(g), _bits(w)), (rep, i)
         assert np.array_equal(_bits(acc), _bits(want_acc)), rep
+
+
+def test_capture_on_fresh_stream_without_eager_call():
+    """Capture first, no eager warm-up: split plans, the grouped backward
+    launch and the split reduction inside a graph on a stream the library has
+    never seen; every replay is exact against the oracle."""
+    X, W, dY = _inputs(4300)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    ws = torch.empty(sbp.SBP_WORKSPACE_BYTES, dtype=torch.uint8, device="cuda")
+    cases = [c for c in CASES if c[3] is not None]
+    outs = [linear.alloc_out(op, sig, P, R, M, K, N, torch.bfloat16, "cuda")
+            for _, sig, op, _ in cases]
+    bwd = [(linear.alloc_out("bwd_data", sig, P, R, M, K, N, torch.bfloat16, "cuda"),
+            linear.alloc_out("bwd_weight", sig, P, R, M, K, N, torch.bfloat16, "cuda"))
+           for sig in BWD_CASES]
+    # the grouped plans of these pairs split their reductions
+    for sig in BWD_CASES:
+        L = linear.layouts(sig, P, R)
+        say("fresh capture: %s backward plan" % sig,
+            sbp.sbp_plan_bwd(*[int(v) for v in _pair_dims(L)]))
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    say("fresh capture: capture")
+    with torch.cuda.graph(graph, stream=stream):
+        sid = torch.cuda.current_stream().cuda_stream
+        for (name, sig, op, ov), out in zip(cases, outs):
+            sbp.sbp_set_plan_override(*ov)
+            try:
+                linear.run_L(op, linear.layouts(sig, P, R), X, W, dY, out, sid, ws=ws)
+            finally:
+                sbp.sbp_set_plan_override(0, 0, 1, 0)
+        for sig, (dX, dW) in zip(BWD_CASES, bwd):
+            sbp.sbp_set_plan_override(128, 128, 3, 4, 0)
+            sbp.sbp_set_bwd_override(2, 4)
+            try:
+                linear.run_bwd_L(linear.layouts(sig, P, R), X, W, dY, dX, dW, sid, ws=ws)
+            finally:
+                sbp.sbp_set_plan_override(0, 0, 1, 0)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for o in outs + [t for pair in bwd for t in pair]:
+            o.fill_(7)
+        torch.cuda.synchronize()
+        say("fresh capture: replay", rep)
+        with torch.cuda.stream(stream):
+            graph.replay()
+        torch.cuda.synchronize()
+        checks = [(op, sig, out) for (_, sig, op, _), out in zip(cases, outs)]
+        checks += [(op, sig, t) for sig, pair in zip(BWD_CASES, bwd)
+                   for op, t in zip(("bwd_data", "bwd_weight"), pair)]
+        for op, sig, out in checks:
+            ref = oracle_full(op, sig, P, R, Xh, Wh, dYh)
+            got = out_bits(out) if out.dtype == torch.bfloat16 else decode(out)
+            exp = oracle.round_bf16(ref) if out.dtype == torch.bfloat16 else ref
+            assert np.array_equal(got, exp), (rep, sig, op)
+
+
+def _pair_dims(L):
+    """(md, nd, kd, fp32 d, mw, nw, kw, fp32 w) of a backward pair at the test shape."""
+    dx = linear.out_shape("bwd_data", L, M, K, N)
+    dw = linear.out_shape("bwd_weight", L, M, K, N)
+    kd = linear.shard(L["dy"], M, N).cols
+    kw = linear.shard(L["x"], M, K).rows
+    fd = 1 if linear.is_partial(L["dx"]) else 0
+    fw = 1 if linear.is_partial(L["dw"]) else 0
+    return dx[0], dx[1], kd, fd, dw[0], dw[1], kw, fw

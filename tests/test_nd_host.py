@@ -148,7 +148,7 @@ def test_nd_call_validation(L):
 
     def call(y, x=X, w=W, llx=lx, llw=lw):
         with pytest.raises(sbp.SbpError) as ei:
-            sbp.sbp_nd_linear_fwd(x, llx, w, llw, y, stream=0)
+            sbp.sbp_nd_linear_fwd(x, llx, w, llw, y, stream=0, ws=sbp.NO_WORKSPACE)
         return ei.value.code
 
     # Y is Partial-sum on mesh axis 2, so a bf16 output is refused
@@ -170,5 +170,6 @@ def test_nd_call_validation(L):
     dY = sbp.raw_view(YA, 64, 48, 48, BF)
     with pytest.raises(sbp.SbpError) as ei:
         sbp.sbp_nd_linear_bwd(dY, ldy, X, lx, W, lw, sbp.raw_view(0x40000000, 32, 16, 16, BF, 1),
-                              sbp.raw_view(0x50000000, 16, 24, 24, F32, 1), stream=0)
+                              sbp.raw_view(0x50000000, 16, 24, 24, F32, 1), stream=0,
+                              ws=sbp.NO_WORKSPACE)
     assert ei.value.code == sbp.SBP_ERR_SIGNATURE
