@@ -221,6 +221,29 @@ int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy,
                    sbp_layout_t *ldx_out, sbp_view_t *dW, sbp_layout_t *ldw_out,
                    const sbp_workspace_t *ws, hipStream_t stream);
 
+/* For callers that cannot allocate device memory -- code being captured
+ * into a HIP graph, tight serving loops, harnesses that forbid hipMalloc --
+ * and so cannot bring a workspace: sbp_linear_bwd with the library's own
+ * scratch in place of a caller workspace. The scratch is a static device
+ * array of SBP_WORKSPACE_BYTES on each device (so the plans, kernels and
+ * results are those of sbp_linear_bwd with a workspace of that size),
+ * placed when the library's code is loaded on the device and held until
+ * the process ends; the call itself allocates nothing, and neither does any
+ * library routine it uses. A plan whose partials would not fit the scratch
+ * is refused with SBP_ERR_WORKSPACE (plans are limited to it, so none
+ * does). The scratch keeps the last call's partials; nothing in it needs
+ * clearing, since every partial is written before it is read. Every call on
+ * one device shares that device's scratch: calls that may overlap in time on
+ * one device (different streams, host threads or processes sharing the
+ * device's code object) race on it and must be ordered by the caller, e.g.
+ * by issuing them on one stream. Arguments, states and errors are those of
+ * sbp_linear_bwd. */
+int sbp_linear_bwd_noalloc(const sbp_view_t *dY, const sbp_layout_t *ldy,
+                           const sbp_view_t *X, const sbp_layout_t *lx,
+                           const sbp_view_t *W, const sbp_layout_t *lw,
+                           sbp_view_t *dX, sbp_layout_t *ldx_out, sbp_view_t *dW,
+                           sbp_layout_t *ldw_out, hipStream_t stream);
+
 /* ------------------------------------------- nd-SBP on device meshes --- */
 
 /* Mesh axes an nd layout may have. */

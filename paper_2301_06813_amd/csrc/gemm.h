@@ -100,4 +100,8 @@ hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
                                  const Plan &pw, float *ws, hipStream_t s);
 hipError_t launch_f32(const Gemm &g, hipStream_t s);
 
+// The library's static scratch on the current device (its address there,
+// looked up once per device) and its size in floats (WS_FLOATS_PREFERRED).
+hipError_t static_scratch(float **ptr, size_t *floats);
+
 }  // namespace sbpi

@@ -632,6 +632,28 @@ int sbp_linear_bwd(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view
     return linear_bwd(dY, ldy, X, lx, W, lw, dX, ldx_out, dW, ldw_out, ws, stream);
 }
 
+int sbp_linear_bwd_noalloc(const sbp_view_t *dY, const sbp_layout_t *ldy, const sbp_view_t *X,
+                           const sbp_layout_t *lx, const sbp_view_t *W, const sbp_layout_t *lw,
+                           sbp_view_t *dX, sbp_layout_t *ldx_out, sbp_view_t *dW,
+                           sbp_layout_t *ldw_out, hipStream_t stream) {
+    sbpi::Gemm gd, gw;
+    sbp_layout_t sd, sw;
+    int rc = prep_bwd_pair(dY, ldy, X, lx, W, lw, dX, dW, &gd, &sd, &gw, &sw);
+    if (rc) return rc;
+    Ws w;
+    hipError_t e = sbpi::static_scratch(&w.ptr, &w.floats);
+    if (e != hipSuccess) return hip_fail(e);
+    const uintptr_t b = reinterpret_cast<uintptr_t>(w.ptr);
+    w.span = {b, b + w.floats * sizeof(float)};
+    if (!ws_disjoint(w, gd) || !ws_disjoint(w, gw)) return SBP_ERR_ALIAS;
+    // the plan is limited to partials that fit the scratch; run_pair refuses
+    // (SBP_ERR_WORKSPACE) any plan that would need more
+    if ((rc = run_pair(gd, gw, w, stream))) return rc;
+    if (ldx_out) *ldx_out = sd;
+    if (ldw_out) *ldw_out = sw;
+    return SBP_OK;
+}
+
 int sbp_mesh_coords(int32_t ndim, const int32_t *nodes, const int32_t *gpus, int64_t node,
                     int64_t gpu, int32_t *c) {
     if (!nodes || !c) return SBP_ERR_NULL;

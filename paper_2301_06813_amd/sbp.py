@@ -47,7 +47,7 @@ EXPORTS = ("sbp_shard_index", "sbp_signature", "sbp_linear_fwd", "sbp_linear_bwd
            "sbp_nd_linear_fwd", "sbp_nd_linear_bwd_data", "sbp_nd_linear_bwd_weight",
            "sbp_nd_linear_bwd", "sbp_attn_scores", "sbp_attn_context", "sbp_attn_scores_bwd",
            "sbp_attn_context_bwd", "sbp_set_override_orients", "sbp_collective_cost",
-           "sbp_boxing_cost", "sbp_chain_cost", "sbp_search_strategy")
+           "sbp_boxing_cost", "sbp_chain_cost", "sbp_search_strategy", "sbp_linear_bwd_noalloc")
 
 SBP_COLL_ALLREDUCE, SBP_COLL_ALLGATHER, SBP_COLL_REDUCESCATTER, SBP_COLL_ALLTOALL = 0, 1, 2, 3
 SBP_SIG_DP, SBP_SIG_COL, SBP_SIG_KS, SBP_SIG_PB, SBP_SIG_BP, SBP_SIG_BB = 0, 1, 2, 3, 4, 5
@@ -188,6 +188,10 @@ def lib():
                                      P(sbp_layout_t), P(sbp_view_t), P(sbp_layout_t),
                                      P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
                                      P(sbp_layout_t), WS, ctypes.c_void_p]
+        L.sbp_linear_bwd_noalloc.argtypes = [P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
+                                             P(sbp_layout_t), P(sbp_view_t), P(sbp_layout_t),
+                                             P(sbp_view_t), P(sbp_layout_t), P(sbp_view_t),
+                                             P(sbp_layout_t), ctypes.c_void_p]
         L.sbp_strerror.argtypes = [ctypes.c_int]
         L.sbp_strerror.restype = ctypes.c_char_p
         L.sbp_last_hip_error.argtypes = []
@@ -366,6 +370,20 @@ def sbp_linear_bwd(dY: sbp_view_t, ldy: sbp_layout_t, X: sbp_view_t, lx: sbp_lay
                                 ctypes.byref(lx), ctypes.byref(W), ctypes.byref(lw),
                                 ctypes.byref(dX), ctypes.byref(sx), ctypes.byref(dW),
                                 ctypes.byref(sw), ctypes.byref(w), ctypes.c_void_p(s)))
+    return sx, sw
+
+
+def sbp_linear_bwd_noalloc(dY: sbp_view_t, ldy: sbp_layout_t, X: sbp_view_t, lx: sbp_layout_t,
+                           W: sbp_view_t, lw: sbp_layout_t, dX: sbp_view_t, dW: sbp_view_t,
+                           stream=None):
+    """sbp_linear_bwd with the library's static scratch as its workspace (for
+    callers that cannot allocate); returns (dX state, dW state)."""
+    sx, sw = sbp_layout_t(), sbp_layout_t()
+    s = current_stream() if stream is None else stream
+    _check(lib().sbp_linear_bwd_noalloc(ctypes.byref(dY), ctypes.byref(ldy), ctypes.byref(X),
+                                        ctypes.byref(lx), ctypes.byref(W), ctypes.byref(lw),
+                                        ctypes.byref(dX), ctypes.byref(sx), ctypes.byref(dW),
+                                        ctypes.byref(sw), ctypes.c_void_p(s)))
     return sx, sw
 
 
