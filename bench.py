@@ -161,15 +161,29 @@ class Step:
         return out
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, seconds):
-    """The oracle on a bounded sample of the same step: leading output rows of
-    every product of the first four layers' 16 linears, timed on the host cores."""
-    import numpy as np
+    """The oracle's plain fp32 triple loop (fp32 accumulator, increasing
+    reduction index) on a bounded sample of the same step: leading output
+    rows of every product of the first four layers' 16 linears, timed on the
+    host cores; plus workload 1 (every signature, rank and product of the
+    tiny fp32 linear) on one thread."""
     import oracle
     from paper_2301_06813_amd import inputs, workloads
     sig_id = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS}
     op_id = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
     oracle.build()
+    threads = oracle.threads()
     lins = wl.linears[:16]
     host = []
     for lin in lins:
@@ -184,8 +198,8 @@ def cpu_baseline(wl, seconds):
                 rows, cols, _, _ = oracle.out_shape(sig_id[lin.sig], op_id[op], lin.M, lin.K,
                                                     lin.N, wl.p, 0)
                 nr = min(nrows, rows)
-                oracle.linear(sig_id[lin.sig], op_id[op], Xh, Wh, dYh, wl.p, 0,
-                              rows=range(0, nr))
+                oracle.linear_f32(sig_id[lin.sig], op_id[op], Xh, Wh, dYh, wl.p, 0,
+                                  rows=range(0, nr))
                 # every local product of a linear is 2 M K N / p flops
                 fl += lin.flops_per_op(wl.p) * nr / rows
         return fl, time.perf_counter() - t0
@@ -200,11 +214,34 @@ def cpu_baseline(wl, seconds):
         nrows *= 2
     nrows = max(1, min(8192, int(nrows * seconds / max(t1, 1e-6))))
     fl, t = run(nrows)
-    cores = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
-    return {"value": fl / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+
+    # workload 1 on one thread: 3 signatures x 4 ranks x 3 products
+    oracle.set_threads(1)
+    try:
+        fl1, t_1 = 0.0, time.perf_counter()
+        for w1 in workloads.tiny_fp32():
+            (lin,) = w1.linears
+            Xh, Wh, dYh = (inputs.host_bits(t_) for t_ in workloads.make_tensors(
+                lin, torch_float32(), "cpu"))
+            for r in w1.ranks:
+                for op in OPS:
+                    oracle.linear_f32(sig_id[lin.sig], op_id[op], Xh, Wh, dYh, w1.p, r)
+                    fl1 += lin.flops_per_op(w1.p)
+        t_1 = time.perf_counter() - t_1
+    finally:
+        oracle.set_threads(threads)
+    return {"value": fl / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": "first %d output rows of each of the 48 local products of layers 0-3 "
-                      "(qkv/out/fc1/fc2 x fwd/bwd_data/bwd_weight), rank 0; %.3g GFLOP in %.1f s"
-                      % (nrows, fl / 1e9, t)}
+                      "(qkv/out/fc1/fc2 x fwd/bwd_data/bwd_weight), rank 0, plain fp32 "
+                      "triple loop; %.3g GFLOP in %.1f s" % (nrows, fl / 1e9, t),
+            "cpu_model": cpu_model(), "threads_available": len(os.sched_getaffinity(0)),
+            "workload1_single_thread": {"ms": t_1 * 1e3, "gflops": fl1 / t_1 / 1e9,
+                                        "products": 36, "threads": 1}}
+
+
+def torch_float32():
+    import torch
+    return torch.float32
 
 
 def report_workload(cid, ranks, reps):
@@ -378,6 +415,38 @@ def report_attention(r, reps):
             "calls": rows}
 
 
+def describe(label, sh):
+    """Shapes (m x n x k) of the products one kernel launch of a call computes."""
+    if "data" in sh:   # a grouped backward pair
+        return "bwd_data %dx%dx%d + bwd_weight %dx%dx%d" % (
+            sh["data"]["m"], sh["data"]["n"], sh["data"]["k"], sh["weight"]["m"],
+            sh["weight"]["n"], sh["weight"]["k"])
+    return "%s %dx%dx%d" % (label, sh["m"], sh["n"], sh["k"])
+
+
+def step_stats(xs):
+    """Mean with its 99 % confidence interval (Student t), and median with a
+    distribution-free 99 % interval from order statistics, of per-step times
+    (ms)."""
+    import math
+    import statistics
+    n = len(xs)
+    out = {"n": n, "mean": statistics.fmean(xs), "median": statistics.median(xs),
+           "min": min(xs), "max": max(xs)}
+    if n >= 2:
+        from scipy import stats as st
+        sd = statistics.stdev(xs)
+        half = st.t.ppf(0.995, n - 1) * sd / math.sqrt(n)
+        out["mean_ci99"] = [float(out["mean"] - half), float(out["mean"] + half)]
+        # ranks j < k with P(x_(j) <= median <= x_(k)) >= 0.99 (binomial)
+        ys = sorted(xs)
+        j = int(st.binom.ppf(0.005, n, 0.5))
+        k = n - j
+        if j >= 1 and k <= n:
+            out["median_ci99"] = [ys[j - 1], ys[k - 1]]
+    return out
+
+
 def sbp_split(D, p, r):
     """(offset, length) of rank r's balanced block of D over p (the library's rule)."""
     from paper_2301_06813_amd import sbp
@@ -451,18 +520,21 @@ def main():
         torch.cuda.synchronize()
 
     log("timing %d steps (%s)" % (args.steps, "eager" if args.eager else "graph"))
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # an event before the first step and after every step: the pair around
+    # all K steps gives the step time, consecutive pairs each step's own
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     with torch.cuda.stream(stream):
-        t0.record()
-        for _ in range(args.steps):
+        ev[0].record()
+        for i in range(args.steps):
             if graph is not None:
                 graph.replay()
             else:
                 step.launch_all(sid)
-        t1.record()
+            ev[i + 1].record()
     torch.cuda.synchronize()
-    ms = t0.elapsed_time(t1) / args.steps
+    ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    per_step = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     tflops = step.flops / (ms * 1e-3) / 1e12
 
     # per-kernel durations: the library records a HIP event pair with every
@@ -531,6 +603,29 @@ def main():
     roof["launches_per_step"] = kn
     roof["avg_launch_us"] = kt / kn * 1e6
     roof["algorithmic_intensity_flop_per_byte"] = intensity
+    # the dominant kernel serves several calls (product shapes): each one's
+    # own fraction of the same bound
+    per = collections.OrderedDict()
+    for m, ks in zip(step.meta, per_call):
+        for j, (name, us) in enumerate(ks):
+            if name != dom:
+                continue
+            gemm_ks = [n_ for n_, _ in ks if n_.startswith("gemm")]
+            if len(gemm_ks) == 2:
+                first = gemm_ks.index(name) == 0
+                sh, label = (m["data"], "bwd_data") if first else (m["weight"], "bwd_weight")
+            else:
+                sh, label = m, m["ops"][0]
+            key = "%s %s: %s" % (m["linear"].split("_", 1)[1], m["sig"], describe(label, sh))
+            e = per.setdefault(key, [0, 0.0, sh["flops"], sh["bytes"]])
+            e[0] += 1
+            e[1] += us
+    roof["per_product"] = []
+    for key, (n_, us_tot, fl_, by_) in per.items():
+        us_ = us_tot / n_
+        ach = by_ / us_ / 1e3 if roof["bound"] == "hbm" else fl_ / us_ / 1e6
+        roof["per_product"].append({"products": key, "launches": n_, "avg_us": us_,
+                                    "achieved": ach, "frac": ach / roof["peak"]})
 
     out = {
         "metric": "local-shard GEMM TFLOP/s (fwd+bwd) per SBP signature; % of bf16 MFMA peak",
@@ -556,6 +651,7 @@ def main():
                            1e3 * workloads.searched_signatures()[1], workloads.XGMI_ALPHA,
                            workloads.XGMI_BETA)} if args.workload == 8 else {})},
         "pct_of_bf16_peak": 100.0 * tflops / BF16_PEAK_TFLOPS,
+        "step_ms_stats": step_stats(per_step),
         "per_signature_tflops": {s: v[1] / v[0] / 1e12 for s, v in sorted(by_sig.items())},
         "kernel_time_sum_ms": sum(v[0] for v in by_kernel.values()) * 1e3,
         "roofline": roof,

@@ -3,8 +3,9 @@
 TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the
 benchmark's ``cpu_baseline`` leg may import this package; the product path
 (``paper_2301_06813_amd``) never does, and this package imports nothing from
-it. The arithmetic lives in ``oracle.c`` (plain C, fp64 accumulation); this
-module only builds it, loads it and marshals numpy arrays.
+it. The arithmetic lives in ``oracle.c`` (plain C, fp64 accumulation, and an
+fp32-accumulating form of the same loop); this module only builds it, loads
+it and marshals numpy arrays.
 
 What it computes follows AutoDDL Sec. 4.2 (the SBP matrix multiplication and
 its local matmul) and Sec. 4.3 (a broadcast weight receives partial-sum
@@ -28,7 +29,14 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "oracle.c")
-LIB = os.path.join(HERE, "liboracle.so")
+# ORACLE_SANITIZE=1: the default build is instrumented with AddressSanitizer
+# and UndefinedBehaviorSanitizer (any finding aborts); the process must then
+# preload the ASan runtime (tests/test_oracle_sanitized.py runs the oracle
+# pins that way)
+SANITIZE = os.environ.get("ORACLE_SANITIZE") == "1"
+LIB = os.path.join(HERE, "liboracle_san.so" if SANITIZE else "liboracle.so")
+SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=all"]
 
 # signature ids (the oracle's own numbering)
 DP, COL, KS, PB, BP, BB = 0, 1, 2, 3, 4, 5
@@ -52,8 +60,9 @@ def build(force: bool = False, src: str = SRC, out: str = LIB) -> str:
     """
     if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(src):
         tmp = out + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
-               "-std=c11", "-o", tmp, src, "-lm"]
+        opt = SAN_FLAGS if (SANITIZE and out == LIB) else ["-O2"]
+        cmd = ["gcc"] + opt + ["-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+                               "-std=c11", "-o", tmp, src, "-lm"]
         subprocess.check_call(cmd)
         os.replace(tmp, out)
     return out
@@ -82,6 +91,12 @@ class Oracle:
         lib.orc_linear_samples.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, i64, i64, i64,
                                            i64, i64, vp, vp, vp, i64, vp, vp, vp]
         lib.orc_linear_samples.restype = ctypes.c_int
+        lib.orc_linear_block_f32.argtypes = lib.orc_linear_block.argtypes
+        lib.orc_linear_block_f32.restype = ctypes.c_int
+        lib.orc_threads.argtypes = []
+        lib.orc_threads.restype = ctypes.c_int
+        lib.orc_set_threads.argtypes = [ctypes.c_int]
+        lib.orc_set_threads.restype = None
         lib.orc_round_bf16.argtypes = [vp, vp, i64]
         lib.orc_round_bf16.restype = None
         ci = ctypes.c_int
@@ -149,6 +164,30 @@ class Oracle:
         if rc != 0:
             raise ValueError("bad oracle arguments")
         return out
+
+    def linear_f32(self, sig: int, op: int, X, W, dY, p: int, r: int, rows=None, cols=None,
+                   M=None, K=None, N=None) -> np.ndarray:
+        """As linear(), with an fp32 accumulator (the plain fp32 triple loop):
+        returns float32."""
+        (X, W, dY), enc = _prep(X, W, dY)
+        M, K, N = _dims(X, W, dY, M, K, N)
+        orow, ocol, _, _ = self.out_shape(sig, op, M, K, N, p, r)
+        rows = range(orow) if rows is None else rows
+        cols = range(ocol) if cols is None else cols
+        out = np.empty((len(rows), len(cols)), dtype=np.float32)
+        rc = self.lib.orc_linear_block_f32(sig, op, enc, M, K, N, p, r, _ptr(X), _ptr(W),
+                                           _ptr(dY), rows.start, rows.start + len(rows),
+                                           cols.start, cols.start + len(cols), out.ctypes.data)
+        if rc != 0:
+            raise ValueError("bad oracle arguments")
+        return out
+
+    def threads(self) -> int:
+        """Threads the oracle's parallel loops use."""
+        return self.lib.orc_threads()
+
+    def set_threads(self, n: int) -> None:
+        self.lib.orc_set_threads(n)
 
     def linear_samples(self, sig: int, op: int, X, W, dY, p: int, r: int, ii, jj,
                        M=None, K=None, N=None) -> np.ndarray:
@@ -352,6 +391,18 @@ def linear(sig, op, X, W, dY, p, r, rows=None, cols=None, M=None, K=None, N=None
 
 def linear_samples(sig, op, X, W, dY, p, r, ii, jj, M=None, K=None, N=None):
     return default().linear_samples(sig, op, X, W, dY, p, r, ii, jj, M, K, N)
+
+
+def linear_f32(sig, op, X, W, dY, p, r, rows=None, cols=None, M=None, K=None, N=None):
+    return default().linear_f32(sig, op, X, W, dY, p, r, rows, cols, M, K, N)
+
+
+def threads() -> int:
+    return default().threads()
+
+
+def set_threads(n: int) -> None:
+    default().set_threads(n)
 
 
 def round_bf16(x) -> np.ndarray:

@@ -38,7 +38,10 @@
  * shift, fp32 as is) and every product and sum is taken in fp64, in
  * increasing reduction index, with no blocking or reordering. Products of two
  * fp32 values are exact in fp64, so the result is the exact product rounded
- * only by the fp64 running sum.
+ * only by the fp64 running sum. orc_linear_block_f32 is the same loop with
+ * an fp32 accumulator (each step c = fl32(c + fl32(a b)), built with
+ * -ffp-contract=off): the plain fp32 triple loop, for the fp32-path parity
+ * check and the timed CPU baseline.
  *
  * The nd-SBP section below extends this to device meshes (one state per
  * mesh axis).
@@ -52,6 +55,9 @@
 #include <stdint.h>
 #include <string.h>
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 /* ----------------------------------------------------------------- ids --- */
 /* signatures */
@@ -213,14 +219,38 @@ static double element(const orc_plan *pl, int op, int enc, int64_t K, int64_t N,
     return acc;
 }
 
-/*
- * Block [i0, i1) x [j0, j1) of rank r's output of operation op, as fp64,
- * written row-major into out ((i1-i0) x (j1-j0)). Inputs are the global,
- * contiguous row-major X (M x K), W (K x N) and dY (M x N); only the tensors
- * the operation reads need to be non-null. Returns 0, or -1 on a bad
- * argument (unknown signature/op, rank out of range, block outside the
- * output).
- */
+/* The same dot product with an fp32 accumulator: c = fl32(c + fl32(a b)) at
+ * every step, in increasing reduction index. */
+static float element_f32(const orc_plan *pl, int op, int enc, int64_t K, int64_t N,
+                         const void *X, const void *W, const void *dY, int64_t i,
+                         int64_t j)
+{
+    float acc = 0.0f;
+    if (op == ORC_FWD) {
+        for (int64_t t = 0; t < pl->x.nc; ++t) {
+            const float a = (float)decode(X, enc, (pl->x.r0 + i) * K + (pl->x.c0 + t));
+            const float b = (float)decode(W, enc, (pl->w.r0 + t) * N + (pl->w.c0 + j));
+            const float ab = a * b;
+            acc = acc + ab;
+        }
+    } else if (op == ORC_BWD_DATA) {
+        for (int64_t t = 0; t < pl->dy.nc; ++t) {
+            const float a = (float)decode(dY, enc, (pl->dy.r0 + i) * N + (pl->dy.c0 + t));
+            const float b = (float)decode(W, enc, (pl->w.r0 + j) * N + (pl->w.c0 + t));
+            const float ab = a * b;
+            acc = acc + ab;
+        }
+    } else {
+        for (int64_t t = 0; t < pl->x.nr; ++t) {
+            const float a = (float)decode(X, enc, (pl->x.r0 + t) * K + (pl->x.c0 + i));
+            const float b = (float)decode(dY, enc, (pl->dy.r0 + t) * N + (pl->dy.c0 + j));
+            const float ab = a * b;
+            acc = acc + ab;
+        }
+    }
+    return acc;
+}
+
 /* Fills block [i0, i1) x [j0, j1) of the output described by pl. */
 static int run_block(const orc_plan *pl, int op, int enc, int64_t K, int64_t N,
                      const void *X, const void *W, const void *dY, int64_t i0,
@@ -270,6 +300,45 @@ int orc_linear_block(int sig, int op, int enc, int64_t M, int64_t K, int64_t N,
     orc_plan pl;
     if (make_plan(sig, op, M, K, N, p, r, &pl) != 0) return -1;
     return run_block(&pl, op, enc, K, N, X, W, dY, i0, i1, j0, j1, out);
+}
+
+/* As orc_linear_block, accumulating in fp32 (element_f32); out is fp32. */
+int orc_linear_block_f32(int sig, int op, int enc, int64_t M, int64_t K, int64_t N,
+                         int64_t p, int64_t r, const void *X, const void *W,
+                         const void *dY, int64_t i0, int64_t i1, int64_t j0,
+                         int64_t j1, float *out)
+{
+    orc_plan pl;
+    if (make_plan(sig, op, M, K, N, p, r, &pl) != 0) return -1;
+    if (enc != ORC_IN_BF16 && enc != ORC_IN_F32) return -1;
+    if (i0 < 0 || j0 < 0 || i1 < i0 || j1 < j0 || i1 > pl.out_rows || j1 > pl.out_cols)
+        return -1;
+    int64_t w = j1 - j0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = i0; i < i1; ++i)
+        for (int64_t j = j0; j < j1; ++j)
+            out[(i - i0) * w + (j - j0)] = element_f32(&pl, op, enc, K, N, X, W, dY, i, j);
+    return 0;
+}
+
+/* Threads the oracle's parallel loops use (omp_get_max_threads), and a way
+ * to change it (for single-thread timings); 1 without OpenMP. */
+int orc_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void orc_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
 }
 
 /* n single elements (ii[s], jj[s]) of rank r's output, as fp64. */

@@ -325,6 +325,85 @@ def test_guard_bands_untouched():
             sbp.sbp_set_plan_override(0, 0, 1)
 
 
+def _guarded(rows, cols, dt, extra_ld, col_off):
+    """A NaN canvas with the output view inside it: one guard row above and
+    below, col_off guard columns on the left and the rest of the row (ld =
+    cols + extra_ld) on the right."""
+    buf = torch.full((rows + 2, cols + extra_ld), float("nan"), dtype=dt, device="cuda")
+    out = buf[1:rows + 1, col_off:col_off + cols]
+    guard = torch.ones_like(buf, dtype=torch.bool)
+    guard[1:rows + 1, col_off:col_off + cols] = False
+    return buf, out, guard
+
+
+def _kernel_names(fn):
+    """Names of the kernels the library launches in fn()."""
+    sbp.sbp_profile_begin(8)
+    try:
+        fn()
+    finally:
+        names = [n for n, _ in sbp.sbp_profile_end(8)]
+    return names
+
+
+# pipelined instances (kernel codes other than the generic 2), each with a
+# split reduction, plus persistent launches of two of them
+PIPE_CASES = [(t, k, 0) for (t, k) in TILE_KERNELS if k != 2] + [((128, 128), 1, 2),
+                                                               ((64, 64), 12, 1)]
+
+
+@pytest.mark.parametrize("extra_ld,col_off", [(7, 2), (8, 8)], ids=["unaligned", "aligned"])
+def test_guard_bands_pipelined_kernels(extra_ld, col_off):
+    """Shapes every pipelined instance can read (all shares and leading
+    dimensions multiples of 8): outputs inside a NaN canvas keep the canvas
+    NaN and are exact, through each epilogue (direct, staged, row-quad; split
+    partials and their reduction; persistent grids) and the grouped backward
+    launch. The profile of each call shows that a pipelined kernel ran. The
+    aligned canvas takes the 16-byte store paths, the unaligned one the
+    element stores."""
+    M, K, N, p, r = 176, 208, 144, 2, 1
+    X, W, dY = _int_inputs(M, K, N, 720)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    for tile, kernel, occ in PIPE_CASES:
+        sbp.sbp_set_plan_override(tile[0], tile[1], 2, kernel, occ)
+        try:
+            for sig in SIGS:
+                L = linear.layouts(sig, p, r)
+                for op in OPS:
+                    rows, cols = linear.out_shape(op, L, M, K, N)
+                    dt = linear.out_dtype(op, L, torch.bfloat16)
+                    buf, out, guard = _guarded(rows, cols, dt, extra_ld, col_off)
+                    names = _kernel_names(lambda: linear.run(op, sig, p, r, X, W, dY, out))
+                    torch.cuda.synchronize()
+                    assert any(n.startswith("gemm_bf16_dma_kernel") for n in names), names
+                    assert torch.all(torch.isnan(buf[guard])), (tile, kernel, occ, sig, op)
+                    want = oracle_full(op, sig, p, r, Xh, Wh, dYh)
+                    got = out_bits(out) if dt == torch.bfloat16 else decode(out)
+                    exp = oracle.round_bf16(want) if dt == torch.bfloat16 else want
+                    assert np.array_equal(got, exp), (tile, kernel, occ, sig, op)
+                if occ:
+                    continue
+                # both backward products in one grouped launch, each split
+                sbp.sbp_set_bwd_override(2, 3)
+                bufs = {}
+                for op in ("bwd_data", "bwd_weight"):
+                    rows, cols = linear.out_shape(op, L, M, K, N)
+                    bufs[op] = _guarded(rows, cols, linear.out_dtype(op, L, torch.bfloat16),
+                                        extra_ld, col_off)
+                names = _kernel_names(lambda: linear.run_bwd(
+                    sig, p, r, X, W, dY, bufs["bwd_data"][1], bufs["bwd_weight"][1]))
+                torch.cuda.synchronize()
+                assert any(n.startswith("gemm_bf16_dma_bwd_kernel") for n in names), names
+                for op, (buf, out, guard) in bufs.items():
+                    assert torch.all(torch.isnan(buf[guard])), (tile, kernel, sig, "pair", op)
+                    want = oracle_full(op, sig, p, r, Xh, Wh, dYh)
+                    got = out_bits(out) if out.dtype == torch.bfloat16 else decode(out)
+                    exp = oracle.round_bf16(want) if out.dtype == torch.bfloat16 else want
+                    assert np.array_equal(got, exp), (tile, kernel, sig, "pair", op)
+        finally:
+            sbp.sbp_set_plan_override(0, 0, 1)
+
+
 def test_split_reduction_is_deterministic():
     M, K, N = 384, 4096, 320
     g = torch.Generator(device="cuda").manual_seed(3)

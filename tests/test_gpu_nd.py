@@ -140,29 +140,44 @@ def test_nd_local_views_equal_global():
         assert torch.equal(out, ref), op
 
 
-def test_workload6_full_size_sampled():
+def test_workload6_full_size():
+    """Workload 6 at full size on every device of the mesh: device (0, 0, 0),
+    the one the benchmark times, over whole outputs; the other devices on a
+    random sample of elements plus the corners."""
     wl = workloads.transformer_3d()
     rng = np.random.default_rng(6)
+    full = (0, 0, 0)
+
+    def compare(op, out, c, what, want_full=None):
+        xs_, ws_ = _orc_states(lin.factors)
+        if tuple(c) == full:
+            want = want_full if want_full is not None else oracle.nd_linear(
+                OP_ID[op], Xh, Wh, dYh, xs_, ws_, wl.mesh, c)
+            rel = normwise_rel(decode(out), want)
+            assert rel <= TOL_BF16, (lin.name, what, op, c, rel)
+            return want
+        rows, cols = out.shape
+        ii = rng.integers(0, rows, 600)
+        jj = rng.integers(0, cols, 600)
+        ii[:4] = [0, 0, rows - 1, rows - 1]
+        jj[:4] = [0, cols - 1, 0, cols - 1]
+        got = decode(out[torch.as_tensor(ii, device="cuda"), torch.as_tensor(jj, device="cuda")])
+        want = oracle.nd_linear_samples(OP_ID[op], Xh, Wh, dYh, xs_, ws_, wl.mesh, c, ii, jj)
+        rel = normwise_rel(got, want)
+        assert rel <= TOL_BF16, (lin.name, what, op, c, rel)
+        return None
+
     for lin in wl.linears:
         X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
         Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
-        xs, ws = _orc_states(lin.factors)
         for c in wl.ranks:
+            wants = {}
             for op in OPS:
-                say(wl.name, lin.name, op, c)
+                say(wl.name, lin.name, op, c, "whole" if tuple(c) == full else "sampled")
                 out, st = linear.call_nd(op, lin.factors, wl.mesh, c, X, W, dY)
                 torch.cuda.synchronize()
                 _expect(op, lin.factors, wl.mesh, c, st, lin.M, lin.K, lin.N)
-                rows, cols = out.shape
-                ii = rng.integers(0, rows, 600)
-                jj = rng.integers(0, cols, 600)
-                ii[:4] = [0, 0, rows - 1, rows - 1]
-                jj[:4] = [0, cols - 1, 0, cols - 1]
-                got = decode(out[torch.as_tensor(ii, device="cuda"),
-                                 torch.as_tensor(jj, device="cuda")])
-                want = oracle.nd_linear_samples(OP_ID[op], Xh, Wh, dYh, xs, ws, wl.mesh, c, ii, jj)
-                rel = normwise_rel(got, want)
-                assert rel <= TOL_BF16, (lin.name, op, c, rel)
+                wants[op] = compare(op, out, c, "alone")
                 del out
             # the backward pair as the benchmark calls it (sbp_nd_linear_bwd)
             say(wl.name, lin.name, "bwd pair", c)
@@ -171,15 +186,6 @@ def test_workload6_full_size_sampled():
             _expect("bwd_data", lin.factors, wl.mesh, c, sx, lin.M, lin.K, lin.N)
             _expect("bwd_weight", lin.factors, wl.mesh, c, sw, lin.M, lin.K, lin.N)
             for op, out in (("bwd_data", dX), ("bwd_weight", dW)):
-                rows, cols = out.shape
-                ii = rng.integers(0, rows, 600)
-                jj = rng.integers(0, cols, 600)
-                ii[:4] = [0, 0, rows - 1, rows - 1]
-                jj[:4] = [0, cols - 1, 0, cols - 1]
-                got = decode(out[torch.as_tensor(ii, device="cuda"),
-                                 torch.as_tensor(jj, device="cuda")])
-                want = oracle.nd_linear_samples(OP_ID[op], Xh, Wh, dYh, xs, ws, wl.mesh, c, ii, jj)
-                rel = normwise_rel(got, want)
-                assert rel <= TOL_BF16, (lin.name, "pair", op, c, rel)
+                compare(op, out, c, "pair", wants[op])
             del dX, dW
         del X, W, dY

@@ -326,6 +326,83 @@ MUTATIONS = [
 ]
 
 
+def f32_failures(orc):
+    """Pins of the fp32-accumulating loop (orc_linear_block_f32), each fixed
+    by arithmetic rather than by the loop itself:
+    * integer inputs: every partial sum is an integer below 2^24, so the fp32
+      result equals the exact (fp64) one;
+    * a reduction of length 1 (K-split with p = K): the result is the single
+      product rounded once to fp32;
+    * recursive summation in increasing reduction order: [2^24, 1, -2^24] .
+      [1, 1, 1] gives fl(fl(2^24 + 1) - 2^24) = 0 in fp32, where the exact
+      sum is 1 (any other order, or a wider accumulator, gives 1);
+    * the error bound of recursive summation of products (Higham, Accuracy
+      and Stability of Numerical Algorithms, Sec. 3.1): |c - s| <=
+      gamma_n sum |a_k b_k|, gamma_n = n u / (1 - n u), u = 2^-24, for random
+      inputs, every op."""
+    bad = []
+    rng = np.random.default_rng(11)
+    M, K, N = 9, 14, 7
+    Xi, Wi, dYi = (rng.integers(-3, 4, s).astype(np.float32) for s in ((M, K), (K, N), (M, N)))
+    for sig in (oracle.DP, oracle.COL, oracle.KS):
+        for op in OPS:
+            a = orc.linear_f32(sig, op, Xi, Wi, dYi, 3, 1)
+            b = orc.linear(sig, op, Xi, Wi, dYi, 3, 1)
+            if a.dtype != np.float32 or not np.array_equal(a.astype(np.float64), b):
+                bad.append(("integer", sig, op))
+    X1 = rng.standard_normal((5, 4)).astype(np.float32)
+    W1 = rng.standard_normal((4, 6)).astype(np.float32)
+    for r in range(4):
+        got = orc.linear_f32(oracle.KS, oracle.FWD, X1, W1, None, 4, r, N=6)
+        want = (X1[:, r:r + 1].astype(np.float64) * W1[r:r + 1, :].astype(np.float64))
+        if not np.array_equal(got, want.astype(np.float32)):
+            bad.append(("single product", r))
+    Xo = np.array([[2.0 ** 24, 1.0, -(2.0 ** 24)]], dtype=np.float32)
+    Wo = np.ones((3, 1), dtype=np.float32)
+    if orc.linear_f32(oracle.DP, oracle.FWD, Xo, Wo, None, 1, 0, N=1)[0, 0] != 0.0:
+        bad.append("summation order")
+    if orc.linear(oracle.DP, oracle.FWD, Xo, Wo, None, 1, 0, N=1)[0, 0] != 1.0:
+        bad.append("exact reference of the order case")
+    Xr = rng.standard_normal((12, 40)).astype(np.float32)
+    Wr = rng.standard_normal((40, 10)).astype(np.float32)
+    dYr = rng.standard_normal((12, 10)).astype(np.float32)
+    u = 2.0 ** -24
+    for op in OPS:
+        got = orc.linear_f32(oracle.DP, op, Xr, Wr, dYr, 1, 0).astype(np.float64)
+        exact = orc.linear(oracle.DP, op, Xr, Wr, dYr, 1, 0)
+        absmag = orc.linear(oracle.DP, op, np.abs(Xr), np.abs(Wr), np.abs(dYr), 1, 0)
+        n = {oracle.FWD: 40, oracle.BWD_DATA: 10, oracle.BWD_WEIGHT: 12}[op]
+        gamma = n * u / (1 - n * u)
+        # the fp64 reference's own error is far below this bound
+        if np.any(np.abs(got - exact) > gamma * absmag * (1 + 1e-9)):
+            bad.append(("error bound", op))
+    return bad
+
+
+def test_f32_accumulation_pins(orc):
+    assert f32_failures(orc) == []
+
+
+F32_MUTATIONS = [
+    ("fp32 loop accumulates in fp64", "    float acc = 0.0f;", "    double acc = 0.0;"),
+    ("fp32 loop sums in decreasing order", "        for (int64_t t = 0; t < pl->x.nc; ++t) {",
+     "        for (int64_t t = pl->x.nc - 1; t >= 0; --t) {"),
+    ("fp32 loop reads X's neighbour column",
+     "(float)decode(X, enc, (pl->x.r0 + i) * K + (pl->x.c0 + t))",
+     "(float)decode(X, enc, (pl->x.r0 + i) * K + (pl->x.c0 + t + 1) % K)"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", F32_MUTATIONS, ids=[m[0] for m in F32_MUTATIONS])
+def test_planted_f32_mistakes_are_caught(tmp_path, name, old, new):
+    src = open(oracle.SRC).read()
+    assert src.count(old) == 1, "mutation anchor not found: " + name
+    mut = tmp_path / "oracle_mut.c"
+    mut.write_text(src.replace(old, new))
+    lib = oracle.build(force=True, src=str(mut), out=str(tmp_path / "liboracle_mut.so"))
+    assert f32_failures(oracle.Oracle(lib)), "planted mistake not caught: " + name
+
+
 @pytest.mark.parametrize("name,old,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
 def test_planted_mistakes_are_caught(tmp_path, name, old, new):
     src = open(oracle.SRC).read()
