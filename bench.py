@@ -620,12 +620,17 @@ def main():
             e = per.setdefault(key, [0, 0.0, sh["flops"], sh["bytes"]])
             e[0] += 1
             e[1] += us
+    # each call's products against their own roofline, min(peak, I x 8 TB/s):
+    # frac = roofline-minimum time / measured time
     roof["per_product"] = []
     for key, (n_, us_tot, fl_, by_) in per.items():
         us_ = us_tot / n_
-        ach = by_ / us_ / 1e3 if roof["bound"] == "hbm" else fl_ / us_ / 1e6
+        t_f, t_b = fl_ / (BF16_PEAK_TFLOPS * 1e6), by_ / (HBM_PEAK_GBS * 1e3)
         roof["per_product"].append({"products": key, "launches": n_, "avg_us": us_,
-                                    "achieved": ach, "frac": ach / roof["peak"]})
+                                    "bound": "mfma" if t_f >= t_b else "hbm",
+                                    "tflops": fl_ / us_ / 1e6, "gbs": by_ / us_ / 1e3,
+                                    "roofline_min_us": max(t_f, t_b),
+                                    "frac": max(t_f, t_b) / us_})
 
     out = {
         "metric": "local-shard GEMM TFLOP/s (fwd+bwd) per SBP signature; % of bf16 MFMA peak",
