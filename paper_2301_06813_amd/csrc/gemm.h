@@ -48,15 +48,25 @@ struct Plan {
     int epi = 0;           // pipelined kernel: epilogue (sbpk::EPI_DIRECT / _STAGED / _ROWQ)
     int occ = 0;           // persistent workgroups per compute unit (0: one per work item)
     int bk = 64;           // pipelined kernel: reduction elements per stage (64 or 32)
+    bool shift = false;    // pipelined kernel in the shifted index space (see dma_mode)
 };
 
 // Compute units of the current device (cached per device).
 int device_cus();
 
-// Whether the pipelined direct-to-LDS kernel can run this product: every
-// operand 16-byte aligned, leading dimensions and contiguous extents
-// multiples of 8 elements, and tile offsets that fit 31-bit buffer offsets.
+// Whether the pipelined direct-to-LDS kernel can run this product: leading
+// dimensions multiples of 8 elements (so every row of an operand sits at the
+// same offset within a 16-byte block), an offset along the reduction only
+// where both operands are k-major and share it, tile offsets that fit
+// 31-bit buffer offsets; batched products need aligned operands.
 bool dma_eligible(const Gemm &g);
+// 0: the generic kernel; 1: the pipelined kernel (operands 16-byte aligned,
+// contiguous extents multiples of 8); 2: the pipelined kernel's shifted
+// form (dma_eligible, but not 1), which only the instances of
+// SBP_DMA_SHIFT_INSTANCES have.
+int dma_mode(const Gemm &g);
+// Offset in elements of a bf16 pointer within its 16-byte block.
+int block_offset(const void *p);
 
 // Workspace of the split reduction: `splits` slices of m x n fp32 partials.
 // Plans never use more than WS_FLOATS_PREFERRED floats, however large the

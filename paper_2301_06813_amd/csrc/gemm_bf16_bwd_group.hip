@@ -7,10 +7,28 @@ namespace sbpi {
 namespace {
 
 template <bool OD, bool OW>
-hipError_t launch_group_tile(const Plan &p, const sbpk::GemmArgs &d, const sbpk::GemmArgs &w,
-                             int data_first, int grid, hipStream_t s) {
+hipError_t launch_group_tile(const Plan &p, const sbpk::GemmArgsShift &ds,
+                             const sbpk::GemmArgsShift &ws, int data_first, int grid,
+                             hipStream_t s) {
+    const sbpk::GemmArgs d = ds, w = ws;   // the unshifted kernels' arguments
     char name[192];
     const char *tf[2] = {"false", "true"};
+    if (p.shift) {
+#define SBP_BWD_SHIFT_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_)                         \
+    if (p.bm == BM_ && p.bn == BN_ && p.bk == BKD_ && (p.ns == 0 || p.ns == NS_) &&             \
+        p.kg == KG_ && p.epi == EPI_) {                                                        \
+        snprintf(name, sizeof(name),                                                           \
+                 "gemm_bf16_dma_bwd_kernel<%d, %d, %d, %d, %d, %d, %d, %d, %s, %s, true>",    \
+                 BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, tf[OD], tf[OW]);                 \
+        return launch_kernel(                                                                  \
+            sbpk::gemm_bf16_dma_bwd_kernel<BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, OD, OW, \
+                                           true>,                                              \
+            name, dim3(grid), dim3(64 * WGM_ * WGN_ * KG_), s, ds, ws, data_first);            \
+    }
+        SBP_DMA_SHIFT_INSTANCES(SBP_BWD_SHIFT_TILE)
+#undef SBP_BWD_SHIFT_TILE
+        return hipErrorInvalidValue;
+    }
 #define SBP_BWD_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_)                           \
     if (p.bm == BM_ && p.bn == BN_ && p.bk == BKD_ && (p.ns == 0 || p.ns == NS_) &&         \
         p.kg == KG_ && p.epi == EPI_) {                                                    \
@@ -32,13 +50,12 @@ hipError_t launch_group_tile(const Plan &p, const sbpk::GemmArgs &d, const sbpk:
 hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
                                  const Plan &pw, float *ws, hipStream_t s) {
     if (pd.bm != pw.bm || pd.bn != pw.bn || pd.bk != pw.bk || pd.ns != pw.ns || pd.kg != pw.kg ||
-        pd.epi != pw.epi ||
-        !pd.dma || !pw.dma)
+        pd.epi != pw.epi || pd.shift != pw.shift || !pd.dma || !pw.dma)
         return hipErrorInvalidValue;
     float *ws_w = ws;
     if (pd.splits > 1) ws_w = ws + (size_t)pd.splits * (size_t)gd.m * (size_t)gd.n;
-    const sbpk::GemmArgs d = make_args(gd, pd, ws);
-    const sbpk::GemmArgs w = make_args(gw, pw, ws_w);
+    const sbpk::GemmArgsShift d = make_args(gd, pd, ws);
+    const sbpk::GemmArgsShift w = make_args(gw, pw, ws_w);
     const int grid = d.tiles_m * d.tiles_n * d.splits + w.tiles_m * w.tiles_n * w.splits;
     const int data_first = pd.kblk_per_split >= pw.kblk_per_split;
     const bool od = gd.out_dtype == DT_F32 || pd.splits > 1;

@@ -96,6 +96,12 @@ struct KTileDma {
     }
 
     // Issue the loads of one stage: rows [mn0, mn0+BMN) x reduction [k0, k0+BK_).
+    // PART (shifted index spaces): a chunk that starts inside the operand is
+    // read whole -- its 16 bytes lie in one 16-byte block of a row that holds
+    // operand elements, so the read stays inside that row's memory -- and
+    // its elements past the limit are zeroed in LDS (zero_outside); else a
+    // chunk is read only if it lies wholly inside.
+    template <bool PART>
     __device__ __forceinline__ static void issue(const uint16_t *base, int64_t ld, int mn0,
                                                  int mn_lim, int k0, int k_lim, char *lds,
                                                  int wave, int lane) {
@@ -105,7 +111,8 @@ struct KTileDma {
             const int s = i * NW + wave;
             const int row = s * RPS + lane / CPR;
             const int c = (lane % CPR) ^ swz(row);
-            const bool ok = (mn0 + row < mn_lim) && (k0 + c * 8 + 8 <= k_lim);
+            const bool ok = (mn0 + row < mn_lim) &&
+                            (PART ? k0 + c * 8 < k_lim : k0 + c * 8 + 8 <= k_lim);
             const int voff = ok ? (int)((row * ld + c * 8) * 2) : OOB;
             dma16(r, lds + s * 1024, voff);
         }
@@ -116,6 +123,23 @@ struct KTileDma {
         const int row = r0 + (lane & 31);
         const int chunk = ks * 2 + (lane >> 5);
         return *reinterpret_cast<const bf16x8 *>(lds + off(row, chunk));
+    }
+
+    // In the stage holding reduction indices [k0, k0 + BK_): zeroes every
+    // element whose index lies outside [lo, hi) in the chunks that hold lo
+    // and hi (the only chunks read whole that can contain such elements),
+    // by nt threads.
+    __device__ static void zero_outside(char *lds, int k0, int lo, int hi, int tid, int nt) {
+        for (int q = tid; q < BMN * 2; q += nt) {
+            const int row = q >> 1;
+            const int kc = ((q & 1) ? hi : lo) & ~7;   // first index of the chunk
+            const int c = (kc - k0) >> 3;
+            if (kc < k0 || c >= CPR) continue;
+            uint16_t *p = reinterpret_cast<uint16_t *>(lds + off(row, c));
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (kc + e < lo || kc + e >= hi) p[e] = 0;
+        }
     }
 };
 
@@ -134,6 +158,9 @@ struct MNTileDma {
         return CPR >= 16 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
     }
 
+    // PART: as for KTileDma (a chunk past mn_lim holds only outputs that are
+    // never stored).
+    template <bool PART>
     __device__ __forceinline__ static void issue(const uint16_t *base, int64_t ld, int mn0,
                                                  int mn_lim, int k0, int k_lim, char *lds,
                                                  int wave, int lane) {
@@ -145,7 +172,8 @@ struct MNTileDma {
             const int row = byte / RB;
             const int phys = (byte % RB) >> 4;
             const int c = phys ^ swz(row);
-            const bool ok = (k0 + row < k_lim) && (mn0 + c * 8 + 8 <= mn_lim);
+            const bool ok = (k0 + row < k_lim) &&
+                            (PART ? mn0 + c * 8 < mn_lim : mn0 + c * 8 + 8 <= mn_lim);
             const int voff = ok ? (int)((row * ld + c * 8) * 2) : OOB;
             dma16(r, lds + s * 1024, voff);
         }
@@ -222,12 +250,13 @@ struct StageRow {
 
 // Stores the BM x BN fp32 tile staged in LDS (`tile`, row stride
 // LD floats) to rows [m0, m0 + BM) x columns [n0, n0 + BN) of C
-// (ld `ldc`, clipped to m x n), by all NT_ threads: each thread moves whole
+// (ld `ldc`, clipped to [0, m) x [0, n); m0 and n0 may be negative in a
+// shifted index space), by all NT_ threads: each thread moves whole
 // 16-byte chunks along a row -- 4 floats, or 8 values rounded to bf16 -- so a
 // wave writes whole contiguous row segments. `vec`: C's base and ldc allow
 // aligned 16-byte stores; otherwise (and at the right edge) elements are
 // stored one by one.
-template <int BM, int BN, int LD, int NT_, bool F32, bool ACC = false>
+template <int BM, int BN, int LD, int NT_, bool F32, bool ACC = false, bool SHIFT = false>
 __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t ldc, int m,
                                              int n, int m0, int n0, bool vec, int tid) {
     static_assert(F32 || !ACC, "accumulation needs an fp32 output");
@@ -240,12 +269,14 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
         const int q = it * NT_ + tid;
         const int r = q / CPR, c = (q % CPR) * EPC;
         const int row = m0 + r, col = n0 + c;
-        if (row >= m || col >= n) continue;
+        if (SHIFT ? ((unsigned)row >= (unsigned)m || col >= n || col + EPC <= 0)
+                  : (row >= m || col >= n))
+            continue;
         const float *src = tile + r * LD + c;
         if constexpr (F32) {
             f32x4 v = *reinterpret_cast<const f32x4 *>(src);
             float *dst = reinterpret_cast<float *>(C) + (int64_t)row * ldc + col;
-            if (vec && col + 4 <= n) {
+            if (vec && (!SHIFT || col >= 0) && col + 4 <= n) {
                 if constexpr (ACC) {
                     v += *reinterpret_cast<const f32x4 *>(dst);
                     *reinterpret_cast<f32x4 *>(dst) = v;
@@ -255,7 +286,7 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    if (col + e < n) {
+                    if (SHIFT ? (unsigned)(col + e) < (unsigned)n : col + e < n) {
                         if constexpr (ACC) dst[e] = dst[e] + v[e];
                         else st_nt(dst + e, v[e]);
                     }
@@ -264,7 +295,7 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
             const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
             const f32x4 b = *reinterpret_cast<const f32x4 *>(src + 4);
             uint16_t *dst = reinterpret_cast<uint16_t *>(C) + (int64_t)row * ldc + col;
-            if (vec && col + 8 <= n) {
+            if (vec && (!SHIFT || col >= 0) && col + 8 <= n) {
                 u32x4 w;
                 w[0] = (uint32_t)f32_to_bf16_bits(a[0]) | ((uint32_t)f32_to_bf16_bits(a[1]) << 16);
                 w[1] = (uint32_t)f32_to_bf16_bits(a[2]) | ((uint32_t)f32_to_bf16_bits(a[3]) << 16);
@@ -274,7 +305,8 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
             } else {
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    if (col + e < n) st_nt(dst + e, f32_to_bf16_bits(e < 4 ? a[e] : b[e - 4]));
+                    if (SHIFT ? (unsigned)(col + e) < (unsigned)n : col + e < n)
+                        st_nt(dst + e, f32_to_bf16_bits(e < 4 ? a[e] : b[e - 4]));
             }
         }
     }
@@ -300,8 +332,8 @@ enum : int {
 // LDS, so the next item may refill it; after the direct epilogue the caller
 // must synchronise the workgroup first.
 template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool A_KMAJ,
-          bool B_KMAJ, bool OUT_F32>
-__device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, char *smem) {
+          bool B_KMAJ, bool OUT_F32, bool SHIFT, class Args>
+__device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *smem) {
     constexpr int NSW = WGM * WGN;                // waves per reduction group
     constexpr int NW = NSW * KG;
     constexpr int WM = BM / WGM, WN = BN / WGN;
@@ -346,9 +378,13 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     const int tn = (t % (GROUP * g.tiles_n)) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // this split's reduction range [k_begin, k_lim)
+    // this split's reduction range [k_begin, k_lim) in the kernel's index
+    // space (the last split also takes the up to 7 extra elements of a
+    // reduction offset)
+    const int k_end = g.k + shift_k(g);
     const int k_begin = split * g.kchunk;
-    const int k_lim = min(g.k, k_begin + g.kchunk);
+    const int k_lim =
+        SHIFT && split == g.splits - 1 ? k_end : min(k_end, k_begin + g.kchunk);
     const int nkb = max(0, (k_lim - k_begin + BKD - 1) / BKD);
 
     using TA = DmaTileOf<BM, NW, BKD, A_KMAJ>;
@@ -357,10 +393,10 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     auto issue = [&](int kb, int stage) {
         char *base = smem + stage * STAGE;
         const int k0 = k_begin + kb * BKD;
-        TA::issue(Ab, g.lda, m0, g.m, k0, k_lim, base, wave, lane);
-        TB::issue(Bb, g.ldb, n0, g.n, k0, k_lim, base + A_BYTES, wave, lane);
+        TA::template issue<SHIFT>(Ab, g.lda, m0, g.m + shift_m(g), k0, k_lim, base, wave, lane);
+        TB::template issue<SHIFT>(Bb, g.ldb, n0, g.n + shift_n(g), k0, k_lim, base + A_BYTES, wave,
+                                  lane);
     };
-
     f32x16 acc[MI][NI];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -381,6 +417,21 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         if (it + NS - 1 < nkb) issue(it + NS - 1, (it + NS - 1) % NS);
 
         const char *cur = smem + (it % NS) * STAGE;
+        if constexpr (SHIFT) {
+            if (kmask_of(g) && (it == 0 || it == nkb - 1)) {
+                // a boundary step: zero the k-major tiles' elements outside
+                // the reduction (at most two partial chunks per row), then
+                // let every wave see them
+                const int k0 = k_begin + it * BKD;
+                if constexpr (A_KMAJ)
+                    TA::zero_outside(const_cast<char *>(cur), k0, shift_k(g), k_end, tid,
+                                     64 * NW);
+                if constexpr (B_KMAJ)
+                    TB::zero_outside(const_cast<char *>(cur) + A_BYTES, k0, shift_k(g), k_end,
+                                     tid, 64 * NW);
+                __syncthreads();
+            }
+        }
 #pragma unroll
         for (int kk = 0; kk < KSG; ++kk) {
             const int ks = kg * KSG + kk;
@@ -407,6 +458,12 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
     // kernel adds the slices in split order.
     const bool partial = g.splits > 1;
     float *const ws_out = g.ws + (size_t)split * (size_t)g.m * (size_t)g.n;
+    const bool ws_vec = g.n % 4 == 0 && shift_n(g) % 4 == 0;
+    // the tile's first output row and column (SHIFT: kernel index minus the
+    // shift; may be negative, and bounds are then checked as unsigned)
+    const int om0 = m0 - shift_m(g), on0 = n0 - shift_n(g);
+    // output index in range: [0, lim) when shifted, else below lim
+    auto inb = [](int i, int lim) { return SHIFT ? (unsigned)i < (unsigned)lim : i < lim; };
 
     if constexpr (EPI != EPI_DIRECT) __syncthreads();   // every wave is done with the pipeline's LDS
 
@@ -451,17 +508,17 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
             constexpr bool ACC = decltype(acc_tag)::value;
 #pragma unroll
             for (int i = 0; i < MI; ++i) {
-                const int row = m0 + wm * WM + i * 32 + (lane & 31);
-                if (row >= g.m) continue;
+                const int row = om0 + wm * WM + i * 32 + (lane & 31);
+                if (!inb(row, g.m)) continue;
 #pragma unroll
                 for (int j = 0; j < NI; ++j) {
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        const int col = n0 + wn * WN + j * 32 + 8 * q + 4 * (lane >> 5);
-                        if (col >= g.n) continue;
+                        const int col = on0 + wn * WN + j * 32 + 8 * q + 4 * (lane >> 5);
+                        if (col >= g.n || (SHIFT && col + 4 <= 0)) continue;
                         if constexpr (F32) {
                             float *dst = reinterpret_cast<float *>(out) + (int64_t)row * ldo + col;
-                            if (vec && col + 4 <= g.n) {
+                            if (vec && (!SHIFT || col >= 0) && col + 4 <= g.n) {
                                 f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1],
                                            acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
                                 if constexpr (ACC) {
@@ -473,7 +530,7 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                             } else {
 #pragma unroll
                                 for (int e = 0; e < 4; ++e)
-                                    if (col + e < g.n) {
+                                    if (inb(col + e, g.n)) {
                                         if constexpr (ACC)
                                             dst[e] = dst[e] + acc[i][j][4 * q + e];
                                         else
@@ -483,7 +540,7 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                         } else {
                             uint16_t *dst =
                                 reinterpret_cast<uint16_t *>(out) + (int64_t)row * ldo + col;
-                            if (vec && col + 4 <= g.n) {
+                            if (vec && (!SHIFT || col >= 0) && col + 4 <= g.n) {
                                 u32x2 w;
                                 w[0] = (uint32_t)f32_to_bf16_bits(acc[i][j][4 * q]) |
                                        ((uint32_t)f32_to_bf16_bits(acc[i][j][4 * q + 1]) << 16);
@@ -493,7 +550,7 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
                             } else {
 #pragma unroll
                                 for (int e = 0; e < 4; ++e)
-                                    if (col + e < g.n)
+                                    if (inb(col + e, g.n))
                                         st_nt(dst + e, f32_to_bf16_bits(acc[i][j][4 * q + e]));
                             }
                         }
@@ -502,7 +559,7 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
             }
         };
         if (partial)
-            store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n, g.n % 4 == 0);
+            store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n, ws_vec);
         else if (OUT_F32 && g.accumulate)
             store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
                       Cb, g.ldc, (bool)g.vec_c4);
@@ -546,14 +603,14 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         }
         __syncthreads();
         if (partial)
-            store_staged<BM, BN, LD, 64 * NW, true>(tile, ws_out, g.n, g.m, g.n, m0, n0,
-                                                    g.n % 4 == 0, tid);
+            store_staged<BM, BN, LD, 64 * NW, true, false, SHIFT>(tile, ws_out, g.n, g.m, g.n,
+                                                                  om0, on0, ws_vec, tid);
         else if (OUT_F32 && g.accumulate)
-            store_staged<BM, BN, LD, 64 * NW, OUT_F32, OUT_F32>(tile, Cb, g.ldc, g.m, g.n, m0,
-                                                                n0, g.vec_c4, tid);
+            store_staged<BM, BN, LD, 64 * NW, OUT_F32, OUT_F32, SHIFT>(
+                tile, Cb, g.ldc, g.m, g.n, om0, on0, g.vec_c4, tid);
         else
-            store_staged<BM, BN, LD, 64 * NW, OUT_F32>(tile, Cb, g.ldc, g.m, g.n, m0, n0,
-                                                       OUT_F32 ? g.vec_c4 : g.vec_c8, tid);
+            store_staged<BM, BN, LD, 64 * NW, OUT_F32, false, SHIFT>(
+                tile, Cb, g.ldc, g.m, g.n, om0, on0, OUT_F32 ? g.vec_c4 : g.vec_c8, tid);
         __syncthreads();   // the staged tile is free again
         return;
     }
@@ -565,13 +622,13 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
         for (int i = 0; i < MI; ++i) {
 #pragma unroll
             for (int j = 0; j < NI; ++j) {
-                const int col = n0 + wn * WN + j * 32 + (lane & 31);
-                const int rbase = m0 + wm * WM + i * 32 + 4 * (lane >> 5);
-                if (col < g.n) {
+                const int col = on0 + wn * WN + j * 32 + (lane & 31);
+                const int rbase = om0 + wm * WM + i * 32 + 4 * (lane >> 5);
+                if (inb(col, g.n)) {
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const int row = rbase + 8 * (r >> 2) + (r & 3);
-                        if (row < g.m) {
+                        if (inb(row, g.m)) {
                             if constexpr (F32 && ACC) {
                                 float *d = reinterpret_cast<float *>(out) + (int64_t)row * ldo + col;
                                 *d = *d + acc[i][j][r];
@@ -603,18 +660,21 @@ __device__ __forceinline__ void dma_tile_body(const GemmArgs &g, const int L, ch
 // every item of one workgroup maps to the same XCD under remap_xcd). With a
 // grid smaller than the item count, one item's output stores drain while
 // the next item's operand loads are in flight.
+template <bool SHIFT>
+using ArgsOf = typename std::conditional<SHIFT, GemmArgsShift, GemmArgs>::type;
+
 template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool A_KMAJ,
-          bool B_KMAJ, bool OUT_F32>
+          bool B_KMAJ, bool OUT_F32, bool SHIFT = false>
 __global__ __launch_bounds__(64 * WGM * WGN * KG,
                              (Occupancy<BM, BN, BKD, NS, WGM * WGN * KG, KG>::VALUE))
-void gemm_bf16_dma_kernel(GemmArgs g) {
+void gemm_bf16_dma_kernel(ArgsOf<SHIFT> g) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
     const int total = g.tiles_m * g.tiles_n * g.splits * g.nbatch;
     for (int v = blockIdx.x; v < total; v += gridDim.x) {
         // a later item refills the pipeline's LDS: every wave must be done
         // reading it (the direct epilogue does not end with a barrier)
         if (EPI == EPI_DIRECT && v != (int)blockIdx.x) __syncthreads();
-        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, A_KMAJ, B_KMAJ, OUT_F32>(
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, A_KMAJ, B_KMAJ, OUT_F32, SHIFT>(
             g, remap_xcd(v, total), smem);
     }
 }
@@ -626,10 +686,10 @@ void gemm_bf16_dma_kernel(GemmArgs g) {
 // items are longer is dispatched first (data_first) so that the short items
 // of the other fill the machine behind them.
 template <int BM, int BN, int BKD, int NS, int WGM, int WGN, int KG, int EPI, bool OUTD_F32,
-          bool OUTW_F32>
+          bool OUTW_F32, bool SHIFT = false>
 __global__ __launch_bounds__(64 * WGM * WGN * KG,
                              (Occupancy<BM, BN, BKD, NS, WGM * WGN * KG, KG>::VALUE))
-void gemm_bf16_dma_bwd_kernel(GemmArgs gd, GemmArgs gw, int data_first) {
+void gemm_bf16_dma_bwd_kernel(ArgsOf<SHIFT> gd, ArgsOf<SHIFT> gw, int data_first) {
     __shared__ __attribute__((aligned(1024))) char smem[NS * DmaStage<BM, BN, BKD, NS>::BYTES];
     const int wd = gd.tiles_m * gd.tiles_n * gd.splits * gd.nbatch;
     const int ww = gw.tiles_m * gw.tiles_n * gw.splits * gw.nbatch;
@@ -637,11 +697,11 @@ void gemm_bf16_dma_bwd_kernel(GemmArgs gd, GemmArgs gw, int data_first) {
     const bool is_data = data_first ? (b < wd) : (b >= ww);
     if (is_data) {
         const int local = data_first ? b : b - ww;
-        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, true, true, OUTD_F32>(
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, true, true, OUTD_F32, SHIFT>(
             gd, remap_xcd(local, wd), smem);
     } else {
         const int local = data_first ? b - wd : b;
-        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, false, false, OUTW_F32>(
+        dma_tile_body<BM, BN, BKD, NS, WGM, WGN, KG, EPI, false, false, OUTW_F32, SHIFT>(
             gw, remap_xcd(local, ww), smem);
     }
 }

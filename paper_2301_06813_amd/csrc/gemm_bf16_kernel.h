@@ -80,6 +80,30 @@ struct GemmArgs {
     int64_t sa_b, sa_h, sb_b, sb_h, sc_b, sc_h;
 };
 
+// Arguments of the pipelined kernel's shifted form, for operands that start
+// inside a 16-byte block (a shard view at an element offset that is not a
+// multiple of 8) or whose contiguous extent is not a multiple of 8: A and B
+// point at the 16-byte boundary at or below the view, and the kernel works
+// in an index space shifted by the view's offset within that block --
+// output rows by sm (an m-major A), output columns by sn (an n-major B), the
+// reduction by sk (both operands k-major, with the same offset). Kernel row
+// i is output row i - sm, and so on; reduction index kk is valid for
+// sk <= kk < sk + k. kmask: the first and last reduction chunks hold
+// elements outside that range (an offset, or k not a multiple of 8), which
+// the kernel zeroes in LDS before those steps. The unshifted kernels take
+// plain GemmArgs, and the accessors below give them zero shifts.
+struct GemmArgsShift : GemmArgs {
+    int32_t sm, sn, sk, kmask;
+};
+__device__ __forceinline__ int shift_m(const GemmArgs &) { return 0; }
+__device__ __forceinline__ int shift_n(const GemmArgs &) { return 0; }
+__device__ __forceinline__ int shift_k(const GemmArgs &) { return 0; }
+__device__ __forceinline__ int kmask_of(const GemmArgs &) { return 0; }
+__device__ __forceinline__ int shift_m(const GemmArgsShift &g) { return g.sm; }
+__device__ __forceinline__ int shift_n(const GemmArgsShift &g) { return g.sn; }
+__device__ __forceinline__ int shift_k(const GemmArgsShift &g) { return g.sk; }
+__device__ __forceinline__ int kmask_of(const GemmArgsShift &g) { return g.kmask; }
+
 // Operand and output bases of batch item z (uniform per work item).
 template <bool OUT_F32>
 __device__ __forceinline__ void batch_bases(const GemmArgs &g, int z, const uint16_t **A,

@@ -71,6 +71,17 @@ namespace sbpi {
     X(64, 128, 128, 3, 2, 2, 2, sbpk::EPI_ROWQ)                    \
     X(64, 64, 128, 4, 2, 2, 2, sbpk::EPI_ROWQ)
 
+// Instances that also exist in the shifted-index-space form (operands at an
+// offset within a 16-byte block, contiguous extents not multiples of 8: see
+// GemmArgs); plan.cpp's kShiftInstances lists the same ones.
+#define SBP_DMA_SHIFT_INSTANCES(X)                              \
+    X(64, 64, 64, SBP_NS_64x64, 2, 2, 1, sbpk::EPI_DIRECT)      \
+    X(128, 128, 64, 2, 2, 2, 1, sbpk::EPI_DIRECT)               \
+    X(64, 64, 128, 4, 2, 2, 2, sbpk::EPI_STAGED)                \
+    X(128, 64, 128, 3, 2, 2, 2, sbpk::EPI_STAGED)               \
+    X(64, 128, 128, 3, 2, 2, 2, sbpk::EPI_STAGED)               \
+    X(128, 128, 128, 2, 2, 2, 2, sbpk::EPI_STAGED)
+
 // Grid of a launch of `items` work items under plan p: one workgroup per item,
 // or (persistent plans) at most occ workgroups per compute unit, a multiple of 8.
 static inline int grid_of(const Plan &p, int items) {
@@ -81,10 +92,28 @@ static inline int grid_of(const Plan &p, int items) {
 }
 
 template <bool AK, bool BK_, bool OUTF>
-static hipError_t launch_tile(const Plan &p, const sbpk::GemmArgs &a, int items, hipStream_t s) {
+static hipError_t launch_tile(const Plan &p, const sbpk::GemmArgsShift &as, int items,
+                              hipStream_t s) {
+    const sbpk::GemmArgs a = as;   // the unshifted kernels' arguments
     char name[192];
     const char *tf[2] = {"false", "true"};
     const int grid = grid_of(p, items);
+    if (p.dma && p.shift) {
+#define SBP_DMA_SHIFT_TILE(BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_)                      \
+    if (p.bm == BM_ && p.bn == BN_ && p.bk == BKD_ && (p.ns == 0 || p.ns == NS_) &&          \
+        p.kg == KG_ && p.epi == EPI_) {                                                     \
+        snprintf(name, sizeof(name),                                                        \
+                 "gemm_bf16_dma_kernel<%d, %d, %d, %d, %d, %d, %d, %d, %s, %s, %s, true>",  \
+                 BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, tf[AK], tf[BK_], tf[OUTF]);    \
+        return launch_kernel(                                                               \
+            sbpk::gemm_bf16_dma_kernel<BM_, BN_, BKD_, NS_, WGM_, WGN_, KG_, EPI_, AK, BK_, \
+                                       OUTF, true>,                                         \
+            name, dim3(grid), dim3(64 * WGM_ * WGN_ * KG_), s, as);                         \
+    }
+        SBP_DMA_SHIFT_INSTANCES(SBP_DMA_SHIFT_TILE)
+#undef SBP_DMA_SHIFT_TILE
+        return hipErrorInvalidValue;
+    }
 #define SBP_TILE(BM_, BN_)                                                                  \
     if (!p.dma && p.bm == BM_ && p.bn == BN_) {                                             \
         snprintf(name, sizeof(name), "gemm_bf16_kernel<%d, %d, %s, %s, %s>", BM_, BN_,     \
@@ -116,10 +145,23 @@ static hipError_t launch_tile(const Plan &p, const sbpk::GemmArgs &a, int items,
 }
 
 // Kernel arguments of product g under plan p (partials, if split, go to ws).
-static inline sbpk::GemmArgs make_args(const Gemm &g, const Plan &p, float *ws) {
-    sbpk::GemmArgs a;
+static inline sbpk::GemmArgsShift make_args(const Gemm &g, const Plan &p, float *ws) {
+    sbpk::GemmArgsShift a;
     a.A = static_cast<const uint16_t *>(g.A);
     a.B = static_cast<const uint16_t *>(g.B);
+    a.sm = a.sn = a.sk = a.kmask = 0;
+    if (p.dma && p.shift) {
+        // operands at an offset within a 16-byte block: read from the block
+        // boundary, shift the kernel's index space (see GemmArgs)
+        const int oa = block_offset(g.A), ob = block_offset(g.B);
+        const bool ak = g.orient != OR_BWD_WEIGHT, bk = g.orient == OR_BWD_DATA;
+        a.A -= oa;
+        a.B -= ob;
+        a.sm = ak ? 0 : oa;
+        a.sn = bk ? 0 : ob;
+        a.sk = ak ? oa : 0;
+        a.kmask = ak && (a.sk != 0 || g.k % 8 != 0);
+    }
     a.C = g.C;
     a.lda = g.lda;
     a.ldb = g.ldb;
@@ -127,8 +169,8 @@ static inline sbpk::GemmArgs make_args(const Gemm &g, const Plan &p, float *ws) 
     a.m = (int32_t)g.m;
     a.n = (int32_t)g.n;
     a.k = (int32_t)g.k;
-    a.tiles_m = (int32_t)((g.m + p.bm - 1) / p.bm);
-    a.tiles_n = (int32_t)((g.n + p.bn - 1) / p.bn);
+    a.tiles_m = (int32_t)((g.m + a.sm + p.bm - 1) / p.bm);
+    a.tiles_n = (int32_t)((g.n + a.sn + p.bn - 1) / p.bn);
     a.splits = p.splits;
     a.kchunk = p.kblk_per_split * 64;
     a.ws = ws;
@@ -140,8 +182,10 @@ static inline sbpk::GemmArgs make_args(const Gemm &g, const Plan &p, float *ws) 
     const int64_t es = g.out_dtype == DT_F32 ? 4 : 2;
     const bool c16 = (reinterpret_cast<uintptr_t>(g.C) & 15) == 0 &&
                      (g.nbatch() == 1 || ((g.sc_b * es) % 16 == 0 && (g.sc_h * es) % 16 == 0));
-    a.vec_c4 = c16 && (g.ldc % 4 == 0);
-    a.vec_c8 = c16 && (g.ldc % 8 == 0);
+    // vector stores of whole 4- or 8-column groups: the shifted output
+    // columns must keep them aligned
+    a.vec_c4 = c16 && (g.ldc % 4 == 0) && a.sn % 4 == 0;
+    a.vec_c8 = c16 && (g.ldc % 8 == 0) && a.sn % 8 == 0;
     a.accumulate = g.accumulate;
     a.nbatch = (int32_t)g.nbatch();
     a.heads = (int32_t)g.heads;
@@ -156,7 +200,7 @@ static inline sbpk::GemmArgs make_args(const Gemm &g, const Plan &p, float *ws) 
 
 template <bool AK, bool BK_>
 static hipError_t launch_orient(const Gemm &g, const Plan &p, float *ws, hipStream_t s) {
-    const sbpk::GemmArgs a = make_args(g, p, ws);
+    const sbpk::GemmArgsShift a = make_args(g, p, ws);
     const int items = a.tiles_m * a.tiles_n * a.splits * a.nbatch;
     // with splits the GEMM writes fp32 partials, whatever the output dtype
     hipError_t e = (g.out_dtype == DT_F32 || p.splits > 1)

@@ -121,6 +121,26 @@ const TunedBwd kTunedBwd[] = {
     {-1, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0}   // end marker
 };
 
+// Instances with a shifted-index-space form (gemm_bf16_launch.h
+// SBP_DMA_SHIFT_INSTANCES): tile, reduction step, stages (0: the tile's
+// default), reduction groups, epilogue.
+struct ShiftInstance {
+    int bm, bn, bk, ns, kg, epi;
+};
+const ShiftInstance kShiftInstances[] = {
+    {64, 64, 64, 0, 1, E_DIRECT},     {128, 128, 64, 2, 1, E_DIRECT},
+    {64, 64, 128, 4, 2, E_STAGED},    {128, 64, 128, 3, 2, E_STAGED},
+    {64, 128, 128, 3, 2, E_STAGED},   {128, 128, 128, 2, 2, E_STAGED},
+};
+
+bool shift_capable(int bm, int bn, int bk, int ns, int kg, int epi) {
+    for (const ShiftInstance &i : kShiftInstances)
+        if (i.bm == bm && i.bn == bn && i.bk == bk && i.ns == ns && i.kg == kg && i.epi == epi)
+            return true;
+    return false;
+}
+bool shift_capable(const Plan &p) { return shift_capable(p.bm, p.bn, p.bk, p.ns, p.kg, p.epi); }
+
 const Instance *find_instance(int code, int bm, int bn) {
     for (const Instance &i : kInstances)
         if (i.code == code && i.bm == bm && i.bn == bn) return &i;
@@ -246,29 +266,51 @@ void set_override(int bm, int bn, int splits, int kernel) {
 static bool kmajor_a(int orient) { return orient != OR_BWD_WEIGHT; }
 static bool kmajor_b(int orient) { return orient == OR_BWD_DATA; }
 
+int block_offset(const void *p) {
+    return (int)((reinterpret_cast<uintptr_t>(p) >> 1) & 7);
+}
+
 bool dma_eligible(const Gemm &g) {
     if (g.in_dtype != DT_BF16) return false;
-    const auto al = [](const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
-    if (!al(g.A) || !al(g.B) || g.lda % 8 || g.ldb % 8) return false;
-    const int64_t a_contig = kmajor_a(g.orient) ? g.k : g.m;
-    const int64_t b_contig = kmajor_b(g.orient) ? g.k : g.n;
-    if (a_contig % 8 || b_contig % 8) return false;
-    // every batch item's operand bases stay 16-byte aligned
-    if (g.nbatch() > 1 && (g.sa_b % 8 || g.sa_h % 8 || g.sb_b % 8 || g.sb_h % 8)) return false;
+    // every row of an operand starts at the same offset within a 16-byte block
+    if (g.lda % 8 || g.ldb % 8) return false;
+    if ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.B)) & 1) return false;
+    const int oa = block_offset(g.A), ob = block_offset(g.B);
+    if (g.nbatch() > 1) {
+        // batched: every item's operand bases 16-byte aligned, ends on chunks
+        if (oa || ob) return false;
+        if (g.sa_b % 8 || g.sa_h % 8 || g.sb_b % 8 || g.sb_h % 8) return false;
+        if ((kmajor_a(g.orient) ? g.k : g.m) % 8 || (kmajor_b(g.orient) ? g.k : g.n) % 8)
+            return false;
+    }
+    // An offset along m or n shifts the output index; along the reduction
+    // both operands must be k-major with the same offset (a k-major A with
+    // an n-major B needs an aligned A).
+    if (g.orient == OR_FWD && oa) return false;
+    if (g.orient == OR_BWD_DATA && oa != ob) return false;
     // per-tile buffer offsets stay below 2^31 bytes
     return g.lda <= (int64_t(1) << 21) && g.ldb <= (int64_t(1) << 21);
 }
 
+int dma_mode(const Gemm &g) {
+    if (!dma_eligible(g)) return 0;
+    const int64_t a_contig = kmajor_a(g.orient) ? g.k : g.m;
+    const int64_t b_contig = kmajor_b(g.orient) ? g.k : g.n;
+    const bool aligned = block_offset(g.A) == 0 && block_offset(g.B) == 0 && a_contig % 8 == 0 &&
+                         b_contig % 8 == 0;
+    return aligned ? 1 : 2;
+}
+
 static Plan plan_uncached(const Gemm &g);
 
-// Tuned entry of product g (nullptr if none).
-static const Tuned *tuned_for(const Gemm &g, bool dma) {
+// Tuned entry of product g under pipelined-kernel mode `mode` (nullptr if none).
+static const Tuned *tuned_for(const Gemm &g, int mode) {
     if (g.in_dtype != DT_BF16) return nullptr;
     const int f32 = g.out_dtype == DT_F32 ? 1 : 0;
     for (const Tuned &t : kTuned) {
         if (t.orient < 0) break;
         if (t.orient == g.orient && t.out_f32 == f32 && t.m == g.m && t.n == g.n && t.k == g.k &&
-            t.dma == (dma ? 1 : 0) && t.nbatch == g.nbatch())
+            t.dma == mode && t.nbatch == g.nbatch())
             return &t;
     }
     return nullptr;
@@ -304,8 +346,8 @@ struct KeyHash {
         return h;
     }
 };
-Key key_of(const Gemm &g, bool dma) {
-    return Key{{g.orient, g.in_dtype, g.out_dtype, g.m, g.n, g.k, dma ? 1 : 0,
+Key key_of(const Gemm &g, int mode) {
+    return Key{{g.orient, g.in_dtype, g.out_dtype, g.m, g.n, g.k, mode,
                 ov_bm * 1000 + ov_bn, ((ov_splits * 100 + ov_kernel) * 100 + ov_occ) * 8 + ov_orients,
                 g.nbatch(), (int64_t)std::min(g.ws_floats, WS_FLOATS_PREFERRED)}};
 }
@@ -313,7 +355,7 @@ thread_local std::unordered_map<Key, Plan, KeyHash> plan_cache;
 }  // namespace
 
 Plan plan_bf16(const Gemm &g) {
-    const Key k = key_of(g, dma_eligible(g));
+    const Key k = key_of(g, dma_mode(g));
     auto it = plan_cache.find(k);
     if (it != plan_cache.end()) return it->second;
     const Plan p = plan_uncached(g);
@@ -326,10 +368,13 @@ Plan plan_bf16(const Gemm &g) {
 // given splits; false if it does not fit the workspace.
 static bool grouped_plan(const Gemm &gd, const Gemm &gw, const Instance *in, int bm, int bn,
                          int sd, int sw, Plan *pd, Plan *pw) {
+    const bool sh = dma_mode(gd) == 2 || dma_mode(gw) == 2;
+    if (sh && !shift_capable(bm, bn, in->bk, in->ns, in->kg, in->epi)) return false;
     for (int w = 0; w < 2; ++w) {
         const Gemm &g = w ? gw : gd;
         Plan &p = w ? *pw : *pd;
         p = Plan{bm, bn, 1, 1, true, in->ns, in->kg, in->epi, 0, in->bk};
+        p.shift = sh;
         split_of(kblocks(g.k), w ? sw : sd, &p.splits, &p.kblk_per_split);
     }
     return (pd->splits > 1 ? (double)pd->splits * gd.m * gd.n : 0.0) +
@@ -372,20 +417,23 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
             }
         }
         // measured plans of both products: they run as measured, one after the other
-        if (tuned_for(gd, true) && tuned_for(gw, true)) return false;
+        if (tuned_for(gd, dma_mode(gd)) && tuned_for(gw, dma_mode(gw))) return false;
     }
+    const bool sh = dma_mode(gd) == 2 || dma_mode(gw) == 2;
     if (ov_bm != 0) {
         // an override fixes the tile (and the splits of both products)
+        if (!pd->dma || !pw->dma) return false;
         pw->bm = pd->bm;
         pw->bn = pd->bn;
         pw->ns = pd->ns;
         pw->kg = pd->kg;
         pw->epi = pd->epi;
         pw->bk = pd->bk;
+        if (sh && !shift_capable(*pd)) return false;
+        pd->shift = pw->shift = sh;
         pd->occ = pw->occ = 0;   // the grouped launch runs one workgroup per item
-        return pd->dma && pw->dma &&
-               (double)plan_ws_floats(gd, *pd) + (double)plan_ws_floats(gw, *pw) <=
-                   ws_budget(gd);
+        return (double)plan_ws_floats(gd, *pd) + (double)plan_ws_floats(gw, *pw) <=
+               ws_budget(gd);
     }
     const TileClass *sep_d = nullptr, *sep_w = nullptr;
     for (const TileClass &t : kDma) {
@@ -402,6 +450,7 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
     bool grouped = false;
     const int kd = kblocks(gd.k), kw = kblocks(gw.k);
     for (const TileClass &t : kDma) {
+        if (sh && !shift_capable(t.bm, t.bn, t.bk, t.ns, t.kg, t.epi)) continue;
         int last_d = 0;
         for (int a = 1; a <= 16; ++a) {
             int sd, perd;
@@ -425,6 +474,7 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
                     grouped = true;
                     *pd = Plan{t.bm, t.bn, sd, perd, true, t.ns, t.kg, t.epi, 0, t.bk};
                     *pw = Plan{t.bm, t.bn, sw, perw, true, t.ns, t.kg, t.epi, 0, t.bk};
+                    pd->shift = pw->shift = sh;
                 }
             }
         }
@@ -434,22 +484,35 @@ bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
 
 static Plan plan_uncached(const Gemm &g) {
     const int kb_total = kblocks(g.k);
-    const bool dma = dma_eligible(g);
+    const int mode = dma_mode(g);
+    const bool dma = mode > 0;
     Plan best{128, 128, 1, std::max(1, kb_total), dma};
+    if (mode == 2) {
+        best.ns = 2;   // the two-stage 128 x 128 instance has a shifted form
+        best.shift = true;
+    }
     if (ov_bm != 0 && ((ov_orients >> g.orient) & 1)) {
         // kernel: 0 or 1 the tile's default pipelined instance (if eligible),
         // 2 generic, other codes the instance of kInstances (if eligible);
-        // a product the pipelined kernel cannot read runs the generic kernel
-        const bool use_dma = dma && ov_kernel != 2;
+        // a product the pipelined kernel cannot read runs the generic kernel,
+        // and so does one that needs the shifted form of an instance without
+        // one
+        bool use_dma = dma && ov_kernel != 2;
+        const Instance *in = nullptr;
+        if (use_dma) {
+            in = find_instance(ov_kernel == 0 ? 1 : ov_kernel, ov_bm, ov_bn);
+            if (!in) in = find_instance(1, ov_bm, ov_bn);
+            if (mode == 2 && !shift_capable(ov_bm, ov_bn, in->bk, in->ns, in->kg, in->epi))
+                use_dma = false;
+        }
         Plan p{ov_bm, ov_bn, 1, 1, use_dma};
         if (use_dma) {
-            const Instance *in = find_instance(ov_kernel == 0 ? 1 : ov_kernel, ov_bm, ov_bn);
-            if (!in) in = find_instance(1, ov_bm, ov_bn);
             p.ns = in->ns;
             p.kg = in->kg;
             p.epi = in->epi;
             p.bk = in->bk;
             p.occ = ov_occ;
+            p.shift = mode == 2;
         } else if (!tile_supported(p.bm, p.bn, false)) {
             p.bn = 128;   // 256x256 only pipelined
         }
@@ -458,9 +521,11 @@ static Plan plan_uncached(const Gemm &g) {
             split_of(kb_total, p.splits - 1, &p.splits, &p.kblk_per_split);
         return p;
     }
-    if (const Tuned *t = tuned_for(g, dma)) {
+    if (const Tuned *t = tuned_for(g, mode)) {
         Plan p{t->bm, t->bn, 1, 1, dma && t->code != 2};
         const Instance *in = p.dma ? find_instance(t->code, t->bm, t->bn) : nullptr;
+        if (in && mode == 2 && !shift_capable(t->bm, t->bn, in->bk, in->ns, in->kg, in->epi))
+            in = nullptr;
         if ((!p.dma && tile_supported(t->bm, t->bn, false)) || in) {
             if (in) {
                 p.ns = in->ns;
@@ -468,6 +533,7 @@ static Plan plan_uncached(const Gemm &g) {
                 p.epi = in->epi;
                 p.bk = in->bk;
                 p.occ = t->occ;
+                p.shift = mode == 2;
             }
             split_of(kb_total, t->splits, &p.splits, &p.kblk_per_split);
             if (fits_ws(g, p.splits)) return p;
@@ -479,6 +545,7 @@ static Plan plan_uncached(const Gemm &g) {
                            : (int)(sizeof(kGeneric) / sizeof(kGeneric[0]));
     for (int ti = 0; ti < ntiles; ++ti) {
         const TileClass &t = tiles_tab[ti];
+        if (mode == 2 && !shift_capable(t.bm, t.bn, t.bk, t.ns, t.kg, t.epi)) continue;
         int last_splits = 0;
         for (int s = 1; s <= 32; ++s) {
             int splits, per;
@@ -491,6 +558,7 @@ static Plan plan_uncached(const Gemm &g) {
             if (tm < best_t * 0.999) {
                 best_t = tm;
                 best = Plan{t.bm, t.bn, splits, per, dma, t.ns, t.kg, t.epi, t.occ_persist, t.bk};
+                best.shift = mode == 2;
             }
         }
     }

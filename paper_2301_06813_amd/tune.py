@@ -64,21 +64,37 @@ def product_cases(wl_ids):
 
 
 def _eligible(op, L, lin):
-    """Whether the pipelined kernel can read rank r's operand views: 16-byte
-    aligned shard offsets, and leading dimensions and contiguous extents (the
-    columns of a row-major share) that are multiples of 8 elements."""
+    """The library's pipelined-kernel mode for rank r's operand views (the
+    key the plan table is looked up by): 0 the generic kernel; 1 the
+    pipelined kernel (every operand 16-byte aligned, leading dimensions and
+    contiguous extents multiples of 8); 2 its shifted form (leading
+    dimensions multiples of 8, a shard that starts inside a 16-byte block
+    only along an output dimension, or along the reduction when both
+    operands are k-major with the same offset)."""
     from . import linear
 
-    def ok(layout, rows, cols):
+    def view(layout, rows, cols):
         s = linear.shard(layout, rows, cols)
-        return (s.row_off * cols + s.col_off) % 8 == 0 and cols % 8 == 0 and s.cols % 8 == 0
+        return (s.row_off * cols + s.col_off) % 8, s.cols
 
     M, K, N = lin.M, lin.K, lin.N
     if op == "fwd":
-        return int(ok(L["x"], M, K) and ok(L["w"], K, N))
-    if op == "bwd_data":
-        return int(ok(L["dy"], M, N) and ok(L["w"], K, N))
-    return int(ok(L["x"], M, K) and ok(L["dy"], M, N))
+        (oa, ca), (ob, cb) = view(L["x"], M, K), view(L["w"], K, N)
+        ok = K % 8 == 0 and N % 8 == 0 and oa == 0
+    elif op == "bwd_data":
+        (oa, ca), (ob, cb) = view(L["dy"], M, N), view(L["w"], K, N)
+        ok = N % 8 == 0 and oa == ob
+    else:
+        (oa, ca), (ob, cb) = view(L["x"], M, K), view(L["dy"], M, N)
+        ok = K % 8 == 0 and N % 8 == 0
+    if not ok:
+        return 0
+    return 1 if (oa == 0 and ob == 0 and ca % 8 == 0 and cb % 8 == 0) else 2
+
+
+# the instances with a shifted form (mode 2 products): tile, kernel code
+SHIFT_CODES = {((64, 64), 1), ((128, 128), 4), ((64, 64), 12), ((128, 64), 12), ((64, 128), 12),
+               ((128, 128), 12)}
 
 
 def valid_candidates(sbp, key, tiles_n_items, max_splits=None, nbatch=1):
@@ -87,10 +103,14 @@ def valid_candidates(sbp, key, tiles_n_items, max_splits=None, nbatch=1):
     orient, f32, m, n, k, dma = key
     kblocks = max(1, (k + 63) // 64)
     out = []
-    codes = CODES if dma else (2,)
+    # shifted-form products: the instances that have that form, and the
+    # generic kernel
+    codes = (CODES + (2,)) if dma == 2 else (CODES if dma else (2,))
     for (bm, bn) in TILES:
         tiles = ((m + bm - 1) // bm) * ((n + bn - 1) // bn)
         for code in codes:
+            if dma == 2 and code != 2 and ((bm, bn), code) not in SHIFT_CODES:
+                continue
             try:
                 sbp.sbp_set_plan_override(bm, bn, 1, code, 0)
             except sbp.SbpError:
@@ -218,6 +238,8 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream, single_best=None):
         timings = []
         kbd, kbw = max(1, (kd[4] + 63) // 64), max(1, (kw[4] + 63) // 64)
         for (bm, bn), code in GROUP_INSTANCES:
+            if 2 in (kd[5], kw[5]) and ((bm, bn), code) not in SHIFT_CODES:
+                continue   # grouped launches of shifted-form products
             for sd in (1, 2, 4, 8, 16):
                 if sd > 1 and kbd // sd < 2:
                     continue

@@ -410,17 +410,22 @@ def test_tuned_tables_name_built_instances(L):
     pairs = _table_rows("tuned_bwd_plans.inc")
     assert len(singles) > 50 and len(pairs) > 15
     try:
+        from paper_2301_06813_amd.tune import SHIFT_CODES
         for orient, f32, m, n, k, dma, bm, bn, code, splits, occ, *nb in singles:
             sbp.sbp_set_plan_override(bm, bn, 1, code)     # raises for an unknown pair
-            assert splits >= 1 and 0 <= occ <= 8
+            assert splits >= 1 and 0 <= occ <= 8 and dma in (0, 1, 2)
             sbp.sbp_set_plan_override(0, 0, 1)
-            if dma and not nb:
+            if dma == 2:   # shifted-form products: an instance that has that form
+                assert ((bm, bn), code) in SHIFT_CODES, (orient, m, n, k, bm, bn, code)
+            if dma == 1 and not nb:
                 out = F32 if f32 else BF
                 tm, tn, s, kn = sbp.sbp_plan(orient, m, n, k, BF, out)
                 assert (tm, tn, s, kn) == (bm, bn, splits, code), (orient, m, n, k)
         for md, nd, kd, fd, mw, nw, kw, fw, bm, bn, code, sd, sw in pairs:
             sbp.sbp_set_plan_override(bm, bn, sd, code)
             sbp.sbp_set_plan_override(0, 0, 1)
+            if kd % 8 or mw % 8 or nw % 8:
+                continue   # not plannable with tight leading dimensions
             g, tm, tn, psd, psw = sbp.sbp_plan_bwd(md, nd, kd, F32 if fd else BF,
                                                      mw, nw, kw, F32 if fw else BF)
             assert (g, tm, tn, psd, psw) == (1, bm, bn, sd, sw), (md, nd, kd)

@@ -245,6 +245,55 @@ def test_exact_misaligned_column_shards():
             _check_exact(op, "COL", 8, r, X, W, dY, Xh, Wh, dYh)
 
 
+# the instances with a shifted form: direct and staged epilogues, 64- and
+# 128-wide stages, one and two reduction groups
+SHIFT_INSTANCES = [((64, 64), 1), ((128, 128), 4), ((64, 64), 12), ((128, 64), 12),
+                   ((64, 128), 12), ((128, 128), 12)]
+
+
+@pytest.mark.parametrize("tile,kernel", SHIFT_INSTANCES,
+                         ids=["%dx%d-k%d" % (t[0], t[1], k) for t, k in SHIFT_INSTANCES])
+def test_exact_shifted_operand_views(tile, kernel):
+    """Shards that start inside a 16-byte block run on the pipelined kernel
+    in a shifted index space: the column shards of a 1000-wide W and dY over
+    8 ranks (125 r, as the VGG head's FC8) -- an n-major operand shifted
+    along the output columns (forward, backward-weight) and both k-major
+    operands shifted along a 125-long reduction (backward-data, with its
+    boundary chunks masked) -- and the K split of a 1000-wide X (an m-major
+    operand shifted along the output rows, backward-weight). Every rank,
+    splits 1 and 3, the backward pair as one grouped launch; the profile
+    shows the pipelined kernel ran (its shifted form on the ranks whose
+    shards need it); results bit-exact. An instance without a shifted form
+    falls back to the generic kernel on those ranks."""
+    M, K, N, p = 200, 1000, 1000, 8
+    X, W, dY = _int_inputs(M, K, N, 1700)
+    Xh, Wh, dYh = (inputs.host_bits(t) for t in (X, W, dY))
+    cases = [("COL", "fwd"), ("COL", "bwd_data"), ("COL", "bwd_weight"), ("KS", "bwd_weight"),
+             ("KS", "bwd_data")]
+    try:
+        for splits in (1, 3):
+            sbp.sbp_set_plan_override(tile[0], tile[1], splits, kernel)
+            for r in range(p):
+                for sig, op in cases:
+                    say("shifted", tile, kernel, splits, r, sig, op)
+                    names = _kernel_names(
+                        lambda: _check_exact(op, sig, p, r, X, W, dY, Xh, Wh, dYh))
+                    assert any(n.startswith("gemm_bf16_dma_kernel") for n in names), names
+                    # 125-wide shards: every product except the K split's
+                    # backward-data (aligned operands, a 1000-long reduction)
+                    # needs the shifted form, whose kernel name has a twelfth
+                    # template argument
+                    shifted = any(n.startswith("gemm_bf16_dma_kernel") and n.count(",") == 11
+                                  for n in names)
+                    assert shifted == (not (sig == "KS" and op == "bwd_data")), names
+                sbp.sbp_set_bwd_override(2, splits)
+                names = _kernel_names(lambda: _check_exact_bwd("COL", p, r, X, W, dY, Xh, Wh, dYh))
+                assert any(n.startswith("gemm_bf16_dma_bwd_kernel") for n in names), names
+                sbp.sbp_set_bwd_override(0, 1)
+    finally:
+        sbp.sbp_set_plan_override(0, 0, 1)
+
+
 def test_exact_local_scope_padded_ld():
     # LOCAL views with ld > cols and an odd element offset; the result must
     # equal the GLOBAL-scope call on the same share.
