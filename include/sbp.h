@@ -516,10 +516,12 @@ int sbp_profile_begin(int capacity);
 int sbp_profile_end(float *us, char *names, int name_len);
 
 /* Thread-local override of the bf16 plan for subsequent calls on this
- * thread (tests and tuning). tile_m x tile_n is one of 256x256, 256x128,
- * 128x256, 128x128, 128x64, 64x128, 64x64; splits >= 1. kernel selects the
- * instance:
- *   0, 1  the tile's default pipelined direct-to-LDS instance;
+ * thread (tests and tuning). tile_m x tile_n is one of 256x256, 256x192,
+ * 256x128, 128x256, 128x128, 128x64, 64x128, 64x64; splits >= 1. kernel
+ * selects the instance:
+ *   0, 1  the tile's default pipelined direct-to-LDS instance (256x192:
+ *         eight waves as 4 x 2, two stages; as many 256 x 192 tiles as
+ *         compute units for a 4096 x 3072 output);
  *   2     the generic kernel;
  *   4     pipelined with two stages (128x128, 128x64, 64x128, 64x64: two or
  *         more workgroups per compute unit);
@@ -544,8 +546,8 @@ int sbp_profile_end(float *us, char *names, int name_len);
  * per compute unit, each taking every G-th work item (0 = one workgroup per
  * item; the grouped backward launch always runs one per item). A call whose
  * operands the pipelined kernel cannot read runs the generic kernel, where
- * 256x256 becomes 256x128; splits are clamped to the reduction blocks and to
- * the call's workspace. tile_m = 0 clears the override.
+ * 256x256 and 256x192 become 256x128; splits are clamped to the reduction
+ * blocks and to the call's workspace. tile_m = 0 clears the override.
  * Errors: SBP_ERR_SHAPE for a (tile, kernel) pair not listed above,
  * splits < 1, or wgs_per_cu outside [0, 8]. */
 int sbp_set_plan_override(int32_t tile_m, int32_t tile_n, int32_t splits,

@@ -145,7 +145,12 @@ struct KTileDma {
 
 // ---------------------------------------------------------------- m/n-major
 // LDS: BK rows (reduction index) x BMN values; chunk c of row r at
-// r*RB + 16*(c ^ (4*(r%4) % CPR)) with RB = 2*BMN bytes, CPR chunks per row.
+// r*RB + 16*(c ^ f(r)) with RB = 2*BMN bytes, CPR chunks per row. A transpose
+// read of one half-wave touches 4 consecutive rows and 4 consecutive chunks
+// (64 bytes of each row); f spreads those 4 rows over the 64 banks: rows of
+// 256 or 512 bytes all start on bank 0, so f(r) = 4 (r % 4); rows of 128 or
+// 384 bytes start on banks 0 and 32 alternately, so f(r) = 4 ((r / 2) % 2)
+// (which keeps the 24 chunks of a 384-byte row inside the row).
 template <int BMN, int NW, int BK_>
 struct MNTileDma {
     static constexpr int RB = BMN * 2;            // bytes per row
@@ -154,8 +159,9 @@ struct MNTileDma {
     static constexpr int PER_WAVE = SEGS / NW;
     static_assert(SEGS % NW == 0, "tile too small for the wave count");
 
+    static_assert(CPR == 8 || CPR == 16 || CPR == 24 || CPR == 32, "unsupported tile width");
     __device__ __forceinline__ static int swz(int row) {
-        return CPR >= 16 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
+        return (CPR == 16 || CPR == 32) ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
     }
 
     // PART: as for KTileDma (a chunk past mn_lim holds only outputs that are

@@ -30,6 +30,7 @@ namespace sbpi {
 // the grouped backward launchers.
 #define SBP_DMA_INSTANCES(X)                                    \
     X(256, 256, 64, 2, 2, 4, 1, sbpk::EPI_DIRECT)               \
+    X(256, 192, 64, 2, 4, 2, 1, sbpk::EPI_DIRECT)               \
     X(256, 256, 64, 2, 2, 4, 1, sbpk::EPI_ROWQ)                     \
     X(256, 128, 64, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \
     X(128, 256, 64, SBP_NS_256x128, 2, 2, 1, sbpk::EPI_DIRECT)      \

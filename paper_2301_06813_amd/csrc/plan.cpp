@@ -41,7 +41,8 @@ const TileClass kGeneric[] = {
 // The 128-wide stages with two reduction groups (one workgroup of eight
 // waves per CU) stream their operands about 20 % faster per CU.
 const TileClass kDma[] = {
-    {256, 256, 1, 1.0, 0}, {256, 128, 1, 1.0, 0}, {128, 256, 1, 1.0, 0}, {128, 128, 1, 1.0, 0},
+    {256, 256, 1, 1.0, 0}, {256, 192, 1, 1.0, 0},
+    {256, 128, 1, 1.0, 0}, {128, 256, 1, 1.0, 0}, {128, 128, 1, 1.0, 0},
     {128, 128, 2, 0.8, 2}, {128, 64, 1, 1.0, 0},  {64, 128, 1, 1.0, 0},  {64, 64, 2, 1.0, 0},
     {128, 128, 1, 1.2, 2, 2, 1, 0, 128}, {128, 64, 1, 1.2, 3, 2, 1, 0, 128},
     {64, 128, 1, 1.2, 3, 2, 1, 0, 128},  {64, 64, 1, 1.2, 4, 2, 1, 0, 128},
@@ -71,7 +72,8 @@ struct Instance {
 };
 constexpr int E_DIRECT = 0, E_STAGED = 1, E_ROWQ = 2;   // = sbpk::EPI_*
 const Instance kInstances[] = {
-    {1, 256, 256, 0, 1, E_DIRECT}, {1, 256, 128, 0, 1, E_DIRECT}, {1, 128, 256, 0, 1, E_DIRECT},
+    {1, 256, 256, 0, 1, E_DIRECT}, {1, 256, 192, 0, 1, E_DIRECT},
+    {1, 256, 128, 0, 1, E_DIRECT}, {1, 128, 256, 0, 1, E_DIRECT},
     {1, 128, 128, 0, 1, E_DIRECT}, {1, 128, 64, 0, 1, E_DIRECT},  {1, 64, 128, 0, 1, E_DIRECT},
     {1, 64, 64, 0, 1, E_DIRECT},   {4, 128, 128, 2, 1, E_DIRECT}, {5, 256, 128, 0, 2, E_STAGED},
     {5, 128, 256, 0, 2, E_STAGED}, {5, 128, 128, 0, 2, E_STAGED}, {6, 256, 256, 0, 1, E_ROWQ},

@@ -30,7 +30,7 @@ import time
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 
-TILES = [(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
+TILES = [(256, 256), (256, 192), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
 CODES = (1, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13)   # pipelined instances; 2 (generic) for the rest
 SPLITS = (1, 2, 3, 4, 6, 8, 12, 16)
 ORIENT = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2}
@@ -127,6 +127,9 @@ def valid_candidates(sbp, key, tiles_n_items, max_splits=None, nbatch=1):
                 items = tiles * eff * nbatch
                 if (items > 8192 and nbatch == 1) or (eff > 1 and items > 4096):
                     continue
+                # the library clamps splits whose partials exceed the workspace
+                if eff > 1 and eff * m * n * 4 > sbp.SBP_WORKSPACE_BYTES:
+                    continue
                 occs = (0,) if (code == 2 or items <= 256) else (0, 1, 2)
                 for occ in occs:
                     out.append((bm, bn, eff, code, occ))
@@ -163,7 +166,7 @@ def time_plan(torch, sbp, fn, plan, reps, stream, keep=False):
             sbp.sbp_set_plan_override(0, 0, 1)
 
 
-GROUP_INSTANCES = [((128, 128), 1), ((128, 128), 4), ((128, 128), 5), ((256, 128), 5),
+GROUP_INSTANCES = [((128, 128), 1), ((256, 192), 1), ((128, 128), 4), ((128, 128), 5), ((256, 128), 5),
                    ((128, 256), 5), ((64, 64), 1), ((128, 64), 1), ((64, 128), 1),
                    ((256, 256), 1), ((128, 128), 7), ((128, 128), 10), ((64, 64), 5),
                    ((64, 64), 7), ((128, 64), 5), ((64, 128), 5), ((128, 128), 12),

@@ -11,7 +11,7 @@ from paper_2301_06813_amd import inputs, linear, sbp
 SIG_ID = {"DP": oracle.DP, "COL": oracle.COL, "KS": oracle.KS, "PB": oracle.PB,
           "BP": oracle.BP, "BB": oracle.BB}
 OP_ID = {"fwd": oracle.FWD, "bwd_data": oracle.BWD_DATA, "bwd_weight": oracle.BWD_WEIGHT}
-TILES = [(256, 256), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
+TILES = [(256, 256), (256, 192), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
 KERNELS = (1, 2)   # pipelined direct-to-LDS, generic
 # (tile, kernel) pairs beyond TILES x KERNELS: the two-stage pipelined 128x128,
 # the eight-wave instances with two reduction groups (staged and row-quad
