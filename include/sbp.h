@@ -118,8 +118,8 @@ typedef struct {
 /* Caller-owned device memory for split reductions. A product with a long
  * reduction and few output tiles runs faster with its reduction split over
  * several workgroups; each split writes an fp32 partial of the m x n output
- * (splits x m x n x 4 bytes in all) that a second kernel adds up in split
- * order. The linear calls take a workspace; data = NULL (or bytes = 0, or a
+ * (rows padded to a multiple of 4 floats: splits x m x 4 ceil(n / 4) x 4
+ * bytes in all) that a second kernel adds up in split order. The linear calls take a workspace; data = NULL (or bytes = 0, or a
  * NULL sbp_workspace_t pointer) means none, and then no reduction is split.
  * With bytes >= SBP_WORKSPACE_BYTES every call gets the library's preferred
  * plan; a smaller workspace limits the splits to what fits (results are the

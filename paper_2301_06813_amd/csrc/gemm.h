@@ -68,7 +68,14 @@ int dma_mode(const Gemm &g);
 // Offset in elements of a bf16 pointer within its 16-byte block.
 int block_offset(const void *p);
 
-// Workspace of the split reduction: `splits` slices of m x n fp32 partials.
+// Row stride (floats) of a split reduction's partial slices for an m x n
+// output: n rounded up to a multiple of 4, so that every 4-column group of a
+// slice is one aligned 16-byte load in the reduction (the padding columns
+// are never written or stored).
+__host__ __device__ inline int64_t partial_ld(int64_t n) { return (n + 3) & ~int64_t(3); }
+
+// Workspace of the split reduction: `splits` slices of m x partial_ld(n)
+// fp32 partials.
 // Plans never use more than WS_FLOATS_PREFERRED floats, however large the
 // caller's workspace, so that a workspace of that size always gets the
 // library's preferred plan (the value of SBP_WORKSPACE_BYTES / 4).

@@ -52,8 +52,7 @@ hipError_t launch_bf16_bwd_group(const Gemm &gd, const Plan &pd, const Gemm &gw,
     if (pd.bm != pw.bm || pd.bn != pw.bn || pd.bk != pw.bk || pd.ns != pw.ns || pd.kg != pw.kg ||
         pd.epi != pw.epi || pd.shift != pw.shift || !pd.dma || !pw.dma)
         return hipErrorInvalidValue;
-    float *ws_w = ws;
-    if (pd.splits > 1) ws_w = ws + (size_t)pd.splits * (size_t)gd.m * (size_t)gd.n;
+    float *const ws_w = ws + plan_ws_floats(gd, pd);
     const sbpk::GemmArgsShift d = make_args(gd, pd, ws);
     const sbpk::GemmArgsShift w = make_args(gw, pw, ws_w);
     const int grid = d.tiles_m * d.tiles_n * d.splits + w.tiles_m * w.tiles_n * w.splits;

@@ -460,11 +460,12 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
     }
 
     // Split reduction: this workgroup's fp32 partial goes to slice `split`
-    // of the workspace, laid out like the output (m x n, ld n); a separate
-    // kernel adds the slices in split order.
+    // of the workspace (m x n, row stride partial_ld(n)); a separate kernel
+    // adds the slices in split order.
     const bool partial = g.splits > 1;
-    float *const ws_out = g.ws + (size_t)split * (size_t)g.m * (size_t)g.n;
-    const bool ws_vec = g.n % 4 == 0 && shift_n(g) % 4 == 0;
+    const int ldw = (int)sbpi::partial_ld(g.n);
+    float *const ws_out = g.ws + (size_t)split * (size_t)g.m * (size_t)ldw;
+    const bool ws_vec = shift_n(g) % 4 == 0;
     // the tile's first output row and column (SHIFT: kernel index minus the
     // shift; may be negative, and bounds are then checked as unsigned)
     const int om0 = m0 - shift_m(g), on0 = n0 - shift_n(g);
@@ -565,7 +566,7 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
             }
         };
         if (partial)
-            store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n, ws_vec);
+            store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)ldw, ws_vec);
         else if (OUT_F32 && g.accumulate)
             store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
                       Cb, g.ldc, (bool)g.vec_c4);
@@ -609,7 +610,7 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
         }
         __syncthreads();
         if (partial)
-            store_staged<BM, BN, LD, 64 * NW, true, false, SHIFT>(tile, ws_out, g.n, g.m, g.n,
+            store_staged<BM, BN, LD, 64 * NW, true, false, SHIFT>(tile, ws_out, ldw, g.m, g.n,
                                                                   om0, on0, ws_vec, tid);
         else if (OUT_F32 && g.accumulate)
             store_staged<BM, BN, LD, 64 * NW, OUT_F32, OUT_F32, SHIFT>(
@@ -651,7 +652,7 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
         }
     };
     if (partial)
-        store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)g.n);
+        store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)ldw);
     else if (OUT_F32 && g.accumulate)
         store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
                   Cb, g.ldc);

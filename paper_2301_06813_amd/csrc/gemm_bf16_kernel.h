@@ -45,6 +45,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gemm.h"
+
 namespace sbpk {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -66,7 +68,8 @@ struct GemmArgs {
     int32_t tiles_m, tiles_n;
     int32_t splits;             // reduction splits (>= 1)
     int32_t kchunk;             // reduction elements per split (a multiple of 64)
-    float *ws;                  // split partials: splits slices of m x n floats
+    float *ws;                  // split partials: splits slices of m x n floats,
+                                // row stride partial_ld(n)
     int32_t vec_a, vec_b;       // operand base and ld allow aligned 16-byte loads
     int32_t vec_c4, vec_c8;     // C's base and ldc allow aligned 16-byte stores of
                                 // 4 fp32 / 8 bf16 elements
@@ -396,9 +399,10 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
     // ---- split reduction: partials to the workspace; split_reduce_kernel adds them
     if (g.splits > 1) {
         // Split reduction: this workgroup's fp32 partial goes to slice
-        // `split` of the workspace, laid out like the output (m x n, ld n);
+        // `split` of the workspace (m x n, row stride partial_ld(n));
         // a separate kernel adds the slices in split order.
-        float *P = g.ws + (size_t)split * (size_t)g.m * (size_t)g.n;
+        const int64_t ldw = sbpi::partial_ld(g.n);
+        float *P = g.ws + (size_t)split * (size_t)g.m * (size_t)ldw;
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -411,7 +415,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
                         const int row = rbase + 8 * (r >> 2) + (r & 3);
                         // ordinary stores: this kernel's partials are small and read
                         // back at once (non-temporal ones measured 15 % slower here)
-                        if (row < g.m) P[(int64_t)row * g.n + col] = acc[i][j][r];
+                        if (row < g.m) P[(int64_t)row * ldw + col] = acc[i][j][r];
                     }
                 }
             }

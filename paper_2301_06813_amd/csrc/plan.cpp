@@ -173,7 +173,7 @@ double ws_budget(const Gemm &g) {
 bool fits_ws(const Gemm &g, int splits) {
     if (splits == 1) return true;
     if (g.nbatch() > 1) return false;   // batched launches never split
-    return (double)splits * (double)g.m * (double)g.n <= ws_budget(g);
+    return (double)splits * (double)g.m * (double)partial_ld(g.n) <= ws_budget(g);
 }
 
 // Work items of one product under (tile, splits): count, time per item, and
@@ -379,13 +379,11 @@ static bool grouped_plan(const Gemm &gd, const Gemm &gw, const Instance *in, int
         p.shift = sh;
         split_of(kblocks(g.k), w ? sw : sd, &p.splits, &p.kblk_per_split);
     }
-    return (pd->splits > 1 ? (double)pd->splits * gd.m * gd.n : 0.0) +
-               (pw->splits > 1 ? (double)pw->splits * gw.m * gw.n : 0.0) <=
-           ws_budget(gd);
+    return (double)plan_ws_floats(gd, *pd) + (double)plan_ws_floats(gw, *pw) <= ws_budget(gd);
 }
 
 size_t plan_ws_floats(const Gemm &g, const Plan &p) {
-    return p.splits > 1 ? (size_t)p.splits * (size_t)g.m * (size_t)g.n : 0;
+    return p.splits > 1 ? (size_t)p.splits * (size_t)g.m * (size_t)partial_ld(g.n) : 0;
 }
 
 bool plan_bf16_bwd(const Gemm &gd, const Gemm &gw, Plan *pd, Plan *pw) {
