@@ -32,7 +32,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 TILES = [(256, 256), (256, 192), (256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)]
 CODES = (1, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13)   # pipelined instances; 2 (generic) for the rest
-SPLITS = (1, 2, 3, 4, 6, 8, 12, 16)
+SPLITS = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32)
 ORIENT = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2}
 
 
@@ -128,7 +128,7 @@ def valid_candidates(sbp, key, tiles_n_items, max_splits=None, nbatch=1):
                 if (items > 8192 and nbatch == 1) or (eff > 1 and items > 4096):
                     continue
                 # the library clamps splits whose partials exceed the workspace
-                if eff > 1 and eff * m * n * 4 > sbp.SBP_WORKSPACE_BYTES:
+                if eff > 1 and eff * m * (-(-n // 4) * 4) * 4 > sbp.SBP_WORKSPACE_BYTES:
                     continue
                 occs = (0,) if (code == 2 or items <= 256) else (0, 1, 2)
                 for occ in occs:
