@@ -171,7 +171,11 @@ GROUP_INSTANCES = [((128, 128), 1), ((256, 192), 1), ((128, 128), 4), ((128, 128
                    ((256, 256), 1), ((128, 128), 7), ((128, 128), 10), ((64, 64), 5),
                    ((64, 64), 7), ((128, 64), 5), ((64, 128), 5), ((128, 128), 12),
                    ((128, 64), 12), ((64, 128), 12), ((64, 64), 12), ((128, 128), 13),
-                   ((64, 64), 13)]
+                   ((64, 64), 13), ((128, 128), 6), ((256, 256), 6), ((256, 128), 7),
+                   ((128, 256), 7), ((128, 64), 7), ((64, 128), 7), ((128, 64), 13),
+                   ((64, 128), 13), ((128, 64), 4), ((64, 128), 4), ((64, 64), 4),
+                   ((256, 256), 8), ((128, 128), 9), ((256, 128), 9), ((128, 256), 9),
+                   ((128, 64), 11), ((64, 128), 11), ((64, 64), 11)]
 
 
 def bwd_pairs(wl_ids):
@@ -243,10 +247,10 @@ def tune_bwd(args, torch, sbp, linear, workloads, stream, single_best=None):
         for (bm, bn), code in GROUP_INSTANCES:
             if 2 in (kd[5], kw[5]) and ((bm, bn), code) not in SHIFT_CODES:
                 continue   # grouped launches of shifted-form products
-            for sd in (1, 2, 4, 8, 16):
+            for sd in (1, 2, 3, 4, 8, 16):
                 if sd > 1 and kbd // sd < 2:
                     continue
-                for sw in (1, 2, 4, 8, 16):
+                for sw in (1, 2, 3, 4, 8, 16):
                     if sw > 1 and kbw // sw < 2:
                         continue
                     try:
