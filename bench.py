@@ -73,94 +73,6 @@ def counted_traffic(kernel: str):
     return None
 
 
-class Step:
-    """Rank r's calls of one workload, with all buffers preallocated: every
-    forward product in layer order, then both backward products of each
-    linear (one sbp_linear_bwd call) in reverse order."""
-
-    def __init__(self, wl, r, device="cuda"):
-        import ctypes
-        import torch
-        from paper_2301_06813_amd import linear, sbp, workloads
-        self.sbp = sbp
-        self.keep = []
-        fwd, bwd = [], []
-        for lin in wl.linears:
-            X, W, dY = workloads.make_tensors(lin, wl.dtype, device)
-            L = linear.layouts(lin.sig, wl.p, r)
-            self.keep += [X, W, dY]
-            vX, vW, vdY = sbp.view(X), sbp.view(W), sbp.view(dY)
-            outs = {}
-            for op in OPS:
-                out = linear.alloc_out(op, lin.sig, wl.p, r, lin.M, lin.K, lin.N, wl.dtype, device)
-                self.keep.append(out)
-                outs[op] = out
-            prods = {}
-            for op, out in outs.items():
-                m, n = out.shape
-                k = {"fwd": sbp.sbp_shard_index(L["x"], lin.M, lin.K).cols,
-                     "bwd_data": sbp.sbp_shard_index(L["dy"], lin.M, lin.N).cols,
-                     "bwd_weight": sbp.sbp_shard_index(L["x"], lin.M, lin.K).rows}[op]
-                ob = 4 if out.dtype == torch.float32 else 2
-                prods[op] = dict(m=m, n=n, k=k, flops=2.0 * m * n * k,
-                                 bytes=2.0 * (m * k + k * n) + ob * m * n)
-            vo = {op: sbp.view(out, sbp.SBP_LOCAL) for op, out in outs.items()}
-            f = ("sbp_linear_fwd", (vX, L["x"], vW, L["w"], vo["fwd"]), 1)
-            fwd.append((f, dict(linear=lin.name, sig=lin.sig, ops=("fwd",), **prods["fwd"])))
-            bcall = ("sbp_linear_bwd", (vdY, L["dy"], vX, L["x"], vW, L["w"], vo["bwd_data"]),
-                     (vo["bwd_weight"],))
-            pb = dict(flops=prods["bwd_data"]["flops"] + prods["bwd_weight"]["flops"],
-                      bytes=prods["bwd_data"]["bytes"] + prods["bwd_weight"]["bytes"])
-            bwd.append((bcall, dict(linear=lin.name, sig=lin.sig, ops=("bwd_data", "bwd_weight"),
-                                    data=prods["bwd_data"], weight=prods["bwd_weight"], **pb)))
-        self.calls, self.meta = [], []
-        for call, meta in fwd + bwd[::-1]:
-            self.calls.append(call)
-            self.meta.append(meta)
-        self.flops = sum(m["flops"] for m in self.meta)
-        L_ = sbp.lib()
-        self._lo = sbp.sbp_layout_t()
-        self._lo2 = sbp.sbp_layout_t()
-        lo, lo2 = ctypes.byref(self._lo), ctypes.byref(self._lo2)
-        # the split reductions' workspace (caller-owned; every call of the
-        # step runs in order on one stream, so they share it)
-        self.ws_mem = torch.empty(sbp.SBP_WORKSPACE_BYTES, dtype=torch.uint8, device=device)
-        self._ws = sbp.workspace(self.ws_mem)
-        ws = ctypes.byref(self._ws)
-        self._bound = []
-        for name, args, extra in self.calls:
-            fn = getattr(L_, name)
-            refs = tuple(ctypes.byref(a) for a in args)
-            if name == "sbp_linear_bwd":
-                refs = refs + (lo, ctypes.byref(extra[0]), lo2, ws)
-            else:
-                refs = refs + (lo, ws)
-            self._bound.append((fn, refs))
-
-    def launch_all(self, stream):
-        import ctypes
-        s = ctypes.c_void_p(stream)
-        for fn, refs in self._bound:
-            rc = fn(*refs, s)
-            if rc != 0:
-                raise self.sbp.SbpError(rc, self.sbp.sbp_last_hip_error())
-
-    def profile(self, stream):
-        """Per call: [(kernel name, us)] of every kernel it launched, each
-        timed by events recorded with its own dispatch."""
-        import ctypes
-        s = ctypes.c_void_p(stream)
-        out = []
-        for fn, refs in self._bound:
-            self.sbp.sbp_profile_begin(16)
-            rc = fn(*refs, s)
-            ks = self.sbp.sbp_profile_end(16)
-            if rc != 0:
-                raise self.sbp.SbpError(rc, self.sbp.sbp_last_hip_error())
-            out.append(ks)
-        return out
-
-
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -478,6 +390,7 @@ def main():
 
     import torch
     from paper_2301_06813_amd import sbp, workloads
+    from paper_2301_06813_amd.step import Step
     torch.cuda.set_device(0)
     if args.copy_calibration:
         src = torch.ones(1 << 29, dtype=torch.bfloat16, device="cuda")
@@ -578,7 +491,8 @@ def main():
                 b[2] += sh["bytes"]
                 g += 1
             kd[name] = kd.get(name, 0.0) + us
-        launches.append(dict(m, kernels=kd, us=sum(us for _, us in ks)))
+        launches.append(dict({k_: v_ for k_, v_ in m.items() if k_ not in ("lin", "layouts")},
+                             kernels=kd, us=sum(us for _, us in ks)))
     if args.dump:
         with open(args.dump, "w") as f:
             json.dump(launches, f)

@@ -4,12 +4,21 @@ library's tuned plan table (csrc/tuned_plans.inc).
 
     python -m paper_2301_06813_amd.tune [--out PATH] [--workloads 2,3,4,5]
     python -m paper_2301_06813_amd.tune --bwd [--out PATH]
+    python -m paper_2301_06813_amd.tune --step [--out PATH]
 
 The second form tunes the backward pair of each linear (sbp_linear_bwd):
 one grouped launch of both products on a shared instance, against the two
 separate launches of their tuned plans, and writes csrc/tuned_bwd_plans.inc
 with the pairs whose grouped launch was faster (run it on a library built
 with the single-product table).
+
+The third form chooses plans inside the 24-layer step (workload 5): for each
+distinct call, largest share of the step first, the whole step is captured
+and replayed with that call's fastest isolated candidates and with its
+current plan, and a candidate is kept when the step is faster (coordinate
+descent). In the step a product runs with warm caches, throttled clocks and
+its neighbours' traffic, so the isolated winner is not always the step's.
+It writes the changed plans as JSON lines for merging into the tables.
 
 A plan is (output tile, kernel instance, reduction splits, persistent
 workgroups per compute unit); candidates are set with sbp_set_plan_override
@@ -24,6 +33,7 @@ writing a new table.
 from __future__ import annotations
 
 import argparse
+import json
 import os
 import sys
 import time
@@ -365,6 +375,192 @@ def pick(timings, retime, top=5, rounds=3):
     return min(med)
 
 
+# ------------------------------------------------------------ in-step tuning
+def _call_key(torch, linear, meta, dtype):
+    """Plan-table key of a step call: ("fwd", product key) or ("bwd", data key,
+    weight key), product keys as in product_cases."""
+    lin, L = meta["lin"], meta["layouts"]
+
+    def pkey(op):
+        rows, cols = linear.out_shape(op, L, lin.M, lin.K, lin.N)
+        k = {"fwd": linear.shard(L["x"], lin.M, lin.K).cols,
+             "bwd_data": linear.shard(L["dy"], lin.M, lin.N).cols,
+             "bwd_weight": linear.shard(L["x"], lin.M, lin.K).rows}[op]
+        f32 = linear.out_dtype(op, L, dtype) == torch.float32
+        return (ORIENT[op], int(f32), rows, cols, k, _eligible(op, L, lin))
+    if meta["ops"] == ("fwd",):
+        return ("fwd", pkey("fwd"))
+    return ("bwd", pkey("bwd_data"), pkey("bwd_weight"))
+
+
+def _isolated_top(args, torch, sbp, linear, workloads, stream, key, wl, lin, r, top):
+    """The `top` fastest candidate plans of one step call, timed in isolation
+    (graph replays over rotating input sets, as the table tuner does)."""
+    per_set = 2 * (2 * lin.M * lin.K + lin.K * lin.N + 2 * lin.M * lin.N)
+    nsets = max(2, min(6, -(-600 * 2 ** 20 // per_set)))
+    Lr = linear.layouts_for(lin, wl, r)
+    sets = []
+    for _ in range(nsets):
+        X, W, dY = workloads.make_tensors(lin, wl.dtype, "cuda")
+        outs = {op: linear.alloc_out_L(op, Lr, lin.M, lin.K, lin.N, wl.dtype, "cuda")
+                for op in ("fwd", "bwd_data", "bwd_weight")}
+        sets.append((X, W, dY, outs))
+    it = [0]
+    timings = []
+    if key[0] == "fwd":
+        def fn():
+            X, W, dY, o = sets[it[0] % nsets]
+            it[0] += 1
+            linear.run_L("fwd", Lr, X, W, dY, o["fwd"], stream.cuda_stream)
+        for plan in valid_candidates(sbp, key[1], None):
+            try:
+                timings.append((time_plan(torch, sbp, fn, plan, args.reps, stream), ("fwd",) + plan))
+            except sbp.SbpError:
+                pass
+    else:
+        def fn():
+            X, W, dY, o = sets[it[0] % nsets]
+            it[0] += 1
+            linear.run_bwd_L(Lr, X, W, dY, o["bwd_data"], o["bwd_weight"], stream.cuda_stream)
+        kd, kw = key[1], key[2]
+        kbd, kbw = max(1, (kd[4] + 63) // 64), max(1, (kw[4] + 63) // 64)
+        for (bm, bn), code in GROUP_INSTANCES:
+            if 2 in (kd[5], kw[5]) and ((bm, bn), code) not in SHIFT_CODES:
+                continue
+            for sd in (1, 2, 3, 4, 8, 16):
+                if sd > 1 and kbd // sd < 2:
+                    continue
+                for sw in (1, 2, 3, 4, 8, 16):
+                    if sw > 1 and kbw // sw < 2:
+                        continue
+                    sbp.sbp_set_plan_override(bm, bn, sd, code, 0)
+                    sbp.sbp_set_bwd_override(2, sw)
+                    try:
+                        timings.append((time_plan(torch, sbp, fn, None, args.reps, stream,
+                                                  keep=True), ("grp", bm, bn, code, sd, sw)))
+                    except sbp.SbpError:
+                        pass
+                    finally:
+                        sbp.sbp_set_plan_override(0, 0, 1)
+        sbp.sbp_set_bwd_override(1, 1)
+        try:
+            timings.append((time_plan(torch, sbp, fn, None, args.reps, stream, keep=True),
+                            ("sep",)))
+        finally:
+            sbp.sbp_set_plan_override(0, 0, 1)
+    del sets
+    torch.cuda.empty_cache()
+    return [p for _, p in sorted(timings)[:top]]
+
+
+def _apply(sbp, cand, on):
+    """Set (on) or clear the overrides that make one call run candidate cand."""
+    if not on:
+        sbp.sbp_set_plan_override(0, 0, 1)
+        return
+    if cand[0] == "fwd":
+        _, bm, bn, splits, code, occ = cand
+        sbp.sbp_set_plan_override(bm, bn, splits, code, occ)
+    elif cand[0] == "grp":
+        _, bm, bn, code, sd, sw = cand
+        sbp.sbp_set_plan_override(bm, bn, sd, code, 0)
+        sbp.sbp_set_bwd_override(2, sw)
+    else:
+        sbp.sbp_set_bwd_override(1, 1)
+
+
+def tune_step(args, torch, sbp, linear, workloads, stream):
+    """Plans of the 24-layer step's calls chosen inside the step: for each
+    distinct call (largest share of the step first) the step graph is
+    captured with that call's candidate plans -- the fastest few in isolation
+    and the library's current plan -- and replayed; a candidate replaces the
+    current plan when the whole step is faster by more than the noise, with
+    earlier choices kept (coordinate descent). Writes the changed table rows
+    to args.out (one line per key: fwd or bwd, key, plan, step ms)."""
+    from .step import Step
+    wl = workloads.transformer_step() if args.step_workload == 5 else \
+        workloads.transformer_step_searched()
+    step = Step(wl, 0)
+    keys = [_call_key(torch, linear, m, wl.dtype) for m in step.meta]
+    calls_of = {}
+    for i, k in enumerate(keys):
+        calls_of.setdefault(k, []).append(i)
+    chosen = {}
+
+    def hook(i, before):
+        c = chosen.get(keys[i]) if trial[0] is None or keys[i] != trial[0][0] else trial[0][1]
+        if c is not None:
+            _apply(sbp, c, before)
+
+    trial = [None]
+
+    def measure(reps=args.step_reps):
+        sid = stream.cuda_stream
+        with torch.cuda.stream(stream):
+            step.launch_all(sid, hook)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                step.launch_all(torch.cuda.current_stream().cuda_stream, hook)
+        torch.cuda.synchronize()
+        g.replay()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        del g
+        return e0.elapsed_time(e1) / reps
+
+    # per-call step time of the current plans orders the keys
+    prof = [0.0] * len(keys)
+    with torch.cuda.stream(stream):
+        step.launch_all(stream.cuda_stream)
+        for _ in range(2):
+            for i, ks in enumerate(step.profile(stream.cuda_stream)):
+                prof[i] += sum(us for _, us in ks)
+    share = {k: sum(prof[i] for i in idx) for k, idx in calls_of.items()}
+    order = sorted(share, key=lambda k: -share[k])
+    base = min(measure() for _ in range(3))
+    log("step %.4f ms with the current plans; %d distinct calls" % (base, len(order)))
+    rows = []
+    for k in order:
+        i0 = calls_of[k][0]
+        m = step.meta[i0]
+        cands = _isolated_top(args, torch, sbp, linear, workloads, stream, k, wl, m["lin"], 0,
+                              args.step_top)
+        res = {}
+        for rnd in range(2):
+            trial[0] = None
+            res.setdefault(None, []).append(measure())
+            for c in cands:
+                trial[0] = (k, c)
+                try:
+                    res.setdefault(c, []).append(measure())
+                except sbp.SbpError as e:
+                    log("  %s failed: %s" % (c, e))
+                    res[c] = [1e9]
+                finally:
+                    trial[0] = None
+        best = min(res, key=lambda c: min(res[c]))
+        cur = min(res[None])
+        log("%s x%d (%.0f us/step): current %.4f ms, best %s %.4f ms" % (
+            k, len(calls_of[k]), share[k] / 2, cur, best, min(res[best])))
+        if best is not None and min(res[best]) < cur * (1 - args.step_gain):
+            chosen[k] = best
+            rows.append((k, best, min(res[best]), cur))
+    trial[0] = None
+    final = min(measure() for _ in range(3))
+    log("step %.4f -> %.4f ms" % (base, final))
+    with open(args.out, "w") as f:
+        for k, c, t, t0 in rows:
+            f.write(json.dumps({"key": k, "plan": c, "step_ms": t, "was_ms": t0}) + "\n")
+    log("wrote %s" % args.out)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--out", default=None)
@@ -374,6 +570,13 @@ def main():
     ap.add_argument("--all", action="store_true",
                     help="tune single products, then backward pairs against their sums")
     ap.add_argument("--out-bwd", default=os.path.join(HERE, "csrc", "tuned_bwd_plans.inc"))
+    ap.add_argument("--step", action="store_true",
+                    help="choose the 24-layer step's plans inside the step (writes JSON lines "
+                         "of changed plans to --out)")
+    ap.add_argument("--step-workload", type=int, default=5, choices=(5, 8))
+    ap.add_argument("--step-top", type=int, default=5)
+    ap.add_argument("--step-reps", type=int, default=30)
+    ap.add_argument("--step-gain", type=float, default=0.002)
     args = ap.parse_args()
     if args.out is None:
         args.out = args.out_bwd if args.bwd else os.path.join(HERE, "csrc", "tuned_plans.inc")
@@ -385,6 +588,9 @@ def main():
     stream = torch.cuda.Stream()
     if args.bwd:
         tune_bwd(args, torch, sbp, linear, workloads, stream)
+        return
+    if args.step:
+        tune_step(args, torch, sbp, linear, workloads, stream)
         return
     cases = product_cases([int(c) for c in args.workloads.split(",") if int(c) != 7])
     log("%d distinct local products" % len(cases))
