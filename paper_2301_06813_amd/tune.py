@@ -393,9 +393,11 @@ def _call_key(torch, linear, meta, dtype):
     return ("bwd", pkey("bwd_data"), pkey("bwd_weight"))
 
 
-def _isolated_top(args, torch, sbp, linear, workloads, stream, key, wl, lin, r, top):
+def _isolated_top(args, torch, sbp, linear, workloads, stream, key, wl, lin, r, top, diverse=0):
     """The `top` fastest candidate plans of one step call, timed in isolation
-    (graph replays over rotating input sets, as the table tuner does)."""
+    (graph replays over rotating input sets, as the table tuner does), and
+    up to `diverse` more: the fastest plan of each instance not yet among
+    them."""
     per_set = 2 * (2 * lin.M * lin.K + lin.K * lin.N + 2 * lin.M * lin.N)
     nsets = max(2, min(6, -(-600 * 2 ** 20 // per_set)))
     Lr = linear.layouts_for(lin, wl, r)
@@ -450,7 +452,20 @@ def _isolated_top(args, torch, sbp, linear, workloads, stream, key, wl, lin, r, 
             sbp.sbp_set_plan_override(0, 0, 1)
     del sets
     torch.cuda.empty_cache()
-    return [p for _, p in sorted(timings)[:top]]
+    ranked = [p for _, p in sorted(timings)]
+    out = ranked[:top]
+    if diverse:
+        # plus the fastest plan of every other (tile, kernel) instance, in order
+        def inst(p):
+            return None if p[0] == "sep" else (p[1], p[2], p[4] if p[0] == "fwd" else p[3])
+        seen = {inst(p) for p in out}
+        for p in ranked[top:]:
+            if len(out) >= top + diverse:
+                break
+            if inst(p) is not None and inst(p) not in seen:
+                seen.add(inst(p))
+                out.append(p)
+    return out
 
 
 def _apply(sbp, cand, on):
@@ -531,7 +546,7 @@ def tune_step(args, torch, sbp, linear, workloads, stream):
         i0 = calls_of[k][0]
         m = step.meta[i0]
         cands = _isolated_top(args, torch, sbp, linear, workloads, stream, k, wl, m["lin"], 0,
-                              args.step_top)
+                              args.step_top, args.step_diverse)
         res = {}
         for rnd in range(2):
             trial[0] = None
@@ -575,6 +590,8 @@ def main():
                          "of changed plans to --out)")
     ap.add_argument("--step-workload", type=int, default=5, choices=(5, 8))
     ap.add_argument("--step-top", type=int, default=5)
+    ap.add_argument("--step-diverse", type=int, default=0,
+                    help="also try the fastest plan of up to this many more instances")
     ap.add_argument("--step-reps", type=int, default=30)
     ap.add_argument("--step-gain", type=float, default=0.002)
     args = ap.parse_args()
