@@ -156,6 +156,23 @@ def torch_float32():
     return torch.float32
 
 
+TIMED_REPLAYS = 10
+
+
+def time_replays(torch, g, reps, n=TIMED_REPLAYS):
+    """Per-call time of a graph of `reps` calls: the mean over n replays from
+    one event pair around them all, and each replay's own (events between
+    consecutive replays), in us per call."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record()
+    for i in range(n):
+        g.replay()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) * 1e3 / reps for i in range(n)]
+    return ev[0].elapsed_time(ev[n]) * 1e3 / (n * reps), per
+
+
 def report_workload(cid, ranks, reps):
     """Per-call throughput of workload cid (2: Transformer FFN shard, 3: attention
     projections, 4: VGG head, 6: a Transformer layer under the 3-D rule on a
@@ -200,13 +217,7 @@ def report_workload(cid, ranks, reps):
                             call()
                 g.replay()
                 torch.cuda.synchronize()
-                t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                t0.record()
-                for _ in range(3):
-                    g.replay()
-                t1.record()
-                torch.cuda.synchronize()
-                us = t0.elapsed_time(t1) * 1e3 / (3 * reps)
+                us, per = time_replays(torch, g, reps)
                 ops = ("fwd",) if kind == "fwd" else ("bwd_data", "bwd_weight")
                 prods, fl, by = [], 0.0, 0.0
                 for op in ops:
@@ -220,7 +231,8 @@ def report_workload(cid, ranks, reps):
                     by += 2.0 * (m * k + k * n) + ob * m * n
                 rank = list(r) if wl.mesh else r
                 rows.append({"linear": lin.name, "sig": lin.sig, "rank": rank, "call": kind,
-                             "products": prods, "us": us, "tflops": fl / us / 1e6,
+                             "products": prods, "us": us, "us_stats": step_stats(per),
+                             "tflops": fl / us / 1e6,
                              "pct_of_bf16_peak": 100.0 * fl / us / 1e6 / BF16_PEAK_TFLOPS,
                              "algorithmic_gbs": by / us / 1e3,
                              "roofline_min_us": max(fl / BF16_PEAK_TFLOPS / 1e6,
@@ -299,16 +311,11 @@ def report_attention(r, reps):
                     call()
         g.replay()
         torch.cuda.synchronize()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0.record()
-        for _ in range(3):
-            g.replay()
-        t1.record()
-        torch.cuda.synchronize()
-        us = t0.elapsed_time(t1) * 1e3 / (3 * reps)
+        us, per = time_replays(torch, g, reps)
         fl = sum(2.0 * B * hr * m * n * k for _, m, n, k in prods)
         by = sum(2.0 * B * hr * (m * k + k * n + m * n) for _, m, n, k in prods)
-        rows.append({"call": name, "products": ["%s %dx%dx%d x%d" % (d, m, n, k, B * hr)
+        rows.append({"call": name, "us_stats": step_stats(per),
+                     "products": ["%s %dx%dx%d x%d" % (d, m, n, k, B * hr)
                                                 for d, m, n, k in prods],
                      "us": us, "tflops": fl / us / 1e6,
                      "pct_of_bf16_peak": 100.0 * fl / us / 1e6 / BF16_PEAK_TFLOPS,
