@@ -232,10 +232,14 @@ struct DmaStage {
     static constexpr int BYTES = A_BYTES + B_BYTES;
 };
 
-// Workgroups per compute unit an instance is compiled for: as many as its
-// LDS pipeline allows (160 KB per CU), at most four waves per SIMD, and one
-// for eight-wave groups. The compiler then budgets registers so that many
-// fit (e.g. two 128 x 128 two-stage workgroups, not one).
+// Launch bound of an instance: the minimum number of waves per SIMD the
+// compiler budgets registers for. A four-wave workgroup puts one wave on each
+// SIMD, so for those this is the number of workgroups per compute unit that
+// the LDS pipeline allows (160 KB per CU; e.g. two 128 x 128 two-stage
+// workgroups, not one). Eight-wave (two-group) workgroups get 1: no register
+// limit. (Budgeting the two-stage 128 x 128 two-group instance for two
+// workgroups per CU, 128 registers, made its reduction steps no faster than
+// the four-wave instance's at two per CU, with a higher fixed cost.)
 template <int BM, int BN, int BKD, int NS, int NWAVES, int KG>
 struct Occupancy {
     static constexpr int BY_LDS = 163840 / (NS * DmaStage<BM, BN, BKD, NS>::BYTES);
