@@ -258,6 +258,31 @@ struct StageRow {
     static constexpr int LD = (BM * (BN + 8) * 4 <= BYTES) ? BN + 8 : BN;
 };
 
+// Stores of split partials (the fp32 slices that the split reduction reads
+// after this launch): buffer stores at device scope (sc1), which write
+// through the XCD's L2 instead of leaving dirty lines there. Measured on the
+// 24-layer step (same box, alternating runs): 1.0-1.3 % faster than
+// non-temporal stores; plain or sc0 stores 1.4 % and sc1 with nt 1.5 %
+// slower than sc1, sc0 with sc1 the same. (Final outputs stay
+// non-temporal: sc1 for them made the step 3.6 % slower.) `idx` is the
+// element index from the slice base; a slice is below 2^31 bytes (the
+// workspace bound of every plan).
+#ifndef SBP_PART_CPOL
+#define SBP_PART_CPOL 16   // sc1
+#endif
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t part_rsrc(const void *slice) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(slice), (short)0, 0x7fffffff,
+                                             0x00020000);
+}
+__device__ __forceinline__ void st_part(__amdgpu_buffer_rsrc_t r, int64_t idx, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, (int)(idx * 4), 0,
+                                          SBP_PART_CPOL);
+}
+__device__ __forceinline__ void st_part(__amdgpu_buffer_rsrc_t r, int64_t idx, f32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)(idx * 4), 0,
+                                           SBP_PART_CPOL);
+}
+
 // Stores the BM x BN fp32 tile staged in LDS (`tile`, row stride
 // LD floats) to rows [m0, m0 + BM) x columns [n0, n0 + BN) of C
 // (ld `ldc`, clipped to [0, m) x [0, n); m0 and n0 may be negative in a
@@ -265,8 +290,9 @@ struct StageRow {
 // 16-byte chunks along a row -- 4 floats, or 8 values rounded to bf16 -- so a
 // wave writes whole contiguous row segments. `vec`: C's base and ldc allow
 // aligned 16-byte stores; otherwise (and at the right edge) elements are
-// stored one by one.
-template <int BM, int BN, int LD, int NT_, bool F32, bool ACC = false, bool SHIFT = false>
+// stored one by one. PART: C is a split partial slice (st_part).
+template <int BM, int BN, int LD, int NT_, bool F32, bool ACC = false, bool SHIFT = false,
+          bool PART = false>
 __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t ldc, int m,
                                              int n, int m0, int n0, bool vec, int tid) {
     static_assert(F32 || !ACC, "accumulation needs an fp32 output");
@@ -290,6 +316,8 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
                 if constexpr (ACC) {
                     v += *reinterpret_cast<const f32x4 *>(dst);
                     *reinterpret_cast<f32x4 *>(dst) = v;
+                } else if constexpr (PART) {
+                    st_part(part_rsrc(C), (int64_t)row * ldc + col, v);
                 } else {
                     st_nt(reinterpret_cast<f32x4 *>(dst), v);
                 }
@@ -298,6 +326,7 @@ __device__ __forceinline__ void store_staged(const float *tile, void *C, int64_t
                 for (int e = 0; e < 4; ++e)
                     if (SHIFT ? (unsigned)(col + e) < (unsigned)n : col + e < n) {
                         if constexpr (ACC) dst[e] = dst[e] + v[e];
+                        else if constexpr (PART) st_part(part_rsrc(C), (int64_t)row * ldc + col + e, v[e]);
                         else st_nt(dst + e, v[e]);
                     }
             }
@@ -514,9 +543,12 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
     if constexpr (EPI == EPI_ROWQ) {
         // lane owns row r = lane % 32 of each 32 x 32 block and, for register
         // quad q, columns 8 q + 4 (lane / 32) + 0..3
-        auto store_all = [&](auto f32_tag, auto acc_tag, void *out, int64_t ldo, bool vec) {
+        // part_tag: out is a split partial slice (st_part)
+        auto store_all = [&](auto f32_tag, auto acc_tag, void *out, int64_t ldo, bool vec,
+                             auto part_tag) {
             constexpr bool F32 = decltype(f32_tag)::value;
             constexpr bool ACC = decltype(acc_tag)::value;
+            constexpr bool PART = decltype(part_tag)::value;
 #pragma unroll
             for (int i = 0; i < MI; ++i) {
                 const int row = om0 + wm * WM + i * 32 + (lane & 31);
@@ -535,6 +567,8 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
                                 if constexpr (ACC) {
                                     v += *reinterpret_cast<const f32x4 *>(dst);
                                     *reinterpret_cast<f32x4 *>(dst) = v;
+                                } else if constexpr (PART) {
+                                    st_part(part_rsrc(out), (int64_t)row * ldo + col, v);
                                 } else {
                                     st_nt(reinterpret_cast<f32x4 *>(dst), v);
                                 }
@@ -544,6 +578,9 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
                                     if (inb(col + e, g.n)) {
                                         if constexpr (ACC)
                                             dst[e] = dst[e] + acc[i][j][4 * q + e];
+                                        else if constexpr (PART)
+                                            st_part(part_rsrc(out), (int64_t)row * ldo + col + e,
+                                                    acc[i][j][4 * q + e]);
                                         else
                                             st_nt(dst + e, acc[i][j][4 * q + e]);
                                     }
@@ -570,13 +607,14 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
             }
         };
         if (partial)
-            store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)ldw, ws_vec);
+            store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)ldw, ws_vec,
+                      std::true_type{});
         else if (OUT_F32 && g.accumulate)
             store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
-                      Cb, g.ldc, (bool)g.vec_c4);
+                      Cb, g.ldc, (bool)g.vec_c4, std::false_type{});
         else
             store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, Cb, g.ldc,
-                      (bool)g.vec_c4);
+                      (bool)g.vec_c4, std::false_type{});
         return;
     }
 
@@ -614,7 +652,7 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
         }
         __syncthreads();
         if (partial)
-            store_staged<BM, BN, LD, 64 * NW, true, false, SHIFT>(tile, ws_out, ldw, g.m, g.n,
+            store_staged<BM, BN, LD, 64 * NW, true, false, SHIFT, true>(tile, ws_out, ldw, g.m, g.n,
                                                                   om0, on0, ws_vec, tid);
         else if (OUT_F32 && g.accumulate)
             store_staged<BM, BN, LD, 64 * NW, OUT_F32, OUT_F32, SHIFT>(
@@ -626,9 +664,11 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
         return;
     }
 
-    auto store_all = [&](auto f32_tag, auto acc_tag, void *out, int64_t ldo) {
+    // part_tag: out is a split partial slice (st_part)
+    auto store_all = [&](auto f32_tag, auto acc_tag, void *out, int64_t ldo, auto part_tag) {
         constexpr bool F32 = decltype(f32_tag)::value;
         constexpr bool ACC = decltype(acc_tag)::value;
+        constexpr bool PART = decltype(part_tag)::value;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
 #pragma unroll
@@ -643,7 +683,9 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
                             if constexpr (F32 && ACC) {
                                 float *d = reinterpret_cast<float *>(out) + (int64_t)row * ldo + col;
                                 *d = *d + acc[i][j][r];
-                            } else if constexpr (F32)
+                            } else if constexpr (F32 && PART)
+                                st_part(part_rsrc(out), (int64_t)row * ldo + col, acc[i][j][r]);
+                            else if constexpr (F32)
                                 st_nt(reinterpret_cast<float *>(out) + (int64_t)row * ldo + col,
                                       acc[i][j][r]);
                             else
@@ -656,12 +698,13 @@ __device__ __forceinline__ void dma_tile_body(const Args &g, const int L, char *
         }
     };
     if (partial)
-        store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)ldw);
+        store_all(std::true_type{}, std::false_type{}, ws_out, (int64_t)ldw, std::true_type{});
     else if (OUT_F32 && g.accumulate)
         store_all(std::integral_constant<bool, OUT_F32>{}, std::integral_constant<bool, OUT_F32>{},
-                  Cb, g.ldc);
+                  Cb, g.ldc, std::false_type{});
     else
-        store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, Cb, g.ldc);
+        store_all(std::integral_constant<bool, OUT_F32>{}, std::false_type{}, Cb, g.ldc,
+                  std::false_type{});
 }
 
 
