@@ -281,10 +281,11 @@ __device__ __forceinline__ int remap_xcd(int wg, int total) {
     return (x < rem) ? x * (per + 1) + idx : rem * (per + 1) + (x - rem) * per + idx;
 }
 
-// Store of a GEMM output (or split partial) that this launch does not read
-// back: non-temporal, so the output stream does not displace the operand
-// tiles that other workgroups still re-read from L2 (measured: the step's
-// fp32 partial-sum outputs 10-13 % faster, the whole step 4 %).
+// Store of a GEMM output that this launch does not read back: non-temporal,
+// so the output stream does not displace the operand tiles that other
+// workgroups still re-read from L2 (measured: the step's fp32 partial-sum
+// outputs 10-13 % faster, the whole step 4 %). Split partials take other
+// stores (st_part in the pipelined kernel; ordinary ones in this kernel).
 template <typename T>
 __device__ __forceinline__ void st_nt(T *p, T v) {
     __builtin_nontemporal_store(v, p);
